@@ -1,0 +1,154 @@
+/*
+ * kdn.h -- C ABI of the MI355X (gfx950) Kalman Delta Network hot path.
+ *
+ * Paper: N. Bui, T. Huang, R. Ying, "Kalman Delta Networks: Uncertainty-aware Associative
+ * Memory", arXiv 2609.07816. Section and equation names below are the paper's.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every data pointer is a DEVICE pointer owned by the caller. The library allocates no device
+ *   memory and never frees caller memory.
+ * - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL = the null stream).
+ *   No call synchronizes the stream or reads device memory from the host. A status other than
+ *   KDN_OK means nothing was launched (argument errors) or a launch failed (KDN_ERR_HIP); the
+ *   outputs are then unspecified.
+ * - Layouts are contiguous row-major "BTHD": q, k [B,T,H,dk]; v, o [B,T,H,dv]; per-channel gates
+ *   [B,T,H,dk]; per-head scalars [B,T,H]. Variable-length batches are packed: B == 1, T is the
+ *   total token count, and cu_seqlens (int32 [N+1], device) gives sequence n the tokens
+ *   [cu_seqlens[n], cu_seqlens[n+1]). Without cu_seqlens, N == B and every row has length T.
+ * - `dtype` is the storage type of q, k, v, alpha, omega, r and o (KDN_F32 or KDN_BF16). The
+ *   recurrent state is always float32: S [N,H,dk,dv] (key-major, S[i][j] at i*dv + j);
+ *   P [N,H,dk] for the diagonal variant, [N,H] for the isotropic one.
+ * - S0 == NULL means S0 = 0; P0 == NULL means P0 = 1 (p_0 = 1, b_0 = 1). S_T / P_T may be NULL
+ *   (not written) and may alias S0 / P0 exactly (in-place state update).
+ * - Supported head sizes: dk, dv in {16, 32, 64, 128}.
+ * - Device-side contract (not checked on the host, which never reads device data):
+ *   cu_seqlens non-decreasing with cu_seqlens[0] == 0 and cu_seqlens[N] == T; 0 < alpha <= 1;
+ *   omega >= 0; r > 0. Kernels never write outside the caller's buffers even when it is broken.
+ * - Errors are returned, never printed or raised; kdn_last_error() gives detail for the calling
+ *   thread's most recent non-OK status.
+ */
+#ifndef KDN_H
+#define KDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KDN_OK = 0,
+    KDN_ERR_INVALID_ARG = 1, /* null required pointer, bad size, mu <= 0, scale <= 0, aliasing */
+    KDN_ERR_UNSUPPORTED = 2, /* dk or dv outside {16, 32, 64, 128}, or an unsupported chunk   */
+    KDN_ERR_WORKSPACE = 3,   /* workspace smaller than the matching *_workspace_bytes query    */
+    KDN_ERR_HIP = 4          /* a HIP launch failed; kdn_last_error() carries the HIP message  */
+} kdn_status_t;
+
+typedef enum { KDN_F32 = 0, KDN_BF16 = 1 } kdn_dtype_t;
+
+/*
+ * Diagonal KDN forward (Prop. "Diagonal Kalman Delta Network", eqs. kla-box-mobius,
+ * kla-box-gain, kla-box-memory; variance update eqs. prefix-diag-uncertainty and
+ * diag-cov-update with information scale mu). For every token of every (sequence, head):
+ *   p_hat = alpha^2 * p + omega;  kappa = p_hat * k / (r + sum_i p_hat_i k_i^2)
+ *   S = diag(alpha) S + kappa (v - (diag(alpha) S)^T k)^T;  o = scale * S^T q
+ *   p = p_hat / (1 + mu k^2 / r * p_hat)
+ * evaluated chunkwise (App. "Hardware-Efficient Chunkwise Algorithm").
+ *   q, k, alpha, omega: [B,T,H,dk]; v, o: [B,T,H,dv]; r: [B,T,H]   (dtype)
+ *   S0, S_T: [N,H,dk,dv] float32;  P0, P_T: [N,H,dk] float32
+ *   mu > 0 (the paper uses mu = dk); scale > 0 (the paper uses dk^-1/2).
+ *   chunk: memory-chunk length (16, 32 or 64), or 0 for the library's choice. Results do not
+ *   depend on it beyond rounding.
+ *   workspace: device scratch of kdn_forward_workspace_bytes(...) bytes (may be NULL when that
+ *   query returns 0).
+ */
+kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const void* alpha,
+                              const void* omega, const void* r, const float* S0, const float* P0,
+                              void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                              int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                              kdn_dtype_t dtype, float mu, float scale, int32_t chunk,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Isotropic KDN forward (Prop. "Isotropic Kalman Delta Network", eqs.
+ * iso-kla-box-cov-update, iso-kla-box-gain, iso-kla-box-memory). One variance b per head:
+ *   a = mean_i alpha_i^2;  b_hat = a b + omega;  beta = b_hat / (r + b_hat ||k||^2)
+ *   S = diag(alpha) S + beta k (v - (diag(alpha) S)^T k)^T;  o = scale * S^T q
+ *   b = b_hat / (1 + mu ||k||^2 / (dk r) * b_hat)
+ *   alpha: [B,T,H,dk] when alpha_per_channel != 0, else [B,T,H] (one gate per head);
+ *   omega, r: [B,T,H]; P0, P_T: [N,H] float32. Other arguments as kdn_forward_diag.
+ */
+kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* omega, const void* r, const float* S0, const float* P0,
+                             void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                             int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
+                             int32_t chunk, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* Device scratch (bytes) the forward needs for these sizes; variant 0 = diagonal, 1 = iso.  */
+size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                   int32_t dk, int32_t dv);
+
+/*
+ * One recurrent decode step: exactly one token of the forward recurrence per row, with the
+ * state resident in a slot pool and updated in place (the paper's constant-memory decoding;
+ * Prop. "Diagonal Kalman Delta Network" / Prop. "Isotropic Kalman Delta Network" for T = 1).
+ *   variant: 0 = diagonal, 1 = isotropic
+ *   q, k: [R,H,dk]; v, o: [R,H,dv]; alpha: [R,H,dk] (diagonal, or isotropic with
+ *   alpha_per_channel) or [R,H]; omega: [R,H,dk] (diagonal) or [R,H]; r: [R,H]   (dtype)
+ *   S: [num_slots,H,dk,dv] float32, P: [num_slots,H,dk] (diag) / [num_slots,H] (iso) float32
+ *   slot_idx: int32 [R] (device) or NULL (row i uses slot i, needs R <= num_slots). A negative
+ *   slot skips the row: its o row and every state slot are left untouched. Two rows naming
+ *   the same slot race (undefined result). Slots >= num_slots are skipped the same way.
+ */
+kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, const void* v,
+                             const void* alpha, const void* omega, const void* r, float* S,
+                             float* P, const int32_t* slot_idx, void* o, int32_t R,
+                             int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
+                             void* stream);
+
+/*
+ * Gain scan alone (App. "Hardware-Efficient Chunkwise Algorithm", Sec. "Chunkwise Gain
+ * Computation", eqs. chunk-gain-summary, chunk-gain-carry, chunk-gain-local-prefix,
+ * chunk-gain-emission): the variance recurrence run as a log-depth associative scan of 2x2
+ * Moebius matrices, emitting the pre-write gain of every token and the final variances.
+ *   Diagonal: kappa_out [B,T,H,dk] float32 (kappa_t), phat_out [B,T,H,dk] float32 or NULL
+ *   (p_hat_t), P_T [N,H,dk] float32 or NULL.
+ *   Isotropic: beta_out [B,T,H] float32 (beta_t), bhat_out [B,T,H] or NULL, P_T [N,H] or NULL.
+ *   Inputs as in the forward (v, q are not needed). workspace: kdn_gain_workspace_bytes(...).
+ */
+kdn_status_t kdn_gain_diag(const void* k, const void* alpha, const void* omega, const void* r,
+                           const float* P0, float* kappa_out, float* phat_out, float* P_T,
+                           const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T,
+                           int32_t H, int32_t dk, kdn_dtype_t dtype, float mu, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+kdn_status_t kdn_gain_iso(const void* k, const void* alpha, const void* omega, const void* r,
+                          const float* P0, float* beta_out, float* bhat_out, float* P_T,
+                          const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T, int32_t H,
+                          int32_t dk, kdn_dtype_t dtype, int32_t alpha_per_channel, float mu,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Device scratch (bytes) the gain scan needs; variant 0 = diagonal, 1 = isotropic.           */
+size_t kdn_gain_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                int32_t dk);
+
+/* Static text for a status code.                                                             */
+const char* kdn_status_string(kdn_status_t status);
+
+/* Detail of the calling thread's most recent non-OK status ("" if none). Valid until the next
+ * library call on the same thread.                                                            */
+const char* kdn_last_error(void);
+
+/* Library version string.                                                                     */
+const char* kdn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KDN_H */

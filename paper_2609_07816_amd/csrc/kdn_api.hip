@@ -1,0 +1,267 @@
+// C ABI of libkdn: host-side argument checks and dispatch to the HIP launchers.
+// Nothing here reads device memory or synchronizes; every check uses host-visible sizes only.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "kdn_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+kdn_status_t fail(kdn_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+
+kdn_status_t fail(kdn_status_t st, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+kdn_status_t ok()
+{
+    g_err[0] = '\0';
+    return KDN_OK;
+}
+
+bool head_ok(int d) { return d == 16 || d == 32 || d == 64 || d == 128; }
+
+size_t esize(kdn_dtype_t dt) { return dt == KDN_F32 ? 4 : 2; }
+
+// Byte ranges [p, p + n) and [q, q + m) overlap.
+bool overlaps(const void* p, size_t n, const void* q, size_t m)
+{
+    if (!p || !q || n == 0 || m == 0) return false;
+    const char *a = (const char*)p, *b = (const char*)q;
+    return a < b + m && b < a + n;
+}
+
+kdn_status_t hip_status(hipError_t e, const char* what)
+{
+    if (e == hipSuccess) return ok();
+    return fail(KDN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Shared validation of the forward / gain argument sets.
+kdn_status_t check_seq(const int32_t* cu, int32_t N, int32_t B, int32_t T, int32_t H)
+{
+    if (B <= 0 || T <= 0 || H <= 0 || N <= 0)
+        return fail(KDN_ERR_INVALID_ARG, "sizes must be positive (N=%d B=%d T=%d H=%d)", N, B,
+                    T, H);
+    if (cu && B != 1)
+        return fail(KDN_ERR_INVALID_ARG, "packed batches (cu_seqlens) need B == 1, got %d", B);
+    if (!cu && N != B)
+        return fail(KDN_ERR_INVALID_ARG, "without cu_seqlens N must equal B (N=%d B=%d)", N, B);
+    if ((int64_t)B * T * H > ((int64_t)1 << 31) / 128)
+        return fail(KDN_ERR_INVALID_ARG, "B*T*H too large for 32-bit token indexing");
+    return KDN_OK;
+}
+
+kdn_status_t check_forward(int variant, const void* q, const void* k, const void* v,
+                           const void* alpha, const void* omega, const void* r, const float* S0,
+                           const float* P0, const void* o, const float* S_T, const float* P_T,
+                           const int32_t* cu, int32_t N, int32_t B, int32_t T, int32_t H,
+                           int32_t dk, int32_t dv, kdn_dtype_t dtype, int apc, float mu,
+                           float scale, int32_t chunk, void* ws, size_t ws_bytes)
+{
+    if (!q || !k || !v || !alpha || !omega || !r || !o)
+        return fail(KDN_ERR_INVALID_ARG, "null required pointer (q, k, v, alpha, omega, r, o)");
+    if (dtype != KDN_F32 && dtype != KDN_BF16)
+        return fail(KDN_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    kdn_status_t st = check_seq(cu, N, B, T, H);
+    if (st != KDN_OK) return st;
+    if (!head_ok(dk) || !head_ok(dv))
+        return fail(KDN_ERR_UNSUPPORTED, "dk=%d dv=%d: head sizes must be 16, 32, 64 or 128", dk,
+                    dv);
+    if (!(mu > 0.f) || !(scale > 0.f))
+        return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
+                    scale);
+    if (chunk != 0 && !kdn::forward_chunk_supported(dtype, dk, dv, chunk))
+        return fail(KDN_ERR_UNSUPPORTED, "chunk=%d does not fit one workgroup's LDS for this "
+                    "dtype, dk=%d and dv=%d (use 0 for the largest that fits)", chunk, dk, dv);
+    const size_t ntok = (size_t)B * T * H, es = esize(dtype);
+    const size_t nk = ntok * dk * es, nv = ntok * dv * es;
+    const size_t na = (variant == 0 || apc) ? nk : ntok * es;
+    const size_t nw = variant == 0 ? nk : ntok * es;
+    const void* ins[6] = {q, k, v, alpha, omega, r};
+    const size_t insz[6] = {nk, nk, nv, na, nw, ntok * es};
+    for (int i = 0; i < 6; ++i)
+        if (overlaps(o, nv, ins[i], insz[i]))
+            return fail(KDN_ERR_INVALID_ARG, "output o overlaps input %d", i);
+    const size_t ns = (size_t)N * H * dk * dv * 4;
+    const size_t np = (size_t)N * H * (variant == 0 ? dk : 1) * 4;
+    if (S_T && S_T != S0 && overlaps(S_T, ns, S0, ns))
+        return fail(KDN_ERR_INVALID_ARG, "S_T partially overlaps S0 (only exact aliasing is "
+                                         "allowed)");
+    if (P_T && P_T != P0 && overlaps(P_T, np, P0, np))
+        return fail(KDN_ERR_INVALID_ARG, "P_T partially overlaps P0");
+    if (overlaps(o, nv, S_T, ns) || overlaps(o, nv, P_T, np))
+        return fail(KDN_ERR_INVALID_ARG, "o overlaps the state outputs");
+    const size_t need = kdn::forward_workspace_bytes(variant, N, B, T, H, dk, dv);
+    if (need > 0 && (!ws || ws_bytes < need))
+        return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : (size_t)0);
+    return KDN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kdn_status_string(kdn_status_t s)
+{
+    switch (s) {
+    case KDN_OK: return "KDN_OK";
+    case KDN_ERR_INVALID_ARG: return "KDN_ERR_INVALID_ARG";
+    case KDN_ERR_UNSUPPORTED: return "KDN_ERR_UNSUPPORTED";
+    case KDN_ERR_WORKSPACE: return "KDN_ERR_WORKSPACE";
+    case KDN_ERR_HIP: return "KDN_ERR_HIP";
+    }
+    return "KDN_ERR_UNKNOWN";
+}
+
+const char* kdn_last_error(void) { return g_err; }
+
+const char* kdn_version(void) { return "kdn-mi355x 0.1 (gfx950)"; }
+
+size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                   int32_t dk, int32_t dv)
+{
+    if (N <= 0 || B <= 0 || T <= 0 || H <= 0) return 0;
+    return kdn::forward_workspace_bytes(variant, N, B, T, H, dk, dv);
+}
+
+size_t kdn_gain_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                int32_t dk)
+{
+    if (N <= 0 || B <= 0 || T <= 0 || H <= 0) return 0;
+    return kdn::gain_workspace_bytes(variant, N, B, T, H, dk);
+}
+
+kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const void* alpha,
+                              const void* omega, const void* r, const float* S0, const float* P0,
+                              void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                              int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                              kdn_dtype_t dtype, float mu, float scale, int32_t chunk,
+                              void* workspace, size_t workspace_bytes, void* stream)
+{
+    kdn_status_t st = check_forward(0, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, cu_seqlens,
+                                    N, B, T, H, dk, dv, dtype, 1, mu, scale, chunk, workspace,
+                                    workspace_bytes);
+    if (st != KDN_OK) return st;
+    kdn::SeqArgs sa = {cu_seqlens, N, B, T, H};
+    return hip_status(kdn::launch_forward(0, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, sa,
+                                          dk, dv, dtype, 1, mu, scale, chunk, workspace,
+                                          (hipStream_t)stream),
+                      "kdn_forward_diag launch");
+}
+
+kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* omega, const void* r, const float* S0, const float* P0,
+                             void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                             int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
+                             int32_t chunk, void* workspace, size_t workspace_bytes,
+                             void* stream)
+{
+    const int apc = alpha_per_channel ? 1 : 0;
+    kdn_status_t st = check_forward(1, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, cu_seqlens,
+                                    N, B, T, H, dk, dv, dtype, apc, mu, scale, chunk, workspace,
+                                    workspace_bytes);
+    if (st != KDN_OK) return st;
+    kdn::SeqArgs sa = {cu_seqlens, N, B, T, H};
+    return hip_status(kdn::launch_forward(1, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, sa,
+                                          dk, dv, dtype, apc, mu, scale, chunk, workspace,
+                                          (hipStream_t)stream),
+                      "kdn_forward_iso launch");
+}
+
+kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, const void* v,
+                             const void* alpha, const void* omega, const void* r, float* S,
+                             float* P, const int32_t* slot_idx, void* o, int32_t R,
+                             int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
+                             void* stream)
+{
+    if (variant != 0 && variant != 1)
+        return fail(KDN_ERR_INVALID_ARG, "variant must be 0 (diagonal) or 1 (isotropic)");
+    if (!q || !k || !v || !alpha || !omega || !r || !S || !P || !o)
+        return fail(KDN_ERR_INVALID_ARG, "null required pointer");
+    if (dtype != KDN_F32 && dtype != KDN_BF16)
+        return fail(KDN_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if (R < 0 || num_slots <= 0 || H <= 0)
+        return fail(KDN_ERR_INVALID_ARG, "bad sizes (R=%d num_slots=%d H=%d)", R, num_slots, H);
+    if (!slot_idx && R > num_slots)
+        return fail(KDN_ERR_INVALID_ARG, "without slot_idx R (%d) must not exceed num_slots (%d)",
+                    R, num_slots);
+    if (!head_ok(dk) || !head_ok(dv))
+        return fail(KDN_ERR_UNSUPPORTED, "dk=%d dv=%d: head sizes must be 16, 32, 64 or 128", dk,
+                    dv);
+    if (!(mu > 0.f) || !(scale > 0.f))
+        return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive");
+    const size_t es = esize(dtype), rows = (size_t)R * H;
+    const size_t ns = (size_t)num_slots * H * dk * dv * 4;
+    const size_t np = (size_t)num_slots * H * (variant == 0 ? dk : 1) * 4;
+    const void* ins[6] = {q, k, v, alpha, omega, r};
+    for (int i = 0; i < 6; ++i)
+        if (overlaps(o, rows * dv * es, ins[i], rows * es))
+            return fail(KDN_ERR_INVALID_ARG, "output o overlaps input %d", i);
+    if (overlaps(o, rows * dv * es, S, ns) || overlaps(o, rows * dv * es, P, np) ||
+        overlaps(S, ns, P, np))
+        return fail(KDN_ERR_INVALID_ARG, "o, S and P must not overlap");
+    return hip_status(kdn::launch_decode(variant, q, k, v, alpha, omega, r, S, P, slot_idx, o, R,
+                                         num_slots, H, dk, dv, dtype,
+                                         alpha_per_channel ? 1 : 0, mu, scale,
+                                         (hipStream_t)stream),
+                      "kdn_decode_step launch");
+}
+
+static kdn_status_t gain_common(int variant, const void* k, const void* alpha, const void* omega,
+                                const void* r, const float* P0, float* gain_out, float* phat_out,
+                                float* P_T, const int32_t* cu, int32_t N, int32_t B, int32_t T,
+                                int32_t H, int32_t dk, kdn_dtype_t dtype, int apc, float mu,
+                                void* ws, size_t ws_bytes, void* stream)
+{
+    if (!k || !alpha || !omega || !r || !gain_out)
+        return fail(KDN_ERR_INVALID_ARG, "null required pointer (k, alpha, omega, r, gain)");
+    if (dtype != KDN_F32 && dtype != KDN_BF16)
+        return fail(KDN_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    kdn_status_t st = check_seq(cu, N, B, T, H);
+    if (st != KDN_OK) return st;
+    if (!head_ok(dk)) return fail(KDN_ERR_UNSUPPORTED, "dk=%d: must be 16, 32, 64 or 128", dk);
+    if (!(mu > 0.f)) return fail(KDN_ERR_INVALID_ARG, "mu must be positive (mu=%g)", mu);
+    const size_t need = kdn::gain_workspace_bytes(variant, N, B, T, H, dk);
+    if (!ws || ws_bytes < need)
+        return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : (size_t)0);
+    kdn::SeqArgs sa = {cu, N, B, T, H};
+    return hip_status(kdn::launch_gain(variant, k, alpha, omega, r, P0, gain_out, phat_out, P_T,
+                                       sa, dk, dtype, apc, mu, ws, (hipStream_t)stream),
+                      "kdn_gain launch");
+}
+
+kdn_status_t kdn_gain_diag(const void* k, const void* alpha, const void* omega, const void* r,
+                           const float* P0, float* kappa_out, float* phat_out, float* P_T,
+                           const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T,
+                           int32_t H, int32_t dk, kdn_dtype_t dtype, float mu, void* workspace,
+                           size_t workspace_bytes, void* stream)
+{
+    return gain_common(0, k, alpha, omega, r, P0, kappa_out, phat_out, P_T, cu_seqlens, N, B, T,
+                       H, dk, dtype, 1, mu, workspace, workspace_bytes, stream);
+}
+
+kdn_status_t kdn_gain_iso(const void* k, const void* alpha, const void* omega, const void* r,
+                          const float* P0, float* beta_out, float* bhat_out, float* P_T,
+                          const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T, int32_t H,
+                          int32_t dk, kdn_dtype_t dtype, int32_t alpha_per_channel, float mu,
+                          void* workspace, size_t workspace_bytes, void* stream)
+{
+    return gain_common(1, k, alpha, omega, r, P0, beta_out, bhat_out, P_T, cu_seqlens, N, B, T,
+                       H, dk, dtype, alpha_per_channel ? 1 : 0, mu, workspace, workspace_bytes,
+                       stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// Internal declarations shared by the HIP sources of libkdn (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "kdn.h"
+
+namespace kdn {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------------------------------
+// element access: inputs are float32 or bf16, computed in float32
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+
+template <class T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+template <class T>
+__device__ __forceinline__ float ldf(const T* p, size_t i) { return to_f32(p[i]); }
+
+// ------------------------------------------------------------------------------------------
+// wavefront reductions (64 lanes)
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float x)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+    return x;
+}
+
+// Power-of-two rescale of a homogeneous pair (n, d): exact, keeps n/d, keeps max(|n|,|d|) in
+// [0.5, 1). The Moebius states and summaries are only defined up to a positive factor.
+__device__ __forceinline__ void renorm2(float& n, float& d)
+{
+    float m = fmaxf(fabsf(n), fabsf(d));
+    int e;
+    (void)frexpf(m, &e);
+    if (m > 0.f && m < INFINITY) {
+        n = ldexpf(n, -e);
+        d = ldexpf(d, -e);
+    }
+}
+
+__device__ __forceinline__ void renorm4(float& a, float& b, float& c, float& d)
+{
+    float m = fmaxf(fmaxf(fabsf(a), fabsf(b)), fmaxf(fabsf(c), fabsf(d)));
+    int e;
+    (void)frexpf(m, &e);
+    if (m > 0.f && m < INFINITY) {
+        a = ldexpf(a, -e);
+        b = ldexpf(b, -e);
+        c = ldexpf(c, -e);
+        d = ldexpf(d, -e);
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// host-side launchers implemented in the kernel sources
+// ------------------------------------------------------------------------------------------
+struct SeqArgs {
+    const int32_t* cu_seqlens;  // device, or nullptr
+    int N, B, T, H;
+};
+
+hipError_t launch_decode(int variant, const void* q, const void* k, const void* v,
+                         const void* alpha, const void* omega, const void* r, float* S, float* P,
+                         const int32_t* slot_idx, void* o, int R, int num_slots, int H, int dk,
+                         int dv, kdn_dtype_t dtype, int alpha_per_channel, float mu, float scale,
+                         hipStream_t stream);
+
+size_t gain_workspace_bytes(int variant, int N, int B, int T, int H, int dk);
+hipError_t launch_gain(int variant, const void* k, const void* alpha, const void* omega,
+                       const void* r, const float* P0, float* gain_out, float* phat_out,
+                       float* P_T, const SeqArgs& sa, int dk, kdn_dtype_t dtype,
+                       int alpha_per_channel, float mu, void* workspace, hipStream_t stream);
+
+int forward_default_chunk(kdn_dtype_t dtype, int dk, int dv);
+bool forward_chunk_supported(kdn_dtype_t dtype, int dk, int dv, int chunk);
+size_t forward_workspace_bytes(int variant, int N, int B, int T, int H, int dk, int dv);
+hipError_t launch_forward(int variant, const void* q, const void* k, const void* v,
+                          const void* alpha, const void* omega, const void* r, const float* S0,
+                          const float* P0, void* o, float* S_T, float* P_T, const SeqArgs& sa,
+                          int dk, int dv, kdn_dtype_t dtype, int alpha_per_channel, float mu,
+                          float scale, int chunk, void* workspace, hipStream_t stream);
+
+}  // namespace kdn

@@ -1,0 +1,102 @@
+"""The C ABI on the host (no GPU): the library loads, exports every entry point declared in
+include/kdn.h, and rejects bad arguments with the documented status before touching a device."""
+
+import ctypes
+
+import pytest
+
+from paper_2609_07816_amd import kdn
+
+F = ctypes.c_float
+
+
+@pytest.fixture(scope="module")
+def L():
+    return kdn.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = kdn.declared_symbols()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(L, name), f"{name} declared in include/kdn.h but not exported"
+
+
+def test_status_strings(L):
+    for code, name in enumerate(["KDN_OK", "KDN_ERR_INVALID_ARG", "KDN_ERR_UNSUPPORTED",
+                                 "KDN_ERR_WORKSPACE", "KDN_ERR_HIP"]):
+        assert L.kdn_status_string(code).decode() == name
+    assert L.kdn_version().decode().startswith("kdn-mi355x")
+
+
+# fake, never-dereferenced device addresses: argument checks run before any launch
+def P(i):
+    return ctypes.c_void_p(0x1000000 * (i + 1))
+
+
+def fwd(L, variant=0, ptrs=None, N=1, B=1, T=8, H=2, dk=64, dv=64, dtype=1, mu=64.0,
+        scale=0.125, chunk=0, cu=None, S0=None, S_T=None, P0=None, P_T=None):
+    p = [P(i) for i in range(7)] if ptrs is None else ptrs
+    args = p[:6] + [S0, P0, p[6], S_T, P_T, cu, N, B, T, H, dk, dv, dtype]
+    if variant == 0:
+        return L.kdn_forward_diag(*args, F(mu), F(scale), chunk, None, 0, None)
+    return L.kdn_forward_iso(*args, 1, F(mu), F(scale), chunk, None, 0, None)
+
+
+@pytest.mark.parametrize("variant", [0, 1])
+def test_forward_argument_errors(L, variant):
+    assert fwd(L, variant, ptrs=[None] + [P(i) for i in range(6)]) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, T=0) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, N=2, B=1) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, cu=P(20), N=2, B=2) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, mu=0.0) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, mu=-1.0) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, scale=0.0) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, dtype=7) == kdn.KDN_ERR_INVALID_ARG
+    assert fwd(L, variant, dk=48) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, dv=256) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, chunk=24) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, dtype=0, dk=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, dtype=0, dk=64, dv=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
+    # output aliasing an input
+    p = [P(i) for i in range(7)]
+    p[6] = p[2]
+    assert fwd(L, variant, ptrs=p) == kdn.KDN_ERR_INVALID_ARG
+    # partial overlap of the state output with the state input
+    base = 0x7000000
+    assert fwd(L, variant, S0=ctypes.c_void_p(base), S_T=ctypes.c_void_p(base + 64)) \
+        == kdn.KDN_ERR_INVALID_ARG
+    assert "S_T" in L.kdn_last_error().decode()
+
+
+def test_decode_argument_errors(L):
+    p = [P(i) for i in range(9)]
+
+    def dec(variant=0, ptrs=p, slot=None, o=P(10), R=4, slots=4, H=2, dk=64, dv=64, dtype=1):
+        return L.kdn_decode_step(variant, *ptrs[:6], ptrs[6], ptrs[7], slot, o, R, slots, H,
+                                 dk, dv, dtype, 1, F(64.0), F(0.125), None)
+
+    assert dec(variant=2) == kdn.KDN_ERR_INVALID_ARG
+    assert dec(o=None) == kdn.KDN_ERR_INVALID_ARG
+    assert dec(R=5, slots=4) == kdn.KDN_ERR_INVALID_ARG        # no slot map, too many rows
+    assert dec(dk=8) == kdn.KDN_ERR_UNSUPPORTED
+    assert dec(o=p[0]) == kdn.KDN_ERR_INVALID_ARG              # o aliases q
+
+
+def test_gain_argument_errors(L):
+    p = [P(i) for i in range(5)]
+    st = L.kdn_gain_diag(*p[:4], None, p[4], None, None, None, 1, 1, 8, 2, 64, 1, F(64.0), None,
+                         0, None)
+    assert st == kdn.KDN_ERR_WORKSPACE
+    need = L.kdn_gain_workspace_bytes(0, 1, 1, 8, 2, 64)
+    assert need > 0
+    st = L.kdn_gain_diag(*p[:4], None, p[4], None, None, None, 1, 1, 8, 2, 64, 1, F(-1.0),
+                         P(30), need, None)
+    assert st == kdn.KDN_ERR_INVALID_ARG
+
+
+def test_workspace_queries(L):
+    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128) == 0
+    small = L.kdn_gain_workspace_bytes(0, 1, 1, 64, 1, 128)
+    big = L.kdn_gain_workspace_bytes(0, 4, 4, 4096, 16, 128)
+    assert big > small > 0

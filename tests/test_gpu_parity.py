@@ -1,0 +1,259 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle on identical seeded
+inputs. Bounds: relative L2 error <= 1e-5 for float32 inputs and <= 2e-2 for bf16 inputs, over
+o, S_T and P_T (gains: <= 1e-5, they are float32 arithmetic on identical inputs).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (NAMES, TOL, dev_tensor, host_f64, rel_l2, run_gpu_forward,
+                      run_oracle_forward, run_oracle_packed_seq, to_device)
+from paper_2609_07816_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2609_07816_amd import kdn
+    kdn.lib()  # fail loudly when the library is missing
+
+
+def check(name, got, ref, tol):
+    err = rel_l2(got, ref)
+    print(f"  {name}: rel-L2 {err:.3e} (bound {tol:g})", flush=True)
+    assert np.all(np.isfinite(got)), f"{name} has non-finite values"
+    assert err <= tol, f"{name}: rel-L2 {err:.3e} > {tol:g}"
+
+
+def compare_forward(x, chunk=0, tol=None):
+    tol = TOL[x.dtype] if tol is None else tol
+    o, S, P = run_gpu_forward(x, chunk)
+    ref = run_oracle_forward(x)
+    check("o", o, ref["o"], tol)
+    check("S_T", S, ref["S_T"], tol)
+    check("P_T", P, ref["P_T"], tol)
+
+
+# ---------------------------------------------------------------------------------------------
+# workload 0 and small multi-chunk cases
+# ---------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
+@pytest.mark.parametrize("chunk", [16, 0])
+def test_forward_tiny_f32(variant, apc, chunk):
+    compare_forward(W.draw_workload(0, variant, apc), chunk)
+
+
+@pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
+@pytest.mark.parametrize("chunk", [16, 32, 64])
+def test_forward_f32_multichunk_ragged(variant, apc, chunk):
+    x = W.draw_inputs(variant, "f32", 2, 150, 3, 32, 32, seed=41, alpha_per_channel=apc,
+                      random_state=True)
+    compare_forward(x, chunk)
+
+
+@pytest.mark.parametrize("dk,dv,chunk", [(128, 64, 32), (64, 128, 32), (16, 128, 16),
+                                         (32, 16, 64)])
+def test_forward_f32_head_sizes(dk, dv, chunk):
+    x = W.draw_inputs("diag", "f32", 1, 100, 2, dk, dv, seed=42, random_state=True)
+    compare_forward(x, chunk)
+
+
+@pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
+def test_forward_bf16_ragged(variant, apc):
+    x = W.draw_inputs(variant, "bf16", 2, 200, 2, 128, 128, seed=43, alpha_per_channel=apc)
+    compare_forward(x)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("variant", ["diag", "iso"])
+def test_forward_packed_ragged(variant, dtype):
+    lens = [1, 63, 64, 0, 65, 130, 7]
+    d = 32 if dtype == "f32" else 128
+    x = W.draw_inputs(variant, dtype, 1, sum(lens), 2, d, d, seed=44, lengths=lens,
+                      random_state=True)
+    compare_forward(x)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_chunk_size_independence(dtype):
+    d = 64
+    x = W.draw_inputs("diag", dtype, 1, 256, 2, d, d, seed=45, random_state=True)
+    chunks = (16, 32, 64) if dtype == "bf16" else (16, 32)  # float32 d=64 fits up to 32
+    outs = [run_gpu_forward(x, c) for c in chunks]
+    for o, S, P in outs[1:]:
+        check("o vs chunk 16", o, outs[0][0], TOL[dtype])
+        check("S vs chunk 16", S, outs[0][1], TOL[dtype])
+
+
+def test_determinism_bitwise():
+    x = W.draw_inputs("diag", "bf16", 2, 300, 2, 128, 128, seed=46)
+    a = run_gpu_forward(x)
+    for _ in range(3):
+        b = run_gpu_forward(x)
+        for u, w in zip(a, b):
+            assert np.array_equal(u, w)
+
+
+# ---------------------------------------------------------------------------------------------
+# gain scan alone
+# ---------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
+@pytest.mark.parametrize("packed", [False, True])
+def test_gain_scan(variant, apc, dtype, packed):
+    from paper_2609_07816_amd import kdn
+    if packed:
+        lens = [5, 64, 200, 0, 129]
+        x = W.draw_inputs(variant, dtype, 1, sum(lens), 3, 64, 64, seed=47, lengths=lens,
+                          alpha_per_channel=apc, random_state=True)
+    else:
+        x = W.draw_inputs(variant, dtype, 2, 300, 3, 64, 64, seed=47, alpha_per_channel=apc,
+                          random_state=True)
+    d = to_device(x)
+    f = kdn.gain_diag if variant == "diag" else kdn.gain_iso
+    g, ph, P = f(d["k"], d["alpha"], d["omega"], d["r"], P0=d["P0"], cu_seqlens=d["cu"],
+                 mu=x.mu)
+    torch.cuda.synchronize()
+    ref = run_oracle_forward(x, traces=True)
+    gname, pname = ("kappa", "phat") if variant == "diag" else ("beta", "bhat")
+    check(gname, host_f64(g), ref[gname], 1e-5)
+    check(pname, host_f64(ph), ref[pname], 1e-5)
+    check("P_T", host_f64(P), ref["P_T"], 1e-5)
+
+
+# ---------------------------------------------------------------------------------------------
+# decode
+# ---------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
+@pytest.mark.parametrize("d", [16, 128])
+def test_decode_steps(variant, apc, dtype, d):
+    from paper_2609_07816_amd import kdn
+    R, H, slots, steps = 5, 3, 7, 6
+    g = np.random.default_rng([48, d])
+    S = (0.1 * g.standard_normal((slots, H, d, d))).astype(np.float32)
+    P = g.uniform(0.1, 1.0, (slots, H, d) if variant == "diag" else (slots, H)).astype(np.float32)
+    slot_idx = np.array([6, 0, -1, 3, 2], dtype=np.int32)
+    S_ref, P_ref = S.astype(np.float64), P.astype(np.float64)
+    S_dev, P_dev = torch.from_numpy(S).cuda(), torch.from_numpy(P).cuda()
+    si = torch.from_numpy(slot_idx).cuda()
+    o_prev = None
+    for step in range(steps):
+        x = W.draw_inputs(variant, dtype, R, 1, H, d, d, seed=49, stream=100 + step,
+                          alpha_per_channel=apc)
+        dd = to_device(x)
+        o_dev = torch.zeros((R, H, d), dtype=dd["k"].dtype, device="cuda")
+        kdn.decode_step(variant, *[dd[n][:, 0].contiguous() for n in NAMES], S_dev, P_dev,
+                        slot_idx=si, mu=x.mu, scale=x.scale, o=o_dev)
+        o_ref = oracle.decode_step(variant, *[x.f64(n)[:, 0] for n in NAMES], S_ref, P_ref,
+                                   slot_idx=slot_idx, mu=x.mu, scale=x.scale)
+        torch.cuda.synchronize()
+        o = host_f64(o_dev)
+        check(f"o step {step}", o, o_ref, TOL[dtype])
+        assert np.all(o[2] == 0.0), "skipped row must be left untouched"
+    check("S", host_f64(S_dev), S_ref, TOL[dtype])
+    check("P", host_f64(P_dev), P_ref, TOL[dtype])
+    untouched = [1, 4, 5]
+    assert np.array_equal(host_f64(S_dev)[untouched], S.astype(np.float64)[untouched])
+
+
+@pytest.mark.parametrize("variant", ["diag", "iso"])
+def test_decode_chain_equals_forward(variant):
+    from paper_2609_07816_amd import kdn
+    x = W.draw_inputs(variant, "f32", 3, 40, 2, 32, 32, seed=50)
+    o_f, S_f, P_f = run_gpu_forward(x)
+    d = to_device(x)
+    S = torch.zeros((3, 2, 32, 32), device="cuda")
+    P = torch.ones((3, 2, 32) if variant == "diag" else (3, 2), device="cuda")
+    outs = []
+    for t in range(40):
+        o = kdn.decode_step(variant, *[d[n][:, t].contiguous() for n in NAMES], S, P,
+                            mu=x.mu, scale=x.scale)
+        outs.append(host_f64(o))
+    torch.cuda.synchronize()
+    check("o", np.stack(outs, axis=1), o_f, 1e-5)
+    check("S", host_f64(S), S_f, 1e-5)
+    check("P", host_f64(P), P_f, 1e-5)
+
+
+# ---------------------------------------------------------------------------------------------
+# full-size workloads, checked on sampled chains
+# ---------------------------------------------------------------------------------------------
+
+def _sample_chains(B, H, k=6, seed=0):
+    g = np.random.default_rng(seed)
+    picks = {(0, 0), (B - 1, H - 1)}
+    while len(picks) < k:
+        picks.add((int(g.integers(B)), int(g.integers(H))))
+    return sorted(picks)
+
+
+@pytest.mark.parametrize("wid", [1, 2])
+def test_full_workload_sampled(wid):
+    x = W.draw_workload(wid)
+    o, S, P = run_gpu_forward(x)
+    chains = _sample_chains(x.B, x.H, seed=wid)
+    refs = run_oracle_forward(x, chains=chains)
+    for (b, h), ref in zip(chains, refs):
+        print(f" chain (b={b}, h={h})")
+        check("o", o[b:b + 1, :, h:h + 1], ref["o"], TOL[x.dtype])
+        check("S_T", S[b:b + 1, h:h + 1], ref["S_T"], TOL[x.dtype])
+        check("P_T", P[b:b + 1, h:h + 1], ref["P_T"], TOL[x.dtype])
+
+
+def test_full_workload_packed_sampled():
+    x = W.draw_workload(3)
+    o, S, P = run_gpu_forward(x)
+    lens = np.diff(x.cu_seqlens)
+    picks = [int(np.argmin(lens)), int(np.argmax(lens)), 7, 20]
+    for n in picks:
+        heads = [0, 5, 15]
+        ref = run_oracle_packed_seq(x, n, heads)
+        t0, t1 = int(x.cu_seqlens[n]), int(x.cu_seqlens[n + 1])
+        print(f" sequence {n} (length {t1 - t0})")
+        check("o", o[:, t0:t1][:, :, heads], ref["o"], TOL[x.dtype])
+        check("S_T", S[n:n + 1][:, heads], ref["S_T"], TOL[x.dtype])
+        check("P_T", P[n:n + 1][:, heads], ref["P_T"], TOL[x.dtype])
+
+
+@pytest.mark.parametrize("variant", ["diag", "iso"])
+def test_decode_workload4_sampled(variant):
+    """Prefill (B256, T1024) on the GPU, then 64 decode steps; sampled rows vs the oracle."""
+    from paper_2609_07816_amd import kdn
+    R, H, d, steps = 256, 16, 128, 64
+    pre = W.draw_decode_prefill(variant)
+    dpre = to_device(pre)
+    f = kdn.forward_diag if variant == "diag" else kdn.forward_iso
+    _, S_dev, P_dev = f(dpre["q"], dpre["k"], dpre["v"], dpre["alpha"], dpre["omega"],
+                        dpre["r"], mu=pre.mu, scale=pre.scale)
+    rows = [0, 77, 255]
+    refs = run_oracle_forward(pre, chains=[(b, h) for b in rows for h in range(H)])
+    S_ref = np.zeros((len(rows), H, d, d))
+    P_ref = np.zeros((len(rows), H, d) if variant == "diag" else (len(rows), H))
+    for i, ref in enumerate(refs):
+        b, h = divmod(i, H)
+        S_ref[b, h] = ref["S_T"][0, 0]
+        P_ref[b, h] = ref["P_T"][0, 0]
+    torch.cuda.synchronize()
+    check("prefill S_T (sampled rows)", host_f64(S_dev)[rows], S_ref, TOL["bf16"])
+    for s in range(steps):
+        x = W.draw_decode_step(variant, s)
+        dd = to_device(x)
+        o = kdn.decode_step(variant, *[dd[n][:, 0].contiguous() for n in NAMES], S_dev, P_dev,
+                            mu=x.mu, scale=x.scale)
+        o_ref = oracle.decode_step(variant, *[x.f64(n)[rows, 0] for n in NAMES], S_ref, P_ref,
+                                   mu=x.mu, scale=x.scale)
+        if s % 16 == 15:
+            torch.cuda.synchronize()
+            check(f"o step {s} (sampled rows)", host_f64(o)[rows], o_ref, TOL["bf16"])
+    torch.cuda.synchronize()
+    check("S after decode", host_f64(S_dev)[rows], S_ref, TOL["bf16"])
+    check("P after decode", host_f64(P_dev)[rows], P_ref, TOL["bf16"])
