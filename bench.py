@@ -49,6 +49,24 @@ def algorithmic_flops(B, T, H, dk, dv, C=64):
     return B * T * H * (6 * d * dv + 10 * C * d + C * C / 3.0)
 
 
+PROFILE = os.path.join(ROOT, "profiles", "kdn_fwd_kernel_diag_B4_T4096_H16_d128.json")
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary (FETCH_SIZE and
+    WRITE_SIZE scaled by a plain copy of known size), or None when the summary is missing or
+    was taken from a different version of the kernel source."""
+    try:
+        from paper_2609_07816_amd.rocprof_summary import source_hash
+        with open(PROFILE) as f:
+            rec = json.load(f)
+        if rec.get("kernel_source_sha256") != source_hash():
+            return None
+        return int(round(rec["traffic_bytes"]))
+    except (OSError, ValueError, KeyError):
+        return None
+
+
 def cpu_baseline(x, nthreads):
     """The oracle, unchanged, on a bounded sample of the workload: a subset of the independent
     (batch row, head) chains at full length. Returns the rate in workload tokens/s."""
@@ -168,7 +186,7 @@ def main():
                    "mu": x.mu, "scale": x.scale},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None,
+                     "traffic": measured_traffic(),
                      "kernel": "kdn_fwd_kernel (bf16, dk=128, dv tile 32, chunk 64, diagonal)",
                      "algorithmic_bytes_per_launch": abytes,
                      "kernel_ms_mean": round(kmean, 4), "kernel_ms_median": round(kmed, 4),
