@@ -69,7 +69,8 @@ struct Cfg {
     static constexpr size_t OFF_RT = OFF_XT + al16((size_t)BV * LDC * sizeof(MT));
     static constexpr size_t OFF_R2T = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));
     static constexpr size_t OFF_INV = OFF_R2T + al16((size_t)BV * LDC * sizeof(MT));
-    static constexpr size_t END_ALIAS = OFF_INV + al16((size_t)4 * 16 * LDI * sizeof(MT));
+    static constexpr size_t OFF_AIT = OFF_INV + al16((size_t)4 * 16 * LDI * sizeof(MT));  // [C][LDC]
+    static constexpr size_t END_ALIAS = OFF_AIT + al16((size_t)C * LDC * sizeof(MT));
     static constexpr size_t SZ_R1 = al16(SZ_RAW > END_ALIAS ? SZ_RAW : END_ALIAS);
     static constexpr size_t OFF_V = SZ_R1;                                         // TI [C][BV]
     static constexpr size_t OFF_KB = OFF_V + al16((size_t)C * BV * sizeof(TI));    // MT [C][LDK]
@@ -78,8 +79,10 @@ struct Cfg {
     static constexpr size_t OFF_PBT = OFF_PB + al16((size_t)C * LDK * sizeof(MT)); // [DK][LDC]
     static constexpr size_t OFF_SMT = OFF_PBT + al16((size_t)DK * LDC * sizeof(MT)); // [BV][LDK]
     static constexpr size_t OFF_SC = OFF_SMT + al16((size_t)BV * LDK * sizeof(MT));
-    // scalars: r[C], mr[C], rden[C], beta[C], gtok[C], gC[DK], wtok[C], atok[C]
-    static constexpr size_t SZ_SC = (size_t)(7 * C + DK + 4) * 4;
+    // scalars: r[C], mr[C], rden[C], beta[C], gtok[C], gC[DK], wtok[C], atok[C]; then the
+    // carried variance state z[DK][2] and the segment summaries M[NSEG-1][DK][4], G[NSEG-1][DK]
+    static constexpr int NSEG = C / 16;                 // 16-token segments of the variance scan
+    static constexpr size_t SZ_SC = (size_t)(7 * C + DK + 4 + 2 * DK + (NSEG - 1) * DK * 5) * 4;
     static constexpr size_t TOTAL = al16(OFF_SC + SZ_SC);  // checked by the launcher
 };
 
@@ -128,6 +131,64 @@ __device__ __forceinline__ floatx4 mm_kc(const MT* A, int lda, const MT* BT, int
     return acc;
 }
 
+// acc1 += A1 * B and acc2 += A2 * B over K, sharing each B fragment (layouts as mm_kc).
+template <class MT, int K>
+__device__ __forceinline__ void mm_kc2(const MT* A1, const MT* A2, int lda, const MT* BT, int ldb,
+                                       floatx4& acc1, floatx4& acc2, int lane)
+{
+    const int i = lane & 15, g = lane >> 4;
+    if constexpr (std::is_same<MT, float>::value) {
+#pragma unroll
+        for (int ks = 0; ks < K / 4; ++ks) {
+            const float b = BT[i * ldb + 4 * ks + g];
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(A1[i * lda + 4 * ks + g], b, acc1, 0, 0, 0);
+            acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(A2[i * lda + 4 * ks + g], b, acc2, 0, 0, 0);
+        }
+    } else if constexpr (K % 32 == 0) {
+#pragma unroll
+        for (int ks = 0; ks < K / 32; ++ks) {
+            const bf16x8 b = *reinterpret_cast<const bf16x8*>(BT + i * ldb + 32 * ks + 8 * g);
+            const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(A1 + i * lda + 32 * ks + 8 * g);
+            const bf16x8 a2 = *reinterpret_cast<const bf16x8*>(A2 + i * lda + 32 * ks + 8 * g);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b, acc1, 0, 0, 0);
+            acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b, acc2, 0, 0, 0);
+        }
+    } else {
+        static_assert(K == 16, "bf16 tiles contract over multiples of 16");
+        const bf16x4 b = *reinterpret_cast<const bf16x4*>(BT + i * ldb + 4 * g);
+        const bf16x4 a1 = *reinterpret_cast<const bf16x4*>(A1 + i * lda + 4 * g);
+        const bf16x4 a2 = *reinterpret_cast<const bf16x4*>(A2 + i * lda + 4 * g);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a1, b, acc1, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a2, b, acc2, 0, 0, 0);
+    }
+}
+
+// acc += A[16 x 16] * B[16 x 16]; A float32 row-major (k contiguous), B given transposed as
+// BT[16][16] in operand precision (k contiguous). Vector reads on both sides.
+template <class MT>
+__device__ __forceinline__ floatx4 mm16_tv(const float* A, int lda, const MT* BT, int ldb,
+                                           floatx4 acc, int lane)
+{
+    const int i = lane & 15, g = lane >> 4;
+    const float4 a4 = *reinterpret_cast<const float4*>(A + i * lda + 4 * g);
+    if constexpr (std::is_same<MT, float>::value) {
+        // fp32 MFMA contracts k = 4 ks + g per step; gather the matching elements
+        const float av[4] = {A[i * lda + g], A[i * lda + 4 + g], A[i * lda + 8 + g],
+                             A[i * lda + 12 + g]};
+        (void)a4;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[ks], BT[i * ldb + 4 * ks + g], acc, 0,
+                                                        0, 0);
+    } else {
+        bf16x4 a;
+        a[0] = (bf16)a4.x; a[1] = (bf16)a4.y; a[2] = (bf16)a4.z; a[3] = (bf16)a4.w;
+        const bf16x4 b = *reinterpret_cast<const bf16x4*>(BT + i * ldb + 4 * g);
+        acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, acc, 0, 0, 0);
+    }
+    return acc;
+}
+
 // acc += A[16 x 16] * B[16 x 16] with A and B both row-major (A of type TA, converted).
 template <class MT, class TA>
 __device__ __forceinline__ floatx4 mm16_rr(const TA* A, int lda, const MT* B, int ldb,
@@ -151,6 +212,14 @@ __device__ __forceinline__ floatx4 mm16_rr(const TA* A, int lda, const MT* B, in
     return acc;
 }
 
+// Make this wave's LDS writes visible to its other lanes (LDS ops of one wave run in order).
+__device__ __forceinline__ void wave_lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 __device__ __forceinline__ floatx4 zero4()
 {
     floatx4 z = {0.f, 0.f, 0.f, 0.f};
@@ -168,6 +237,39 @@ __device__ __forceinline__ void seq_range(const int32_t* cu, int n, int T, int& 
         t0 = n * T;
         t1 = t0 + T;
     }
+}
+
+// Two adjacent elements as floats (bf16 pair in one 32-bit word, or two floats).
+__device__ __forceinline__ float2 ld2(const bf16* p)
+{
+    const unsigned u = *reinterpret_cast<const unsigned*>(p);
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xFFFF0000u));
+}
+__device__ __forceinline__ float2 ld2(const float* p) { return *reinterpret_cast<const float2*>(p); }
+
+// Store two adjacent values in operand precision.
+template <class MT>
+__device__ __forceinline__ void st2(MT* p, float x, float y)
+{
+    if constexpr (std::is_same<MT, float>::value) {
+        *reinterpret_cast<float2*>(p) = make_float2(x, y);
+    } else {
+        bf16x4 v;  // only the first two lanes are stored
+        v[0] = (bf16)x;
+        v[1] = (bf16)y;
+        *reinterpret_cast<unsigned*>(p) = *reinterpret_cast<const unsigned*>(&v);
+    }
+}
+
+// m <- M_t m for the token matrix M_t = [[a, w], [u a, 1 + u w]] (m row-major [m00 m01 m10 m11]);
+// the second row uses M_t's structure: row1 = u * row0' + row1.
+__device__ __forceinline__ void mob_left(float* m, float a, float w, float u)
+{
+    const float r00 = fmaf(a, m[0], w * m[2]), r01 = fmaf(a, m[1], w * m[3]);
+    m[2] = fmaf(u, r00, m[2]);
+    m[3] = fmaf(u, r01, m[3]);
+    m[0] = r00;
+    m[1] = r01;
 }
 
 // Store 8 consecutive values (16-byte aligned destination).
@@ -200,7 +302,8 @@ struct ChunkRegs {
     static constexpr int NARR = 4;                        // alpha, k, omega, q
     uint4 raw[NARR][PER];
     uint4 vv[PERV];
-    float r, w, a;                                        // per-token scalars (tid < C)
+    TI r, w, a;  // per-token scalars (tid < C), kept raw: converting them at load time would
+                 // make the load wait for every earlier load of the prefetch
 };
 
 template <class TI, class CF>
@@ -212,36 +315,58 @@ __device__ __forceinline__ void load_chunk(ChunkRegs<TI, CF>& R, const TI* const
     using CR = ChunkRegs<TI, CF>;
     constexpr int DK = CF::DK;
     const size_t rs = (size_t)H * DK;
+    // rows past the sequence end: alpha = 1 (no decay), everything else 0
+    const unsigned one = sizeof(TI) == 2 ? 0x3F803F80u : 0x3F800000u;
+    if (L == CF::C) {  // full chunk: every row is valid, no predicates
 #pragma unroll
-    for (int a = 0; a < CR::NARR; ++a) {
+        for (int a = 0; a < CR::NARR; ++a) {
+            if (!use[a]) continue;
+            const TI* base = src[a] + row0 * DK;
 #pragma unroll
-        for (int j = 0; j < CR::PER; ++j) {
+            for (int j = 0; j < CR::PER; ++j) {
+                const int idx = tid + j * NT;
+                const int t = idx / CR::VPR, e = (idx % CR::VPR) * CR::VE;
+                if (CR::NVEC % NT == 0 || idx < CR::NVEC)
+                    R.raw[a][j] = *reinterpret_cast<const uint4*>(base + t * rs + e);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < CR::PERV; ++j) {
             const int idx = tid + j * NT;
-            const int t = idx / CR::VPR, e = (idx % CR::VPR) * CR::VE;
-            // rows past the sequence end: alpha = 1 (no decay), everything else 0
-            const unsigned one = sizeof(TI) == 2 ? 0x3F803F80u : 0x3F800000u;
-            uint4 val = a == 0 ? make_uint4(one, one, one, one) : make_uint4(0, 0, 0, 0);
-            if (use[a] && idx < CR::NVEC && t < L)
-                val = *reinterpret_cast<const uint4*>(src[a] + row0 * DK + t * rs + e);
-            R.raw[a][j] = val;
+            const int t = idx / CR::VPRV, e = (idx % CR::VPRV) * CR::VE;
+            if (CR::NVECV % NT == 0 || idx < CR::NVECV)
+                R.vv[j] = *reinterpret_cast<const uint4*>(gv + (row0 + (size_t)t * H) * DV + col0 + e);
+        }
+    } else {
+#pragma unroll
+        for (int a = 0; a < CR::NARR; ++a) {
+#pragma unroll
+            for (int j = 0; j < CR::PER; ++j) {
+                const int idx = tid + j * NT;
+                const int t = idx / CR::VPR, e = (idx % CR::VPR) * CR::VE;
+                uint4 val = a == 0 ? make_uint4(one, one, one, one) : make_uint4(0, 0, 0, 0);
+                if (use[a] && idx < CR::NVEC && t < L)
+                    val = *reinterpret_cast<const uint4*>(src[a] + row0 * DK + t * rs + e);
+                R.raw[a][j] = val;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < CR::PERV; ++j) {
+            const int idx = tid + j * NT;
+            const int t = idx / CR::VPRV, e = (idx % CR::VPRV) * CR::VE;
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (idx < CR::NVECV && t < L)
+                val = *reinterpret_cast<const uint4*>(gv + (row0 + (size_t)t * H) * DV + col0 + e);
+            R.vv[j] = val;
         }
     }
-#pragma unroll
-    for (int j = 0; j < CR::PERV; ++j) {
-        const int idx = tid + j * NT;
-        const int t = idx / CR::VPRV, e = (idx % CR::VPRV) * CR::VE;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (idx < CR::NVECV && t < L)
-            val = *reinterpret_cast<const uint4*>(gv + (row0 + (size_t)t * H) * DV + col0 + e);
-        R.vv[j] = val;
-    }
-    R.r = 1.f; R.w = 0.f; R.a = 1.f;
+    R.r = from_f32<TI>(1.f); R.w = from_f32<TI>(0.f); R.a = from_f32<TI>(1.f);
     if (tid < L) {
         const size_t row = row0 + (size_t)tid * H;
-        R.r = ldf(gr, row);
+        R.r = gr[row];
         if (CF::VARIANT == 1) {
-            R.w = ldf(gw, row);
-            if (!CF::APC) R.a = ldf(ga, row);
+            R.w = gw[row];
+            if (!CF::APC) R.a = ga[row];
         }
     }
 }
@@ -311,6 +436,7 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
     MT* RT = (MT*)(smem + CF::OFF_RT);
     MT* R2T = (MT*)(smem + CF::OFF_R2T);
     MT* Inv = (MT*)(smem + CF::OFF_INV);
+    MT* AiT = (MT*)(smem + CF::OFF_AIT);  // A transposed: AiT[col][row]
     TI* sV = (TI*)(smem + CF::OFF_V);
     MT* Kb = (MT*)(smem + CF::OFF_KB);
     MT* Qb = (MT*)(smem + CF::OFF_QB);
@@ -325,6 +451,9 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
     float* s_gC = s_gtok + C;
     float* s_wtok = s_gC + DK;
     float* s_atok = s_wtok + C;
+    float* s_zin = s_atok + C + 4;                 // [DK][2] carried (n, d) per channel
+    float* s_segM = s_zin + 2 * DK;                // [NSEG-1][DK][4] segment Moebius products
+    float* s_segG = s_segM + (CF::NSEG - 1) * DK * 4;  // [NSEG-1][DK] segment decay products
 
     int t0, t1;
     seq_range(a.cu, n, a.T, t0, t1);
@@ -345,8 +474,10 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
     }
 
     // ---- variance state (diagonal: per channel, owned by threads [0, DK)) ------------------
-    float zn = 1.f, zd = 1.f;
-    if (DIAG && tid < DK && a.P0) zn = a.P0[(size_t)nh * DK + tid];
+    if (DIAG && tid < DK) {
+        s_zin[2 * tid] = a.P0 ? a.P0[(size_t)nh * DK + tid] : 1.f;  // z_0 = [p_0; 1]
+        s_zin[2 * tid + 1] = 1.f;
+    }
     // isotropic: one chain per head, carried by every lane of wave 0
     float izn = 1.f, izd = 1.f;
     if (!DIAG && a.P0) izn = a.P0[nh];
@@ -379,11 +510,12 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
         __syncthreads();  // previous chunk finished with every LDS region
         store_chunk<TI, CF>(pre, dsts, use, sV, tid);
         if (tid < C) {
-            s_r[tid] = pre.r;
-            s_mr[tid] = a.mu / pre.r;
+            const float rr = to_f32(pre.r);
+            s_r[tid] = rr;
+            s_mr[tid] = a.mu / rr;
             if (!DIAG) {
-                s_wtok[tid] = pre.w;
-                if (!APC) s_atok[tid] = pre.a;
+                s_wtok[tid] = to_f32(pre.w);
+                if (!APC) s_atok[tid] = to_f32(pre.a);
             }
         }
         __syncthreads();
@@ -394,58 +526,93 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
         // loops below run over the whole chunk without branches (fully unrolled: the LDS loads
         // of later tokens are issued ahead of the serial variance chain).
         if (DIAG) {
-            if (tid < DK) {
-                // variance chain of channel c and the gain operand P_bar = p_hat k / gamma
-                const int c = tid;
-                float g = 1.f;
+            // Segmented scan of the variance chain. Wave s owns tokens [16 s, 16 s + 16) and
+            // every lane an adjacent channel pair (2 p, 2 p + 1), so each lane carries two
+            // independent chains. Pass 1: each segment's Moebius product (later tokens on the
+            // left) and decay product. Pass 2: each wave composes the earlier segments onto the
+            // carried state, then replays its tokens emitting P_bar = p_hat k / gamma,
+            // K_bar = gamma k and Q_bar = gamma q. The last segment leaves the next carry.
+            constexpr int NSEG = CF::NSEG, NP = DK / 2;
+            const int seg = wave, pc = lane;
+            const bool active = seg < NSEG && pc < NP;
+            const int c0 = 2 * pc, t0s = 16 * seg;
+            if (active && seg < NSEG - 1) {
+                float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
+                float g0 = 1.f, g1 = 1.f;
 #pragma unroll
-                for (int t8 = 0; t8 < C; t8 += 8) {
-                    float pb8[8], al8[8], kk8[8], w8[8], mr8[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {  // issue the block's LDS reads together
-                        al8[j] = to_f32(sA[(t8 + j) * DK + c]);
-                        kk8[j] = to_f32(sK[(t8 + j) * DK + c]);
-                        w8[j] = to_f32(sW[(t8 + j) * DK + c]);
-                        mr8[j] = s_mr[t8 + j];
+                for (int j = 0; j < 16; ++j) {
+                    const int t = t0s + j;
+                    const float2 al = ld2(sA + t * DK + c0), kk = ld2(sK + t * DK + c0);
+                    const float2 w = ld2(sW + t * DK + c0);
+                    const float mr = s_mr[t];
+                    g0 *= al.x;
+                    g1 *= al.y;
+                    mob_left(m0, al.x * al.x, w.x, kk.x * kk.x * mr);
+                    mob_left(m1, al.y * al.y, w.y, kk.y * kk.y * mr);
+                    if (j & 1) {
+                        renorm4(m0[0], m0[1], m0[2], m0[3]);
+                        renorm4(m1[0], m1[1], m1[2], m1[3]);
                     }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int t = t8 + j;
-                        const float al = al8[j], kk = kk8[j], w = w8[j];
-                        g *= al;
-                        const float n2 = fmaf(al * al, zn, w * zd);   // n_t
-                        const float u = kk * kk * mr8[j];               // mu k^2 / r
-                        pb8[j] = n2 * kk * __builtin_amdgcn_rcpf(zd * g); // (n_t/d_{t-1}) k / g
-                        zd = fmaf(u, n2, zd);                           // d_t
-                        zn = n2;
-                        if (j & 1) renorm2(zn, zd);
-                        Pb[t * LDK + c] = from_f32<MT>(pb8[j]);
-                    }
-                    store8<MT>(PbT + c * LDC + t8, pb8);
                 }
-                s_gC[c] = g;
-            } else if (tid < 2 * DK) {
-                // cumulative decay of channel c and the decayed key / query rows
-                const int c = tid - DK;
-                float g = 1.f;
+                float* M = s_segM + (size_t)(seg * DK + c0) * 4;
+                *reinterpret_cast<float4*>(M) = make_float4(m0[0], m0[1], m0[2], m0[3]);
+                *reinterpret_cast<float4*>(M + 4) = make_float4(m1[0], m1[1], m1[2], m1[3]);
+                *reinterpret_cast<float2*>(s_segG + seg * DK + c0) = make_float2(g0, g1);
+            }
+            __syncthreads();
+            float zn0 = 0.f, zd0 = 1.f, zn1 = 0.f, zd1 = 1.f;
+            if (active) {
+                zn0 = s_zin[2 * c0]; zd0 = s_zin[2 * c0 + 1];
+                zn1 = s_zin[2 * c0 + 2]; zd1 = s_zin[2 * c0 + 3];
+                float g0 = 1.f, g1 = 1.f;
+                for (int ps = 0; ps < seg; ++ps) {  // state entering this segment
+                    const float4 A0 = *reinterpret_cast<const float4*>(s_segM + (ps * DK + c0) * 4);
+                    const float4 A1 =
+                        *reinterpret_cast<const float4*>(s_segM + (ps * DK + c0) * 4 + 4);
+                    float n = A0.x * zn0 + A0.y * zd0, d = A0.z * zn0 + A0.w * zd0;
+                    zn0 = n; zd0 = d; renorm2(zn0, zd0);
+                    n = A1.x * zn1 + A1.y * zd1; d = A1.z * zn1 + A1.w * zd1;
+                    zn1 = n; zd1 = d; renorm2(zn1, zd1);
+                    const float2 gg = *reinterpret_cast<const float2*>(s_segG + ps * DK + c0);
+                    g0 *= gg.x;
+                    g1 *= gg.y;
+                }
+                float pb0[16], pb1[16];
 #pragma unroll
-                for (int t8 = 0; t8 < C; t8 += 8) {
-                    float al8[8], kk8[8], qq8[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        al8[j] = to_f32(sA[(t8 + j) * DK + c]);
-                        kk8[j] = to_f32(sK[(t8 + j) * DK + c]);
-                        qq8[j] = to_f32(sQ[(t8 + j) * DK + c]);
+                for (int j = 0; j < 16; ++j) {
+                    const int t = t0s + j;
+                    const float2 al = ld2(sA + t * DK + c0), kk = ld2(sK + t * DK + c0);
+                    const float2 w = ld2(sW + t * DK + c0), qq = ld2(sQ + t * DK + c0);
+                    const float mr = s_mr[t];
+                    g0 *= al.x;
+                    g1 *= al.y;
+                    const float n0 = fmaf(al.x * al.x, zn0, w.x * zd0);  // n_t
+                    const float n1 = fmaf(al.y * al.y, zn1, w.y * zd1);
+                    pb0[j] = n0 * kk.x * __builtin_amdgcn_rcpf(zd0 * g0);  // p_hat k / gamma
+                    pb1[j] = n1 * kk.y * __builtin_amdgcn_rcpf(zd1 * g1);
+                    zd0 = fmaf(kk.x * kk.x * mr, n0, zd0);               // d_t
+                    zd1 = fmaf(kk.y * kk.y * mr, n1, zd1);
+                    zn0 = n0;
+                    zn1 = n1;
+                    if (j & 1) {
+                        renorm2(zn0, zd0);
+                        renorm2(zn1, zd1);
                     }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int t = t8 + j;
-                        g *= al8[j];
-                        Kb[t * LDK + c] = from_f32<MT>(g * kk8[j]);
-                        Qb[t * LDK + c] = from_f32<MT>(g * qq8[j]);
-                    }
+                    st2<MT>(Kb + t * LDK + c0, g0 * kk.x, g1 * kk.y);
+                    st2<MT>(Qb + t * LDK + c0, g0 * qq.x, g1 * qq.y);
+                    st2<MT>(Pb + t * LDK + c0, pb0[j], pb1[j]);
+                }
+                store8<MT>(PbT + c0 * LDC + t0s, pb0);
+                store8<MT>(PbT + c0 * LDC + t0s + 8, pb0 + 8);
+                store8<MT>(PbT + (c0 + 1) * LDC + t0s, pb1);
+                store8<MT>(PbT + (c0 + 1) * LDC + t0s + 8, pb1 + 8);
+                if (seg == NSEG - 1) {
+                    *reinterpret_cast<float2*>(s_gC + c0) = make_float2(g0, g1);
                 }
             }
+            __syncthreads();  // every wave has read the carried state before it is replaced
+            if (active && seg == NSEG - 1)
+                *reinterpret_cast<float4*>(s_zin + 2 * c0) = make_float4(zn0, zd0, zn1, zd1);
         } else {
             // isotropic: per-token trace average of alpha^2 and ||k||^2; thread (token, quarter)
             // sums a quarter of the channels, two lane exchanges finish the sum
@@ -565,67 +732,105 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
                 }
                 if (tid < DK) s_gC[tid] = s_gtok[L - 1];
             }
+            __syncthreads();
         }
-        __syncthreads();
 
         // issue the next chunk's loads now (after the register-heavy token loops); they land
         // while phases 2-6 of this chunk compute
-        if (c0 + C < t1)
-            load_chunk<TI, CF>(pre, srcs, use, gv, gr, gw, ga, row0 + (size_t)C * H, H, DV,
-                               col0, min(C, t1 - c0 - C), tid);
+        // (unconditional: past the last chunk every load is predicated off; a branch on the
+        // loop condition here would let the compiler merge the loads into the loop latch)
+        load_chunk<TI, CF>(pre, srcs, use, gv, gr, gw, ga, row0 + (size_t)C * H, H, DV, col0,
+                           max(0, min(C, t1 - c0 - C)), tid);
+        __builtin_amdgcn_sched_barrier(0);  // keep the loads here, ahead of phases 2-6
 
         // ---- phase 2: T = tril(K_bar P_bar^T, -1) / den and A_qk = tril(Q_bar P_bar^T) / den
-        // diagonal T blocks first: their diagonal is sum_i p_hat k^2, giving den.
-        floatx4 tdiag = zero4();
+        // 2a: wave b owns diagonal block b. Its K_bar P_bar^T diagonal is sum_i p_hat k^2, which
+        // gives den; the wave scales the block, stores it and inverts I + T_bb by forward
+        // substitution (lanes 0..15, one column each) without waiting for the other waves.
         if (wave < NB) {
             const int b = wave;
-            tdiag = mm_kc<MT, DK>(Kb + 16 * b * LDK, LDK, Pb + 16 * b * LDK, LDK, zero4(), lane);
+            const floatx4 tdiag =
+                mm_kc<MT, DK>(Kb + 16 * b * LDK, LDK, Pb + 16 * b * LDK, LDK, zero4(), lane);
             if (DIAG && lg == (li >> 2)) {
                 const int t = 16 * b + li;
                 s_rden[t] = 1.f / (s_r[t] + tdiag[li & 3]);
             }
-        }
-        __syncthreads();
-        if (wave < NB) {
-            const int b = wave;
+            wave_lds_sync();
             const float rd = s_rden[16 * b + li];
 #pragma unroll
             for (int rr = 0; rr < 4; ++rr) {
                 const int row = 4 * lg + rr;
                 Tm[(16 * b + row) * LDT + 16 * b + li] = row > li ? tdiag[rr] * rd : 0.f;
             }
-        }
-        {
-            // remaining blocks: T (ib > jb) and A_qk (ib >= jb); A_qk above the diagonal = 0
-            constexpr int NOFF = NB * (NB - 1) / 2, NAQ = NB * (NB + 1) / 2;
-            for (int job = wave; job < NOFF + NAQ; job += 4) {
-                int ib = 0, jb = 0, x = job < NOFF ? job : job - NOFF;
-                if (job < NOFF) {  // enumerate (ib > jb)
-                    ib = 1;
-                    while (x >= ib) { x -= ib; ++ib; }
-                    jb = x;
-                } else {           // enumerate (ib >= jb)
-                    ib = 0;
-                    while (x > ib) { x -= ib + 1; ++ib; }
-                    jb = x;
-                }
-                const MT* Asrc = job < NOFF ? Kb : Qb;
-                floatx4 acc = mm_kc<MT, DK>(Asrc + 16 * ib * LDK, LDK, Pb + 16 * jb * LDK, LDK,
-                                            zero4(), lane);
-                const float rd = s_rden[16 * jb + li];
+            wave_lds_sync();
+            if (lg == 0) {
+                const int j = li;
+                float x[16];
+                const float* Tb = Tm + (16 * b) * LDT + 16 * b;
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
-                    const float val = acc[rr] * rd;
-                    if (job < NOFF) {
-                        Tm[row * LDT + col] = val;
+                for (int i = 0; i < 16; ++i) {
+                    float trow[16];  // row i of the block, 16-byte broadcast reads
+#pragma unroll
+                    for (int v4 = 0; v4 < (i + 3) / 4; ++v4) {
+                        const float4 q4 = *reinterpret_cast<const float4*>(Tb + i * LDT + 4 * v4);
+                        trow[4 * v4] = q4.x; trow[4 * v4 + 1] = q4.y;
+                        trow[4 * v4 + 2] = q4.z; trow[4 * v4 + 3] = q4.w;
+                    }
+                    float sum = 0.f;
+#pragma unroll
+                    for (int kk = 0; kk < i; ++kk) sum = fmaf(trow[kk], x[kk], sum);
+                    x[i] = i < j ? 0.f : (i == j ? 1.f : -sum);
+                }
+#pragma unroll
+                for (int i = 0; i < 16; ++i) Ai[(16 * b + i) * LDC + 16 * b + j] = from_f32<MT>(x[i]);
+                // column j of the block is row j of the transposed copy: 16 consecutive values
+                store8<MT>(AiT + (16 * b + j) * LDC + 16 * b, x);
+                store8<MT>(AiT + (16 * b + j) * LDC + 16 * b + 8, x + 8);
+            }
+        }
+        __syncthreads();
+        // 2b: off-diagonal T blocks and every A_qk block, columns scaled by 1/den. T(ib, jb) and
+        // A_qk(ib, jb) share the P_bar fragment of block column jb; wave w takes the units
+        // w, w + 4, ... of [pairs (ib > jb) ..., diagonal A_qk blocks ...].
+        {
+            constexpr int NPAIR = NB * (NB - 1) / 2, NUNIT = NPAIR + NB;
+#pragma unroll
+            for (int u0 = 0; u0 < NUNIT; u0 += 4) {
+                const int unit = u0 + wave;
+                if (unit < NUNIT) {
+                    int ib, jb;
+                    if (unit < NPAIR) {  // enumerate (ib > jb) in row order
+                        int x = unit;
+                        ib = 1;
+                        while (x >= ib) { x -= ib; ++ib; }
+                        jb = x;
                     } else {
-                        Aq[row * LDC + col] = from_f32<MT>(ib > jb || (4 * lg + rr) >= li ? val
-                                                                                       : 0.f);
+                        ib = jb = unit - NPAIR;
+                    }
+                    const float rd = s_rden[16 * jb + li];
+                    if (ib > jb) {
+                        floatx4 tacc = zero4(), qacc = zero4();
+                        mm_kc2<MT, DK>(Kb + 16 * ib * LDK, Qb + 16 * ib * LDK, LDK,
+                                       Pb + 16 * jb * LDK, LDK, tacc, qacc, lane);
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
+                            Tm[row * LDT + col] = tacc[rr] * rd;
+                            Aq[row * LDC + col] = from_f32<MT>(qacc[rr] * rd);
+                        }
+                    } else {
+                        const floatx4 qacc = mm_kc<MT, DK>(Qb + 16 * ib * LDK, LDK,
+                                                           Pb + 16 * jb * LDK, LDK, zero4(), lane);
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
+                            Aq[row * LDC + col] = from_f32<MT>((4 * lg + rr) >= li ? qacc[rr] * rd
+                                                                                  : 0.f);
+                        }
                     }
                 }
             }
-            // zero the blocks above the diagonal: 16-byte stores, one row segment per store
+            // zero the blocks above the diagonal of A_qk and A: 16-byte stores
             constexpr int VPB = 16 * (int)sizeof(MT) / 16;         // 16-byte vectors per block row
             constexpr int NUP = NB * (NB - 1) / 2;                  // blocks above the diagonal
             if constexpr (NUP > 0)
@@ -643,48 +848,33 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
         }
         __syncthreads();
 
-        // ---- phase 3: A = (I + T)^-1, blockwise ----------------------------------------
-        // 3a: 16 x 16 diagonal blocks by forward substitution; lane = (block, column)
-        if (wave == 0) {
-            const int b = lg, j = li;
-            if (b < NB) {
-                float x[16];
-                const float* Tb = Tm + (16 * b) * LDT + 16 * b;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    float s = 0.f;
-#pragma unroll
-                    for (int kk = 0; kk < i; ++kk) s = fmaf(Tb[i * LDT + kk], x[kk], s);
-                    x[i] = i < j ? 0.f : (i == j ? 1.f : -s);
-                }
-#pragma unroll
-                for (int i = 0; i < 16; ++i) Ai[(16 * b + i) * LDC + 16 * b + j] = from_f32<MT>(x[i]);
-            }
-        }
-        __syncthreads();
-        // 3b: off-diagonal blocks, A_ij = -A_ii sum_{j<=k<i} T_ik A_kj, one block row at a time
-        // (rows of blocks below depend on the blocks to their upper right).
+        // ---- phase 3: A = (I + T)^-1 off the diagonal (diagonal blocks done in 2a) -----
+        // A_ij = -A_ii sum_{j<=k<i} T_ik A_kj, one block diagonal d = i - j at a time (blocks
+        // further from the diagonal depend on the nearer ones). Operands are read as vectors:
+        // T rows (fp32), A columns from the transposed copy.
 #pragma unroll
         for (int d = 1; d < NB; ++d) {
-            // blocks (ib, jb) with ib - jb == d are independent of each other
             const int nblk = NB - d;
             if (wave < nblk) {
                 const int jb = wave, ib = jb + d;
                 floatx4 acc = zero4();
                 for (int kb = jb; kb < ib; ++kb)
-                    acc = mm16_rr<MT, float>(Tm + (16 * ib) * LDT + 16 * kb, LDT,
-                                             Ai + (16 * kb) * LDC + 16 * jb, LDC, acc, lane);
-                MT* tmp = Inv + wave * 16 * CF::LDI;
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) tmp[(4 * lg + rr) * CF::LDI + li] = from_f32<MT>(acc[rr]);
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-                floatx4 res = mm16_rr<MT, MT>(Ai + (16 * ib) * LDC + 16 * ib, LDC, tmp, CF::LDI,
-                                              zero4(), lane);
+                    acc = mm16_tv<MT>(Tm + (16 * ib) * LDT + 16 * kb, LDT,
+                                      AiT + (16 * jb) * LDC + 16 * kb, LDC, acc, lane);
+                // tmp = acc, stored transposed (tmpT[col][row]) as the next B operand
+                MT* tmpT = Inv + wave * 16 * CF::LDI;
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr)
-                    Ai[(16 * ib + 4 * lg + rr) * LDC + 16 * jb + li] = from_f32<MT>(-res[rr]);
+                    tmpT[li * CF::LDI + 4 * lg + rr] = from_f32<MT>(acc[rr]);
+                wave_lds_sync();
+                const floatx4 res = mm_kc<MT, 16>(Ai + (16 * ib) * LDC + 16 * ib, LDC, tmpT,
+                                                  CF::LDI, zero4(), lane);
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
+                    Ai[row * LDC + col] = from_f32<MT>(-res[rr]);
+                    AiT[col * LDC + row] = from_f32<MT>(-res[rr]);
+                }
             }
             __syncthreads();
         }
@@ -697,10 +887,9 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
             Oacc[j] = zero4();
             if (ot < CF::NOUT) {
                 const int mt = ot / CF::NNT, nt = ot % CF::NNT;
-                floatx4 x = mm_kc<MT, DK>(Kb + 16 * mt * LDK, LDK, SmT + 16 * nt * LDK, LDK,
-                                          zero4(), lane);
-                Oacc[j] = mm_kc<MT, DK>(Qb + 16 * mt * LDK, LDK, SmT + 16 * nt * LDK, LDK,
-                                        zero4(), lane);
+                floatx4 x = zero4();
+                mm_kc2<MT, DK>(Kb + 16 * mt * LDK, Qb + 16 * mt * LDK, LDK, SmT + 16 * nt * LDK,
+                               LDK, x, Oacc[j], lane);
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr) {
                     const int t = 16 * mt + 4 * lg + rr, cc = 16 * nt + li;
@@ -790,7 +979,7 @@ __global__ __launch_bounds__(NT, 1) void kdn_fwd_kernel(FwdArgs a)
     }
     if (a.P_T && tile == 0) {
         if (DIAG) {
-            if (tid < DK) a.P_T[(size_t)nh * DK + tid] = zn / zd;
+            if (tid < DK) a.P_T[(size_t)nh * DK + tid] = s_zin[2 * tid] / s_zin[2 * tid + 1];
         } else if (tid == 0) {
             a.P_T[nh] = izn / izd;
         }
