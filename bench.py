@@ -187,7 +187,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(),
-                     "kernel": "kdn_fwd_kernel (bf16, dk=128, dv tile 32, chunk 64, diagonal)",
+                     "kernel": "forward = chunk summaries + carry scan + WY prep + state "
+                               "passing (bf16, dk=dv=128, chunk 64, state dv tile 32)",
                      "algorithmic_bytes_per_launch": abytes,
                      "kernel_ms_mean": round(kmean, 4), "kernel_ms_median": round(kmed, 4),
                      "mfma_frac": round(aflops / (kmean * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,

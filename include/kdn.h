@@ -61,8 +61,8 @@ typedef enum { KDN_F32 = 0, KDN_BF16 = 1 } kdn_dtype_t;
  *   mu > 0 (the paper uses mu = dk); scale > 0 (the paper uses dk^-1/2).
  *   chunk: memory-chunk length (16, 32 or 64), or 0 for the library's choice. Results do not
  *   depend on it beyond rounding.
- *   workspace: device scratch of kdn_forward_workspace_bytes(...) bytes (may be NULL when that
- *   query returns 0).
+ *   workspace: device scratch of at least kdn_forward_workspace_bytes(...) bytes
+ *   (KDN_ERR_WORKSPACE when smaller or NULL).
  */
 kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const void* alpha,
                               const void* omega, const void* r, const float* S0, const float* P0,
@@ -88,9 +88,19 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
                              int32_t chunk, void* workspace, size_t workspace_bytes,
                              void* stream);
 
-/* Device scratch (bytes) the forward needs for these sizes; variant 0 = diagonal, 1 = iso.  */
+/*
+ * Device scratch (bytes) that kdn_forward_diag (variant 0) / kdn_forward_iso (variant 1) need
+ * for these sizes; packed != 0 for a packed batch (cu_seqlens given), chunk as passed to the
+ * forward (0 = the library's choice). Returns 0 for arguments the forward rejects. The scratch
+ * carries, between the forward's passes, the variance-chain summaries and carries of every
+ * chunk (App. "Hardware-Efficient Chunkwise Algorithm", eqs. chunk-gain-summary and
+ * chunk-gain-carry) and every (chunk, head)'s WY factors W, Q_bar, K_tail, A_qk, U and
+ * gamma_C (Sec. "Chunkwise Memory Scan"). It needs no initialisation and is dead once the
+ * forward's work on the stream has finished; two forwards in flight at once need two.
+ */
 size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
-                                   int32_t dk, int32_t dv);
+                                   int32_t dk, int32_t dv, kdn_dtype_t dtype, int32_t packed,
+                                   int32_t chunk);
 
 /*
  * One recurrent decode step: exactly one token of the forward recurrence per row, with the

@@ -79,7 +79,7 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
     if (!(mu > 0.f) || !(scale > 0.f))
         return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
                     scale);
-    if (chunk != 0 && !kdn::forward_chunk_supported(dtype, dk, dv, chunk))
+    if (chunk != 0 && !kdn::chunked_supported(dtype, dk, dv, chunk))
         return fail(KDN_ERR_UNSUPPORTED, "chunk=%d does not fit one workgroup's LDS for this "
                     "dtype, dk=%d and dv=%d (use 0 for the largest that fits)", chunk, dk, dv);
     const size_t ntok = (size_t)B * T * H, es = esize(dtype);
@@ -100,11 +100,28 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
         return fail(KDN_ERR_INVALID_ARG, "P_T partially overlaps P0");
     if (overlaps(o, nv, S_T, ns) || overlaps(o, nv, P_T, np))
         return fail(KDN_ERR_INVALID_ARG, "o overlaps the state outputs");
-    const size_t need = kdn::forward_workspace_bytes(variant, N, B, T, H, dk, dv);
+    const size_t need =
+        kdn::chunked_workspace_bytes(variant, cu != nullptr, N, B, T, H, dk, dv, dtype, chunk);
     if (need > 0 && (!ws || ws_bytes < need))
         return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                     ws ? ws_bytes : (size_t)0);
     return KDN_OK;
+}
+
+kdn::FwdCall fwd_call(int variant, int apc, const void* q, const void* k, const void* v,
+                      const void* alpha, const void* omega, const void* r, const float* S0,
+                      const float* P0, void* o, float* S_T, float* P_T, const int32_t* cu,
+                      int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                      kdn_dtype_t dtype, float mu, float scale, int32_t chunk, void* ws)
+{
+    kdn::FwdCall c;
+    c.variant = variant; c.apc = apc;
+    c.q = q; c.k = k; c.v = v; c.alpha = alpha; c.omega = omega; c.r = r;
+    c.S0 = S0; c.P0 = P0; c.o = o; c.S_T = S_T; c.P_T = P_T;
+    c.sa = {cu, N, B, T, H};
+    c.dk = dk; c.dv = dv; c.dtype = dtype; c.mu = mu; c.scale = scale; c.chunk = chunk;
+    c.workspace = ws;
+    return c;
 }
 
 }  // namespace
@@ -128,10 +145,13 @@ const char* kdn_last_error(void) { return g_err; }
 const char* kdn_version(void) { return "kdn-mi355x 0.1 (gfx950)"; }
 
 size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
-                                   int32_t dk, int32_t dv)
+                                   int32_t dk, int32_t dv, kdn_dtype_t dtype, int32_t packed,
+                                   int32_t chunk)
 {
-    if (N <= 0 || B <= 0 || T <= 0 || H <= 0) return 0;
-    return kdn::forward_workspace_bytes(variant, N, B, T, H, dk, dv);
+    if (N <= 0 || B <= 0 || T <= 0 || H <= 0 || !head_ok(dk) || !head_ok(dv)) return 0;
+    if (dtype != KDN_F32 && dtype != KDN_BF16) return 0;
+    if (chunk != 0 && !kdn::chunked_supported(dtype, dk, dv, chunk)) return 0;
+    return kdn::chunked_workspace_bytes(variant, packed != 0, N, B, T, H, dk, dv, dtype, chunk);
 }
 
 size_t kdn_gain_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
@@ -152,9 +172,9 @@ kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const
                                     N, B, T, H, dk, dv, dtype, 1, mu, scale, chunk, workspace,
                                     workspace_bytes);
     if (st != KDN_OK) return st;
-    kdn::SeqArgs sa = {cu_seqlens, N, B, T, H};
-    return hip_status(kdn::launch_forward(0, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, sa,
-                                          dk, dv, dtype, 1, mu, scale, chunk, workspace,
+    return hip_status(kdn::launch_chunked(fwd_call(0, 1, q, k, v, alpha, omega, r, S0, P0, o, S_T,
+                                                   P_T, cu_seqlens, N, B, T, H, dk, dv, dtype,
+                                                   mu, scale, chunk, workspace),
                                           (hipStream_t)stream),
                       "kdn_forward_diag launch");
 }
@@ -172,9 +192,9 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
                                     N, B, T, H, dk, dv, dtype, apc, mu, scale, chunk, workspace,
                                     workspace_bytes);
     if (st != KDN_OK) return st;
-    kdn::SeqArgs sa = {cu_seqlens, N, B, T, H};
-    return hip_status(kdn::launch_forward(1, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, sa,
-                                          dk, dv, dtype, apc, mu, scale, chunk, workspace,
+    return hip_status(kdn::launch_chunked(fwd_call(1, apc, q, k, v, alpha, omega, r, S0, P0, o,
+                                                   S_T, P_T, cu_seqlens, N, B, T, H, dk, dv,
+                                                   dtype, mu, scale, chunk, workspace),
                                           (hipStream_t)stream),
                       "kdn_forward_iso launch");
 }

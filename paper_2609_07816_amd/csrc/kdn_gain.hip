@@ -70,10 +70,10 @@ __device__ __forceinline__ void seq_bounds(const int32_t* cu, int n, int T, int&
 // Chunk offsets: fixed length -> n * ceil(T / CG); packed -> the table built on the device.
 __device__ __forceinline__ bool locate_chunk(const int32_t* cu, const int32_t* choff, int N,
                                              int T, int g, int& n, int& c0, int& c1,
-                                             int& mloc, bool& last)
+                                             int& mloc, bool& last, int cg = CG)
 {
     if (!cu) {
-        const int ncs = (T + CG - 1) / CG;
+        const int ncs = (T + cg - 1) / cg;
         n = g / ncs;
         if (n >= N) return false;
         mloc = g - n * ncs;
@@ -89,14 +89,14 @@ __device__ __forceinline__ bool locate_chunk(const int32_t* cu, const int32_t* c
     }
     int t0, t1;
     seq_bounds(cu, n, T, t0, t1);
-    c0 = t0 + mloc * CG;
-    c1 = min(c0 + CG, t1);
+    c0 = t0 + mloc * cg;
+    c1 = min(c0 + cg, t1);
     last = (c1 == t1);
     return c0 < c1;
 }
 
-// Chunk-offset table for packed batches: choff[n] = sum_{m < n} ceil(len_m / CG).
-__global__ void chunk_table_kernel(const int32_t* __restrict__ cu, int N,
+// Chunk-offset table for packed batches: choff[n] = sum_{m < n} ceil(len_m / cg).
+__global__ void chunk_table_kernel(const int32_t* __restrict__ cu, int N, int cg,
                                    int32_t* __restrict__ choff)
 {
     if (threadIdx.x != 0 || blockIdx.x != 0) return;
@@ -105,7 +105,7 @@ __global__ void chunk_table_kernel(const int32_t* __restrict__ cu, int N,
         choff[n] = acc;
         int len = cu[n + 1] - cu[n];
         if (len < 0) len = 0;
-        acc += (len + CG - 1) / CG;
+        acc += (len + cg - 1) / cg;
     }
     choff[N] = acc;
 }
@@ -135,20 +135,19 @@ __global__ __launch_bounds__(DK) void diag_summary_kernel(
     summ[((size_t)g * H + h) * DK + c] = make_float4(acc.a, acc.b, acc.c, acc.d);
 }
 
-// Pass 2: per (sequence, head, channel) exclusive scan of the summaries over chunks.
-// One wavefront per channel; lanes are chunks; blocks of 64 chunks carry into the next.
-template <int DK>
+// Pass 2: per (sequence, head, channel) exclusive scan of the summaries over chunks of cg
+// tokens. One wavefront per channel; lanes are chunks; blocks of 64 chunks carry into the next.
 __global__ __launch_bounds__(256) void carry_scan_kernel(
     const float4* __restrict__ summ, const float* __restrict__ P0,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ choff, int N, int T, int H,
-    int nchan, float2* __restrict__ carry, float* __restrict__ P_T)
+    int nchan, int cg, float2* __restrict__ carry, float* __restrict__ P_T)
 {
     const int n = blockIdx.x / H, h = blockIdx.x % H;
     if (n >= N) return;
     int t0, t1;
     seq_bounds(cu, n, T, t0, t1);
-    const int nch = (t1 - t0 + CG - 1) / CG;
-    const int g0 = cu ? choff[n] : n * ((T + CG - 1) / CG);
+    const int nch = (t1 - t0 + cg - 1) / cg;
+    const int g0 = cu ? choff[n] : n * ((T + cg - 1) / cg);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     if (nch == 0) {  // an empty sequence keeps its initial variances
         if (P_T)
@@ -346,7 +345,7 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
     if (maxch == 0) return hipSuccess;
     if (sa.cu_seqlens)
         hipLaunchKernelGGL(chunk_table_kernel, dim3(1), dim3(1), 0, st, sa.cu_seqlens, sa.N,
-                           choff);
+                           CG, choff);
     const dim3 grid(maxch, sa.H);
     if (variant == 0) {
         hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
@@ -358,8 +357,8 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, false>), grid, dim3(64), 0, st, k_, a_,
                            w_, r_, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, summ);
     }
-    hipLaunchKernelGGL((carry_scan_kernel<DK>), dim3(sa.N * sa.H), dim3(256), 0, st, summ, P0,
-                       sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, carry, P_T);
+    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H), dim3(256), 0, st, summ, P0,
+                       sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, CG, carry, P_T);
     if (variant == 0) {
         hipLaunchKernelGGL((diag_emit_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
                            carry, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, gain_out,
@@ -396,6 +395,21 @@ hipError_t launch_gain_dk(int dk, int variant, const void* k, const void* alpha,
 }
 
 }  // namespace
+
+hipError_t launch_chunk_table(const int32_t* cu, int N, int cg, int32_t* choff, hipStream_t st)
+{
+    hipLaunchKernelGGL(chunk_table_kernel, dim3(1), dim3(1), 0, st, cu, N, cg, choff);
+    return hipGetLastError();
+}
+
+hipError_t launch_carry_scan(const float4* summ, const float* P0, const SeqArgs& sa, int nchan,
+                             int cg, const int32_t* choff, float2* carry, float* P_T,
+                             hipStream_t st)
+{
+    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H), dim3(256), 0, st, summ, P0,
+                       sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, cg, carry, P_T);
+    return hipGetLastError();
+}
 
 size_t gain_workspace_bytes(int variant, int N, int B, int T, int H, int dk)
 {

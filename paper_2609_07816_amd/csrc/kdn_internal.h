@@ -83,13 +83,32 @@ hipError_t launch_gain(int variant, const void* k, const void* alpha, const void
                        float* P_T, const SeqArgs& sa, int dk, kdn_dtype_t dtype,
                        int alpha_per_channel, float mu, void* workspace, hipStream_t stream);
 
-int forward_default_chunk(kdn_dtype_t dtype, int dk, int dv);
-bool forward_chunk_supported(kdn_dtype_t dtype, int dk, int dv, int chunk);
-size_t forward_workspace_bytes(int variant, int N, int B, int T, int H, int dk, int dv);
-hipError_t launch_forward(int variant, const void* q, const void* k, const void* v,
-                          const void* alpha, const void* omega, const void* r, const float* S0,
-                          const float* P0, void* o, float* S_T, float* P_T, const SeqArgs& sa,
-                          int dk, int dv, kdn_dtype_t dtype, int alpha_per_channel, float mu,
-                          float scale, int chunk, void* workspace, hipStream_t stream);
+// Chunk machinery of the variance scan (kdn_gain.hip), shared with the chunked forward.
+// choff[n] = first global chunk of sequence n for chunks of cg tokens (packed batches only).
+hipError_t launch_chunk_table(const int32_t* cu, int N, int cg, int32_t* choff, hipStream_t st);
+// Exclusive carries z_in (float2 per chunk, head and channel) from chunk summaries, and P_T.
+hipError_t launch_carry_scan(const float4* summ, const float* P0, const SeqArgs& sa, int nchan,
+                             int cg, const int32_t* choff, float2* carry, float* P_T,
+                             hipStream_t st);
+
+// Chunked forward (kdn_chunked.hip).
+struct FwdCall {
+    int variant, apc;  // 0 = diagonal, 1 = isotropic; per-channel gate (isotropic)
+    const void *q, *k, *v, *alpha, *omega, *r;
+    const float *S0, *P0;
+    void* o;
+    float *S_T, *P_T;
+    SeqArgs sa;
+    int dk, dv;
+    kdn_dtype_t dtype;
+    float mu, scale;
+    int chunk;        // 16, 32, 64 or 0 (largest that fits)
+    void* workspace;  // chunked_workspace_bytes(...) bytes
+};
+bool chunked_supported(kdn_dtype_t dtype, int dk, int dv, int chunk);
+int chunked_default_chunk(kdn_dtype_t dtype, int dk, int dv);
+size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
+                               int dv, kdn_dtype_t dtype, int chunk);
+hipError_t launch_chunked(const FwdCall& fc, hipStream_t stream);
 
 }  // namespace kdn

@@ -65,7 +65,7 @@ def lib():
                                                                    vp]
     L.kdn_gain_diag.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, f32, vp, sz, vp]
     L.kdn_gain_iso.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, i32, f32, vp, sz, vp]
-    L.kdn_forward_workspace_bytes.argtypes = [i32] * 7
+    L.kdn_forward_workspace_bytes.argtypes = [i32] * 7 + [ctypes.c_int, i32, i32]
     L.kdn_gain_workspace_bytes.argtypes = [i32] * 6
     for name in ("kdn_forward_diag", "kdn_forward_iso", "kdn_decode_step", "kdn_gain_diag",
                  "kdn_gain_iso"):
@@ -130,7 +130,8 @@ def _forward(variant, q, k, v, alpha, omega, r, S0, P0, cu_seqlens, mu, scale, c
     o = torch.empty((B, T, H, dv), dtype=k.dtype, device=dev)
     S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
     P_T = torch.empty((N, H, dk) if variant == 0 else (N, H), dtype=torch.float32, device=dev)
-    ws_bytes = lib().kdn_forward_workspace_bytes(variant, N, B, T, H, dk, dv)
+    ws_bytes = lib().kdn_forward_workspace_bytes(variant, N, B, T, H, dk, dv, _dtype_code(k),
+                                                 int(cu_seqlens is not None), int(chunk))
     ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None
     cu = None if cu_seqlens is None else cu_seqlens
     if cu is not None and cu.dtype != torch.int32:

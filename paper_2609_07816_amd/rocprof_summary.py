@@ -22,12 +22,18 @@ import json
 import os
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_07816_amd", "csrc", "kdn_forward.hip")
+CSRC = os.path.join(ROOT, "paper_2609_07816_amd", "csrc")
 
 
-def source_hash(path: str = KERNEL_SOURCE) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def source_hash() -> str:
+    """Hash of every HIP source and header of the library (a summary is stale once any of the
+    kernels it measured has changed)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(CSRC, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
 
 
 def _one(dirname: str, pattern: str) -> str:

@@ -95,8 +95,31 @@ def test_gain_argument_errors(L):
     assert st == kdn.KDN_ERR_INVALID_ARG
 
 
+def test_forward_workspace(L):
+    # the forward refuses a missing or short workspace before launching anything
+    assert fwd(L, 0) == kdn.KDN_ERR_WORKSPACE
+    need = L.kdn_forward_workspace_bytes(0, 1, 1, 8, 2, 64, 64, 1, 0, 0)
+    assert need > 0
+    p = [P(i) for i in range(7)]
+    args = p[:6] + [None, None, p[6], None, None, None, 1, 1, 8, 2, 64, 64, 1]
+    assert L.kdn_forward_diag(*args, F(64.0), F(0.125), 0, P(40), need - 1, None) \
+        == kdn.KDN_ERR_WORKSPACE
+
+
 def test_workspace_queries(L):
-    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128) == 0
+    full = L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 1, 0, 0)
+    # the WY factors of every (chunk, head) dominate: W, Q_bar, K_tail (C x dk each), A_qk
+    # (C x C) and U (C x dv) in bf16 per chunk of 64 tokens, i.e. at least (3*128+64+128)*2 B
+    # per token-head
+    assert full >= 4 * 4096 * 16 * (3 * 128 + 64 + 128) * 2
+    assert full < 2 * 4 * 4096 * 16 * (3 * 128 + 64 + 128) * 2
+    # fp32 factors take twice the bytes; a packed batch adds at most one partial chunk per
+    # sequence; rejected arguments give 0
+    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 0, 0, 32) > full
+    assert L.kdn_forward_workspace_bytes(0, 4, 1, 16384, 16, 128, 128, 1, 1, 0) >= full
+    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 0, 0, 64) == 0
+    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 48, 128, 1, 0, 0) == 0
+    assert L.kdn_forward_workspace_bytes(1, 4, 4, 4096, 16, 128, 128, 1, 0, 0) < full
     small = L.kdn_gain_workspace_bytes(0, 1, 1, 64, 1, 128)
     big = L.kdn_gain_workspace_bytes(0, 4, 4, 4096, 16, 128)
     assert big > small > 0
