@@ -25,6 +25,9 @@
 //      LDS (Sec. "Chunkwise Memory Scan", inter-chunk recurrence).
 // Dense products run on MFMA (bf16 operands with fp32 accumulation for bf16 inputs, fp32
 // MFMA for fp32 inputs); S, the variance chain and the triangular solve stay in fp32.
+#include <algorithm>
+#include <mutex>
+
 #include "kdn_device.h"
 
 namespace kdn {
@@ -84,6 +87,36 @@ __device__ __forceinline__ bool chunk_at(const int32_t* cu, const int32_t* choff
     L = min(C, t1 - c0);
     if (last) *last = c0 + L == t1;
     return L > 0;
+}
+
+// The chunks of every sequence are cut into nseg consecutive parts (segments) of near-equal
+// count: segment k of a sequence with nch chunks holds its chunks [k nch / nseg, (k+1) nch / nseg).
+// The state pass of segment k only needs the prep records of segment k, so it can run while
+// the prep pass works on segment k + 1.
+__device__ __forceinline__ void seg_range(int nch, int seg, int nseg, int& lo, int& hi)
+{
+    lo = (int)((long long)seg * nch / nseg);
+    hi = (int)((long long)(seg + 1) * nch / nseg);
+}
+
+// segoff[k * (N + 1) + n] = number of chunks of segment k in the sequences before n (packed
+// batches; fixed-length batches compute it directly).
+__global__ void seg_table_kernel(const int32_t* __restrict__ cu, int N, int C, int nseg,
+                                 int32_t* __restrict__ segoff)
+{
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    for (int k = 0; k < nseg; ++k) {
+        int acc = 0;
+        for (int n = 0; n < N; ++n) {
+            segoff[k * (N + 1) + n] = acc;
+            int len = cu[n + 1] - cu[n];
+            if (len < 0) len = 0;
+            int lo, hi;
+            seg_range((len + C - 1) / C, k, nseg, lo, hi);
+            acc += hi - lo;
+        }
+        segoff[k * (N + 1) + N] = acc;
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -167,6 +200,13 @@ __device__ __forceinline__ void mat_mul_left(float* m, const float4& x)  // m <-
     renorm4(m[0], m[1], m[2], m[3]);
 }
 
+// Two adjacent inputs from one raw word (bf16 pair) or a float pair.
+__device__ __forceinline__ float2 unpack2(unsigned u)
+{
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xFFFF0000u));
+}
+__device__ __forceinline__ float2 unpack2(float2 v) { return v; }
+
 // Diagonal: wave s composes the token matrices of segment s (tokens [16 s, 16 s + 16)) for the
 // channel pair (2 l, 2 l + 1) of lane l (later tokens on the left), with the segment's decay
 // product; wave 0 then composes the segments into the chunk summary.
@@ -190,24 +230,27 @@ __global__ __launch_bounds__(NT) void summary_diag_kernel(
         // every load is issued up front from a valid row (tokens past the end re-read the last
         // one) and its value replaced afterwards: loads under a branch would be waited for one
         // token at a time
-        float2 al[16], kk[16], ww[16];
-        float rr[16];
+        // (raw words: a conversion next to its load would make it wait for the load)
+        using P2 = typename std::conditional<sizeof(TI) == 2, unsigned, float2>::type;
+        P2 al[16], kk[16], ww[16];
+        TI rr[16];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const size_t row = (size_t)(c0 + min(16 * wave + j, L - 1)) * H + h;
-            al[j] = ld2(alpha + row * DK + ch);
-            kk[j] = ld2(k + row * DK + ch);
-            ww[j] = ld2(omega + row * DK + ch);
-            rr[j] = to_f32(r[row]);
+            al[j] = *reinterpret_cast<const P2*>(alpha + row * DK + ch);
+            kk[j] = *reinterpret_cast<const P2*>(k + row * DK + ch);
+            ww[j] = *reinterpret_cast<const P2*>(omega + row * DK + ch);
+            rr[j] = r[row];
         }
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             if (16 * wave + j < L) {  // past the end: identity matrix, no decay
-                const float mr = mu / rr[j];
-                g0 *= al[j].x;
-                g1 *= al[j].y;
-                mob_left(m0, al[j].x * al[j].x, ww[j].x, kk[j].x * kk[j].x * mr);
-                mob_left(m1, al[j].y * al[j].y, ww[j].y, kk[j].y * kk[j].y * mr);
+                const float2 alv = unpack2(al[j]), kv = unpack2(kk[j]), wv = unpack2(ww[j]);
+                const float mr = mu / to_f32(rr[j]);
+                g0 *= alv.x;
+                g1 *= alv.y;
+                mob_left(m0, alv.x * alv.x, wv.x, kv.x * kv.x * mr);
+                mob_left(m1, alv.y * alv.y, wv.y, kv.y * kv.y * mr);
                 if (j & 1) {
                     renorm4(m0[0], m0[1], m0[2], m0[3]);
                     renorm4(m1[0], m1[1], m1[2], m1[3]);
@@ -353,8 +396,7 @@ struct PrepCfg {
     static constexpr int NSG = NSEG > 1 ? NSEG - 1 : 1;  // segment summaries read per lane
     static constexpr int NWC = (DK / 16 + 3) / 4;       // W column blocks per wave
     static constexpr int NUC = (DV / 16 + 3) / 4;       // U column blocks per wave
-    // LDS map (bytes). P_bar^T is staged only for the isotropic variant (the diagonal one keeps
-    // it in registers).
+    // LDS map (bytes)
     static constexpr size_t OFF_TM = 0;                                    // float [C][LDT]
     static constexpr size_t OFF_AI = OFF_TM + al16((size_t)C * LDT * 4);   // MT [C][LDC]
     static constexpr size_t OFF_AIT = OFF_AI + al16((size_t)C * LDC * sizeof(MT));
@@ -365,8 +407,7 @@ struct PrepCfg {
     static constexpr size_t OFF_PB = OFF_QB + al16((size_t)C * LDK * sizeof(MT));
     static constexpr size_t OFF_KBT = OFF_PB + al16((size_t)C * LDK * sizeof(MT));  // [DK][LDC]
     static constexpr size_t OFF_PBT = OFF_KBT + al16((size_t)DK * LDC * sizeof(MT));
-    static constexpr size_t OFF_SC =
-        OFF_PBT + (VARIANT == 1 ? al16((size_t)DK * LDC * sizeof(MT)) : 0);
+    static constexpr size_t OFF_SC = OFF_PBT + al16((size_t)DK * LDC * sizeof(MT));
     // scalars: r, mu/r, 1/den, beta (or u), gamma_tok (or ||k||^2), a_tok, w_tok, alpha_tok [C];
     // gamma_C [DK]
     static constexpr size_t SZ_SC = (size_t)(8 * C + DK) * 4;
@@ -381,9 +422,56 @@ struct PrepArgs {
     const float* seggam;
     float* P_T;
     char* rec;
+    const int32_t* segoff;  // packed batches: this segment's row of the segment table
     int N, T, H;
+    int seg, nseg;
     float mu, scale;
 };
+
+// Position of prep slot x of segment a.seg (slots are chunk slot * H + head): head h,
+// sequence n, global chunk g, first token c0, length L, and whether the chunk is the
+// sequence's last. False past the segment's last slot (and for every later slot).
+struct PrepPos {
+    int h, n, g, c0, L;
+    bool last;
+};
+
+__device__ __forceinline__ bool prep_pos(const PrepArgs& a, int C, int x, PrepPos& p)
+{
+    const int cs = x / a.H;
+    p.h = x % a.H;
+    int m;
+    if (!a.cu) {
+        const int ncs = (a.T + C - 1) / C;
+        int lo, hi;
+        seg_range(ncs, a.seg, a.nseg, lo, hi);
+        const int per = hi - lo;
+        if (per <= 0) return false;
+        p.n = cs / per;
+        if (p.n >= a.N) return false;
+        m = lo + cs % per;
+        p.g = p.n * ncs + m;
+    } else {
+        if (cs >= a.segoff[a.N]) return false;
+        int lo = 0, hi = a.N - 1;  // largest n with segoff[n] <= cs
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (a.segoff[mid] <= cs) lo = mid; else hi = mid - 1;
+        }
+        p.n = lo;
+        const int len = max(0, a.cu[p.n + 1] - a.cu[p.n]);
+        int slo, shi;
+        seg_range((len + C - 1) / C, a.seg, a.nseg, slo, shi);
+        m = slo + (cs - a.segoff[p.n]);
+        p.g = a.choff[p.n] + m;
+    }
+    int t0, t1;
+    seq_range(a.cu, p.n, a.T, t0, t1);
+    p.c0 = t0 + m * C;
+    p.L = min(C, t1 - p.c0);
+    p.last = p.c0 + p.L == t1;
+    return p.L > 0;
+}
 
 // B fragment of U = A V for value columns 16 nt .. 16 nt + 15, contraction slice s over the
 // chunk's tokens, read straight from v: lane (g, i) takes column 16 nt + i at KF/4 consecutive
@@ -408,6 +496,84 @@ __device__ __forceinline__ typename Frag<MT, C>::V vfrag_pack(const VFrag<TI, MT
     return out;
 }
 
+// Raw global inputs of one (chunk, head) for one thread of the prep kernel. They are loaded
+// unconditionally (rows past the end of the sequence re-read its last row and are masked when
+// used) and kept raw, so that a persistent workgroup can have the next chunk's loads in flight
+// while it computes the current one.
+template <class TI, class CF>
+struct PrepIn {
+    using MT = typename CF::MT;
+    using FC = Frag<MT, CF::C>;
+    using P2 = typename std::conditional<sizeof(TI) == 2, unsigned, float2>::type;
+    TI rraw;                               // r of token tid
+    VFrag<TI, MT, CF::C> vf[CF::NUC][FC::NS];  // B fragments of U = A V
+    // diagonal variant: carry and earlier-segment summaries of the lane's channel pair, and
+    // alpha, k, omega, q of its 16 tokens (bf16 pairs or float pairs)
+    float2 z0, z1;
+    float4 sgA0[CF::NSG], sgA1[CF::NSG];
+    float2 sgG[CF::NSG];
+    P2 al[16], kk[16], ww[16], qq[16];
+};
+
+template <class TI, class CF>
+__device__ __forceinline__ void prep_load_main(PrepIn<TI, CF>& in, const PrepArgs& a,
+                                               const PrepPos& p, int ch, int t0s, int tid)
+{
+    using P2 = typename PrepIn<TI, CF>::P2;
+    constexpr int DK = CF::DK, C = CF::C, NSEG = CF::NSEG;
+    const int H = a.H;
+    const size_t row0 = (size_t)p.c0 * H + p.h;
+    in.rraw = ((const TI*)a.r)[row0 + (size_t)min(min(tid, C - 1), p.L - 1) * H];
+    if constexpr (CF::VARIANT == 0) {
+        const size_t cbase = ((size_t)p.g * H + p.h) * DK + ch;
+        in.z0 = a.carry[cbase];
+        in.z1 = a.carry[cbase + 1];
+        if constexpr (NSEG > 1) {
+#pragma unroll
+            for (int ps = 0; ps < NSEG - 1; ++ps) {
+                const size_t sb = (((size_t)p.g * H + p.h) * (NSEG - 1) + ps) * DK + ch;
+                in.sgA0[ps] = a.segsum[sb];
+                in.sgA1[ps] = a.segsum[sb + 1];
+                in.sgG[ps] = *reinterpret_cast<const float2*>(a.seggam + sb);
+            }
+        }
+        const TI *ga = (const TI*)a.alpha, *gk = (const TI*)a.k, *gw = (const TI*)a.omega,
+                 *gq = (const TI*)a.q;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const size_t e = (row0 + (size_t)min(t0s + j, p.L - 1) * H) * DK + ch;
+            in.al[j] = *reinterpret_cast<const P2*>(ga + e);
+            in.kk[j] = *reinterpret_cast<const P2*>(gk + e);
+            in.ww[j] = *reinterpret_cast<const P2*>(gw + e);
+            in.qq[j] = *reinterpret_cast<const P2*>(gq + e);
+        }
+    }
+}
+
+template <class TI, class CF>
+__device__ __forceinline__ void prep_load_v(PrepIn<TI, CF>& in, const PrepArgs& a,
+                                            const PrepPos& p, int wave, int lane)
+{
+    using FC = Frag<typename CF::MT, CF::C>;
+    constexpr int DV = CF::DV;
+    const int H = a.H, li = lane & 15, lg = lane >> 4;
+    const size_t row0 = (size_t)p.c0 * H + p.h;
+    const TI* gv = (const TI*)a.v;
+#pragma unroll
+    for (int u = 0; u < CF::NUC; ++u) {
+        const int nt = min(wave + 4 * u, DV / 16 - 1);
+#pragma unroll
+        for (int s = 0; s < FC::NS; ++s) {
+            const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+#pragma unroll
+            for (int j = 0; j < VFrag<TI, typename CF::MT, CF::C>::NE; ++j)
+                in.vf[u][s].e[j] = gv[(row0 + (size_t)min(k0 + j, p.L - 1) * H) * DV + 16 * nt + li];
+        }
+    }
+}
+
+// Persistent: workgroup b takes the slots b, b + gridDim.x, ... of the segment (one (chunk,
+// head) each) and loads the next slot's inputs while it computes the current one.
 template <class TI, class CF>
 __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
 {
@@ -420,22 +586,14 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     constexpr bool APC = CF::APC;
     extern __shared__ __attribute__((aligned(16))) char smem[];
 
-    const int g = blockIdx.x, h = blockIdx.y, H = a.H;
-    int n, c0, L;
-    bool last;
-    if (!chunk_at(a.cu, a.choff, a.N, a.T, C, g, n, c0, L, &last)) return;
+    const int H = a.H;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int li = lane & 15, lg = lane >> 4;
-    const size_t row0 = (size_t)c0 * H + h;  // (token c0, head h)
     const TI* gq = (const TI*)a.q;
     const TI* gk = (const TI*)a.k;
-    const TI* gv = (const TI*)a.v;
     const TI* ga = (const TI*)a.alpha;
     const TI* gw = (const TI*)a.omega;
     const TI* gr = (const TI*)a.r;
-    char* recb = a.rec + ((size_t)g * H + h) * RC::BYTES;
-    MT* rec = (MT*)recb;
-    float* rec_gc = (float*)(recb + RC::GC_BYTES);
 
     float* Tm = (float*)(smem + CF::OFF_TM);
     MT* Ai = (MT*)(smem + CF::OFF_AI);
@@ -447,7 +605,7 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     MT* Wst = Qb;  // W staging once Q_bar has been copied out
     MT* Pb = (MT*)(smem + CF::OFF_PB);
     MT* KbT = (MT*)(smem + CF::OFF_KBT);
-    MT* PbT = (MT*)(smem + CF::OFF_PBT);  // isotropic variant only
+    MT* PbT = (MT*)(smem + CF::OFF_PBT);
     float* s_r = (float*)(smem + CF::OFF_SC);
     float* s_mr = s_r + C;
     float* s_rden = s_mr + C;
@@ -458,66 +616,30 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     float* s_alph = s_wtok + C;
     float* s_gC = s_alph + C;
 
-    // Every global load is issued here, up front and unconditionally (rows past the end of the
-    // sequence re-read its last row and are masked later), so that all of them are in flight
-    // together; values stay raw until used.
-    // r of the chunk's tokens
-    const TI rraw = gr[row0 + (size_t)min(min(tid, C - 1), L - 1) * H];
-    // B fragments of U = A V: wave w takes the value column blocks w, w + 4, ...
-    VFrag<TI, MT, C> vf[CF::NUC][FC::NS];
-#pragma unroll
-    for (int u = 0; u < CF::NUC; ++u) {
-        const int nt = min(wave + 4 * u, DV / 16 - 1);
-#pragma unroll
-        for (int s = 0; s < FC::NS; ++s) {
-            const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-#pragma unroll
-            for (int j = 0; j < VFrag<TI, MT, C>::NE; ++j)
-                vf[u][s].e[j] = gv[(row0 + (size_t)min(k0 + j, L - 1) * H) * DV + 16 * nt + li];
-        }
-    }
     // diagonal variant: wave s replays tokens [16 s, 16 s + 16) for the channel pair
     // (2 l, 2 l + 1) of lane l, from the chunk carry and the summaries of earlier segments
     constexpr int NSEG = CF::NSEG, NP = DK / 2;
     const int seg = wave, pc = lane;
     const bool dact = DIAG && seg < NSEG && pc < NP;
     const int ch = 2 * min(pc, NP - 1), t0s = 16 * min(seg, NSEG - 1);
-    float2 z0 = make_float2(1.f, 1.f), z1 = z0;
-    float4 sgA0[CF::NSG], sgA1[CF::NSG];
-    float2 sgG[CF::NSG];
-    unsigned al[16], kk[16], ww[16], qq[16];  // raw pairs (bf16) or first of a pair (fp32)
-    float2 alf[16], kkf[16], wwf[16], qqf[16];
-    if constexpr (DIAG) {
-        const size_t cbase = ((size_t)g * H + h) * DK + ch;
-        z0 = a.carry[cbase];
-        z1 = a.carry[cbase + 1];
-        if constexpr (NSEG > 1) {
-#pragma unroll
-            for (int ps = 0; ps < NSEG - 1; ++ps) {
-                const size_t sb = (((size_t)g * H + h) * (NSEG - 1) + ps) * DK + ch;
-                sgA0[ps] = a.segsum[sb];
-                sgA1[ps] = a.segsum[sb + 1];
-                sgG[ps] = *reinterpret_cast<const float2*>(a.seggam + sb);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const size_t e = (row0 + (size_t)min(t0s + j, L - 1) * H) * DK + ch;
-            if constexpr (sizeof(TI) == 2) {
-                al[j] = *reinterpret_cast<const unsigned*>(ga + e);
-                kk[j] = *reinterpret_cast<const unsigned*>(gk + e);
-                ww[j] = *reinterpret_cast<const unsigned*>(gw + e);
-                qq[j] = *reinterpret_cast<const unsigned*>(gq + e);
-            } else {
-                alf[j] = *reinterpret_cast<const float2*>(ga + e);
-                kkf[j] = *reinterpret_cast<const float2*>(gk + e);
-                wwf[j] = *reinterpret_cast<const float2*>(gw + e);
-                qqf[j] = *reinterpret_cast<const float2*>(gq + e);
-            }
-        }
-    }
+
+    PrepPos cur;
+    if (!prep_pos(a, C, blockIdx.x, cur)) return;
+    PrepIn<TI, CF> in;
+    prep_load_main<TI, CF>(in, a, cur, ch, t0s, tid);
+    for (int x = blockIdx.x;; x += gridDim.x) {
+    PrepPos nxt;
+    const bool more = prep_pos(a, C, x + gridDim.x, nxt);
+    if (!more) nxt = cur;  // the prefetch below then re-reads valid rows, unused
+    const int h = cur.h, n = cur.n, g = cur.g, c0 = cur.c0, L = cur.L;
+    const bool last = cur.last;
+    const size_t row0 = (size_t)c0 * H + h;  // (token c0, head h)
+    char* recb = a.rec + ((size_t)g * H + h) * RC::BYTES;
+    MT* rec = (MT*)recb;
+    float* rec_gc = (float*)(recb + RC::GC_BYTES);
+
     if (tid < C) {
-        const float rr = tid < L ? to_f32(rraw) : 1.f;
+        const float rr = tid < L ? to_f32(in.rraw) : 1.f;
         s_r[tid] = rr;
         s_mr[tid] = a.mu / rr;
         s_rden[tid] = 1.f;
@@ -527,38 +649,30 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     // ---- phase 1: variance replay and operands ------------------------------------------
     // Tokens past the end of the sequence act as alpha = 1, k = q = v = omega = 0: they leave
     // every state unchanged and give zero operand rows (and identity rows of A).
-    float pb0[16], pb1[16];  // P_bar of the lane's two channels (diagonal variant)
     if (DIAG) {
         if (dact) {
-            float zn0 = z0.x, zd0 = z0.y, zn1 = z1.x, zd1 = z1.y;
+            float zn0 = in.z0.x, zd0 = in.z0.y, zn1 = in.z1.x, zd1 = in.z1.y;
             float g0 = 1.f, g1 = 1.f;
             if constexpr (NSEG > 1) {
 #pragma unroll
                 for (int ps = 0; ps < NSEG - 1; ++ps) {
                     if (ps < seg) {
-                        const float4 A0 = sgA0[ps], A1 = sgA1[ps];
+                        const float4 A0 = in.sgA0[ps], A1 = in.sgA1[ps];
                         float nn = A0.x * zn0 + A0.y * zd0, dd = A0.z * zn0 + A0.w * zd0;
                         zn0 = nn; zd0 = dd; renorm2(zn0, zd0);
                         nn = A1.x * zn1 + A1.y * zd1; dd = A1.z * zn1 + A1.w * zd1;
                         zn1 = nn; zd1 = dd; renorm2(zn1, zd1);
-                        g0 *= sgG[ps].x;
-                        g1 *= sgG[ps].y;
+                        g0 *= in.sgG[ps].x;
+                        g1 *= in.sgG[ps].y;
                     }
                 }
             }
-            float kb0[16], kb1[16];
+            float kb0[16], kb1[16], pb0[16], pb1[16];
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
                 const int t = t0s + j;
-                float2 alv, kv, wv, qv;
-                if constexpr (sizeof(TI) == 2) {
-                    alv = make_float2(__uint_as_float(al[j] << 16), __uint_as_float(al[j] & 0xFFFF0000u));
-                    kv = make_float2(__uint_as_float(kk[j] << 16), __uint_as_float(kk[j] & 0xFFFF0000u));
-                    wv = make_float2(__uint_as_float(ww[j] << 16), __uint_as_float(ww[j] & 0xFFFF0000u));
-                    qv = make_float2(__uint_as_float(qq[j] << 16), __uint_as_float(qq[j] & 0xFFFF0000u));
-                } else {
-                    alv = alf[j]; kv = kkf[j]; wv = wwf[j]; qv = qqf[j];
-                }
+                float2 alv = unpack2(in.al[j]), kv = unpack2(in.kk[j]);
+                float2 wv = unpack2(in.ww[j]), qv = unpack2(in.qq[j]);
                 if (t >= L) {
                     alv = make_float2(1.f, 1.f);
                     kv = wv = qv = make_float2(0.f, 0.f);
@@ -584,6 +698,10 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
                 st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv.x, a.scale * g1 * qv.y);
                 st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
             }
+            store8<MT>(PbT + ch * LDC + t0s, pb0);
+            store8<MT>(PbT + ch * LDC + t0s + 8, pb0 + 8);
+            store8<MT>(PbT + (ch + 1) * LDC + t0s, pb1);
+            store8<MT>(PbT + (ch + 1) * LDC + t0s + 8, pb1 + 8);
             store8<MT>(KbT + ch * LDC + t0s, kb0);
             store8<MT>(KbT + ch * LDC + t0s + 8, kb0 + 8);
             store8<MT>(KbT + (ch + 1) * LDC + t0s, kb1);
@@ -703,6 +821,8 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
             if (tid < DK) s_gC[tid] = s_gtok[C - 1];
         }
     }
+    // the next slot's inputs (this thread is done with the current ones)
+    prep_load_main<TI, CF>(in, a, nxt, ch, t0s, tid);
     __syncthreads();
 
     // ---- phase 2: T = tril(K_bar P_bar^T, -1) / den and A_qk = tril(Q_bar P_bar^T) / den ---
@@ -749,22 +869,6 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
         }
     }
     __syncthreads();
-    // K_tail^T = gamma_C (.) P_bar^T / den (1/den is complete): the diagonal variant writes it
-    // from the phase-1 registers, 16-byte stores along each channel row
-    if (DIAG && dact) {
-        const float gc0 = s_gC[ch], gc1 = s_gC[ch + 1];
-        float k0[16], k1[16];
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const float rd = s_rden[t0s + j];
-            k0[j] = gc0 * pb0[j] * rd;
-            k1[j] = gc1 * pb1[j] * rd;
-        }
-        store8<MT>(rec + RC::KT + (size_t)ch * C + t0s, k0);
-        store8<MT>(rec + RC::KT + (size_t)ch * C + t0s + 8, k0 + 8);
-        store8<MT>(rec + RC::KT + (size_t)(ch + 1) * C + t0s, k1);
-        store8<MT>(rec + RC::KT + (size_t)(ch + 1) * C + t0s + 8, k1 + 8);
-    }
     // 2b: off-diagonal T blocks and every A_qk block, columns scaled by 1/den; T(ib, jb) and
     // A_qk(ib, jb) share the P_bar fragment of block column jb
     {
@@ -823,10 +927,14 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     }
     __syncthreads();
 
-    // ---- record: Q_bar, A_qk, gamma_C (and K_tail^T for the isotropic variant) ------------
+    // V fragments of this slot for phase 4 (loaded here so that they do not occupy registers
+    // during the replay; they land while the record is written and phase 3 runs)
+    prep_load_v<TI, CF>(in, a, cur, wave, lane);
+
+    // ---- record: Q_bar, A_qk, K_tail^T = gamma_C (.) P_bar^T / den, gamma_C ---------------
     copy_out<MT>(rec + RC::Q, Qb, C, DK, LDK, tid);
     copy_out<MT>(rec + RC::AQ, Aq, C, C, LDC, tid);
-    if (!DIAG) {
+    {
         constexpr int VE = 16 / (int)sizeof(MT);
         constexpr int VPR = C / VE;
         for (int idx = tid; idx < DK * VPR; idx += NT) {
@@ -906,7 +1014,7 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
                 typename FC::V bfr[FC::NS];
 #pragma unroll
                 for (int s = 0; s < FC::NS; ++s)
-                    bfr[s] = vfrag_pack<TI, MT, C>(vf[u][s], FC::KF * s + (FC::KF / 4) * lg, L);
+                    bfr[s] = vfrag_pack<TI, MT, C>(in.vf[u][s], FC::KF * s + (FC::KF / 4) * lg, L);
 #pragma unroll
                 for (int mt = 0; mt < NB; ++mt) {
                     floatx4 acc = zero4();
@@ -921,6 +1029,10 @@ __global__ __launch_bounds__(NT) void prep_kernel(PrepArgs a)
     }
     __syncthreads();
     copy_out<MT>(rec + RC::W, Wst, C, DK, LDK, tid);
+    if (!more) break;
+    __syncthreads();  // every LDS region is reused by the next slot
+    cur = nxt;
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -945,10 +1057,11 @@ struct StateCfg {
 struct StateArgs {
     const char* rec;
     const int32_t *cu, *choff;
-    const float* S0;
-    float* S_T;
+    const float* S0;  // state entering the segment (NULL = 0)
+    float* S_T;       // state leaving it (NULL = not stored)
     void* o;
     int N, T, H, DV;
+    int seg, nseg;
 };
 
 // Record fragments of one chunk for one wave, kept in storage precision until used (a
@@ -979,18 +1092,36 @@ struct ChunkFrags {
     float4 gc[CF::KB];
 };
 
-// Every load is unconditional (row blocks past the end re-read the last valid one, whose
-// values go unused), so the compiler can count them and let them fly across the next chunk's
-// compute instead of waiting at the first use.
 template <class CF>
-__device__ __forceinline__ void load_frags(ChunkFrags<CF>& F, const char* recb, int wave,
-                                           int lane, int col0)
+__device__ __forceinline__ void load_frags_early(ChunkFrags<CF>& F, const char* recb, int wave,
+                                                 int lane)
 {
     using MT = typename CF::MT;
     using RC = Rec<MT, CF::DK, CF::DV, CF::C>;
     using FK = Frag<MT, CF::DK>;
+    constexpr int DK = CF::DK;
+    const int li = lane & 15, lg = lane >> 4;
+    const MT* rec = (const MT*)recb;
+#pragma unroll
+    for (int mb = 0; mb < CF::MB; ++mb) {
+        const int row = 16 * min(wave + 4 * mb, CF::NB - 1) + li;
+#pragma unroll
+        for (int s = 0; s < FK::NS; ++s) {
+            const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+            F.w[mb][s] = FK::ld(rec + RC::W + (size_t)row * DK + k0);
+            F.q[mb][s] = FK::ld(rec + RC::Q + (size_t)row * DK + k0);
+        }
+    }
+}
+
+template <class CF>
+__device__ __forceinline__ void load_frags_late(ChunkFrags<CF>& F, const char* recb, int wave,
+                                                int lane, int col0)
+{
+    using MT = typename CF::MT;
+    using RC = Rec<MT, CF::DK, CF::DV, CF::C>;
     using FC = Frag<MT, CF::C>;
-    constexpr int DK = CF::DK, C = CF::C;
+    constexpr int C = CF::C;
     const int li = lane & 15, lg = lane >> 4;
     const MT* rec = (const MT*)recb;
     const float* gcp = (const float*)(recb + RC::GC_BYTES);
@@ -998,12 +1129,6 @@ __device__ __forceinline__ void load_frags(ChunkFrags<CF>& F, const char* recb, 
     for (int mb = 0; mb < CF::MB; ++mb) {
         const int mt = min(wave + 4 * mb, CF::NB - 1);
         const int row = 16 * mt + li;
-#pragma unroll
-        for (int s = 0; s < FK::NS; ++s) {
-            const int k0 = FK::KF * s + (FK::KF / 4) * lg;
-            F.w[mb][s] = FK::ld(rec + RC::W + (size_t)row * DK + k0);
-            F.q[mb][s] = FK::ld(rec + RC::Q + (size_t)row * DK + k0);
-        }
 #pragma unroll
         for (int s = 0; s < FC::NS; ++s)
             F.aq[mb][s] = FC::ld(rec + RC::AQ + (size_t)row * C + FC::KF * s + (FC::KF / 4) * lg);
@@ -1021,6 +1146,17 @@ __device__ __forceinline__ void load_frags(ChunkFrags<CF>& F, const char* recb, 
             F.kt[kb][s] = FC::ld(rec + RC::KT + (size_t)row * C + FC::KF * s + (FC::KF / 4) * lg);
         F.gc[kb] = *reinterpret_cast<const float4*>(gcp + 16 * it + 4 * lg);
     }
+}
+
+// Every load is unconditional (row blocks past the end re-read the last valid one, whose
+// values go unused), so the compiler can count them and let them fly across the compute of
+// the chunks in between instead of waiting at the first use.
+template <class CF>
+__device__ __forceinline__ void load_frags(ChunkFrags<CF>& F, const char* recb, int wave,
+                                           int lane, int col0)
+{
+    load_frags_early<CF>(F, recb, wave, lane);
+    load_frags_late<CF>(F, recb, wave, lane, col0);
 }
 
 // O rows of a finished chunk, staged in LDS by state_step, go out as 16-byte stores (rows past
@@ -1043,10 +1179,10 @@ __device__ __forceinline__ void store_o(const TI* Ost, TI* go, size_t row0, int 
 //   K_tail^T R, and S written back as the next chunk's B operand. The O tile of the previous
 //   chunk (row0p, Lp; Lp = 0 for none) is stored first.
 template <class TI, class CF>
-__device__ __forceinline__ void state_step(const ChunkFrags<CF>& F, floatx4 (&Sacc)[CF::KB][CF::NNT],
+__device__ __forceinline__ void state_step(ChunkFrags<CF>& F, floatx4 (&Sacc)[CF::KB][CF::NNT],
                                            typename CF::MT* SmT, typename CF::MT* RT, TI* Ost,
                                            TI* go, size_t row0p, int Lp, int H, int DV, int col0,
-                                           int wave, int lane)
+                                           int wave, int lane, const char* rec_next2)
 {
     using MT = typename CF::MT;
     using FK = Frag<MT, CF::DK>;
@@ -1088,6 +1224,8 @@ __device__ __forceinline__ void state_step(const ChunkFrags<CF>& F, floatx4 (&Sa
             }
         }
     }
+    // W and Q_bar of this set are consumed: the chunk two steps ahead reuses their registers
+    load_frags_early<CF>(F, rec_next2, wave, lane);
     __syncthreads();
 
     // B fragments of R, shared by the O and S products
@@ -1141,6 +1279,7 @@ __device__ __forceinline__ void state_step(const ChunkFrags<CF>& F, floatx4 (&Sa
                            Sacc[kb][nt][1], Sacc[kb][nt][2], Sacc[kb][nt][3]);
         }
     }
+    load_frags_late<CF>(F, rec_next2, wave, lane, col0);
     __syncthreads();
 }
 
@@ -1191,14 +1330,19 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
 
     int t0, t1;
     seq_range(a.cu, n, a.T, t0, t1);
-    const int nch = (t1 - t0 + C - 1) / C;
+    int mlo, mhi;  // this segment's chunks of the sequence
+    seg_range((t1 - t0 + C - 1) / C, a.seg, a.nseg, mlo, mhi);
     const int gbase = a.cu ? a.choff[n] : n * ((a.T + C - 1) / C);
     auto recp = [&](int m) { return a.rec + ((size_t)(gbase + m) * H + h) * RC::BYTES; };
 
-    // two fragment sets: chunk m + 1 loads while chunk m computes (the loads past the last
-    // chunk re-read it)
+    // two fragment sets used alternately; while chunk m computes with one, the other holds
+    // chunk m + 1, and each half of the first is reloaded with chunk m + 2 as soon as chunk m
+    // has consumed it (loads past the segment's last chunk re-read it)
     ChunkFrags<CF> F0, F1;
-    if (nch > 0) load_frags<CF>(F0, recp(0), wave, lane, col0);
+    if (mhi > mlo) {
+        load_frags<CF>(F0, recp(mlo), wave, lane, col0);
+        load_frags<CF>(F1, recp(min(mlo + 1, mhi - 1)), wave, lane, col0);
+    }
     // the first chunk's fragments are needed at once; waiting for them here, outside the loop,
     // also tells the compiler that nothing is in flight when the loop is entered, so the loop
     // head does not wait for the previous prefetch before issuing the next one
@@ -1206,17 +1350,15 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     __syncthreads();
     // chunk m's O goes out during chunk m + 1 (and after the loop for the last one)
     auto row_of = [&](int m) { return (size_t)(t0 + m * C) * H + h; };
-    auto len_of = [&](int m) { return m < 0 ? 0 : min(C, t1 - (t0 + m * C)); };
-    for (int m = 0; m < nch; m += 2) {
-        load_frags<CF>(F1, recp(min(m + 1, nch - 1)), wave, lane, col0);
-        state_step<TI, CF>(F0, Sacc, SmT, RT, Ost, go, row_of(m - 1), len_of(m - 1), H, DV, col0,
-                           wave, lane);
-        if (m + 1 >= nch) break;
-        load_frags<CF>(F0, recp(min(m + 2, nch - 1)), wave, lane, col0);
+    auto len_of = [&](int m) { return min(C, t1 - (t0 + m * C)); };
+    for (int m = mlo; m < mhi; m += 2) {
+        state_step<TI, CF>(F0, Sacc, SmT, RT, Ost, go, row_of(m - 1), m > mlo ? len_of(m - 1) : 0,
+                           H, DV, col0, wave, lane, recp(min(m + 2, mhi - 1)));
+        if (m + 1 >= mhi) break;
         state_step<TI, CF>(F1, Sacc, SmT, RT, Ost, go, row_of(m), len_of(m), H, DV, col0, wave,
-                           lane);
+                           lane, recp(min(m + 3, mhi - 1)));
     }
-    if (nch > 0) store_o<TI, CF>(Ost, go, row_of(nch - 1), len_of(nch - 1), H, DV, col0, tid);
+    if (mhi > mlo) store_o<TI, CF>(Ost, go, row_of(mhi - 1), len_of(mhi - 1), H, DV, col0, tid);
 
     if (a.S_T) {
         float* dst = a.S_T + (size_t)nh * DK * DV;
@@ -1245,23 +1387,33 @@ constexpr bool prep_fits()
            PrepCfg<TI, DK, DV, C, 1, false>::TOTAL <= 160 * 1024;
 }
 
+// Number of segments the chunks of every sequence are cut into (see seg_range): one for short
+// sequences, up to four when the longest possible sequence has 64 chunks or more.
+inline int pick_nseg(int T, int C)
+{
+    const int maxm = (T + C - 1) / C;  // chunks of the longest possible sequence
+    return std::max(1, std::min(4, maxm / 16));
+}
+
 // Workspace map of one call.
 struct WsMap {
-    size_t choff, chunksum, segsum, seggam, carry, rec, total;
+    size_t choff, segoff, chunksum, segsum, seggam, carry, S, rec, total;
 };
 
-inline WsMap ws_map(int variant, size_t maxch, int N, int H, int dk, size_t nseg_m1,
-                    size_t rec_bytes)
+inline WsMap ws_map(int variant, bool packed, size_t maxch, int N, int H, int dk, int dv,
+                    int nseg, size_t nseg16_m1, size_t rec_bytes)
 {
     const size_t nchan = variant == 0 ? (size_t)dk : 1;
     WsMap m;
     m.choff = 0;
-    m.chunksum = al256(((size_t)N + 1) * 4);
+    m.segoff = al256(((size_t)N + 1) * 4);
+    m.chunksum = m.segoff + (packed ? al256((size_t)nseg * (N + 1) * 4) : 0);
     m.segsum = m.chunksum + al256(maxch * H * nchan * 16);
-    const size_t nsg = variant == 0 ? maxch * H * nseg_m1 * dk : 0;
+    const size_t nsg = variant == 0 ? maxch * H * nseg16_m1 * dk : 0;
     m.seggam = m.segsum + al256(nsg * 16);
     m.carry = m.seggam + al256(nsg * 4);
-    m.rec = m.carry + al256(maxch * H * nchan * 8);
+    m.S = m.carry + al256(maxch * H * nchan * 8);
+    m.rec = m.S + (nseg > 1 ? al256((size_t)N * H * dk * dv * 4) : 0);
     m.total = m.rec + maxch * H * rec_bytes;
     return m;
 }
@@ -1277,8 +1429,34 @@ template <class TI, int DK, int DV, int C>
 size_t ws_bytes_t(int variant, bool packed, int N, int T, int H)
 {
     using MT = typename OpOf<TI>::type;
-    return ws_map(variant, max_chunks(packed, N, T, C), N, H, DK, C / 16 - 1,
-                  Rec<MT, DK, DV, C>::BYTES).total;
+    return ws_map(variant, packed, max_chunks(packed, N, T, C), N, H, DK, DV, pick_nseg(T, C),
+                  C / 16 - 1, Rec<MT, DK, DV, C>::BYTES).total;
+}
+
+// A second stream per device for the state pass, so that it overlaps the prep pass of the next
+// segment; created once, default priority, never destroyed.
+hipError_t side_stream(hipStream_t main, hipStream_t& side)
+{
+    int dev = 0;
+    hipError_t e = main ? hipStreamGetDevice(main, &dev) : hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    static std::mutex mu;
+    static hipStream_t streams[64] = {};
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!streams[dev]) {
+        int cur = 0;
+        if ((e = hipGetDevice(&cur)) != hipSuccess) return e;
+        if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+        e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+        if (cur != dev) (void)hipSetDevice(cur);
+        if (e != hipSuccess) {
+            streams[dev] = nullptr;
+            return e;
+        }
+    }
+    side = streams[dev];
+    return hipSuccess;
 }
 
 template <class TI, int DK, int DV, int C, int VARIANT, bool APC>
@@ -1290,21 +1468,31 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
     constexpr int BV = DV >= 32 ? 32 : DV;
     using SC = StateCfg<TI, DK, DV, BV, C>;
     const SeqArgs& sa = fc.sa;
-    const size_t maxch = max_chunks(sa.cu_seqlens != nullptr, sa.N, sa.T, C);
+    const bool packed = sa.cu_seqlens != nullptr;
+    const size_t maxch = max_chunks(packed, sa.N, sa.T, C);
     if (maxch == 0) return hipSuccess;
-    const WsMap wm = ws_map(VARIANT, maxch, sa.N, sa.H, DK, C / 16 - 1, RC::BYTES);
+    const int nseg = pick_nseg(sa.T, C);
+    const WsMap wm = ws_map(VARIANT, packed, maxch, sa.N, sa.H, DK, DV, nseg, C / 16 - 1,
+                            RC::BYTES);
     char* ws = (char*)fc.workspace;
     int32_t* choff = (int32_t*)(ws + wm.choff);
+    int32_t* segoff = (int32_t*)(ws + wm.segoff);
     float4* chunksum = (float4*)(ws + wm.chunksum);
     float4* segsum = (float4*)(ws + wm.segsum);
     float* seggam = (float*)(ws + wm.seggam);
     float2* carry = (float2*)(ws + wm.carry);
+    float* Sws = (float*)(ws + wm.S);
     char* rec = ws + wm.rec;
     const TI *k = (const TI*)fc.k, *al = (const TI*)fc.alpha, *om = (const TI*)fc.omega,
              *r = (const TI*)fc.r;
     hipError_t e;
-    if (sa.cu_seqlens && (e = launch_chunk_table(sa.cu_seqlens, sa.N, C, choff, st)) != hipSuccess)
-        return e;
+
+    // 1-2: chunk summaries and carries (every chunk of every sequence)
+    if (packed) {
+        if ((e = launch_chunk_table(sa.cu_seqlens, sa.N, C, choff, st)) != hipSuccess) return e;
+        hipLaunchKernelGGL(seg_table_kernel, dim3(1), dim3(1), 0, st, sa.cu_seqlens, sa.N, C,
+                           nseg, segoff);
+    }
     const dim3 grid((unsigned)maxch, sa.H);
     if (VARIANT == 0)
         hipLaunchKernelGGL((summary_diag_kernel<TI, DK, C>), grid, dim3(NT), 0, st, k, al, om, r,
@@ -1318,28 +1506,80 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
                                fc.P_T, st)) != hipSuccess)
         return e;
 
-    static bool attr_done = false;  // one attribute call per instantiation and process
-    if (!attr_done) {
+    // persistent prep: as many workgroups as fit on the device at once (queried once per
+    // instantiation and device; the LDS map usually allows one per CU)
+    static int prep_slots[64] = {};
+    int dev = 0;
+    if ((e = st ? hipStreamGetDevice(st, &dev) : hipGetDevice(&dev)) != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (!prep_slots[dev]) {
         if ((e = hipFuncSetAttribute((const void*)prep_kernel<TI, PC>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)PC::TOTAL)) != hipSuccess)
             return e;
-        attr_done = true;
+        int per_cu = 0, ncu = 0;
+        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                 &per_cu, prep_kernel<TI, PC>, NT, PC::TOTAL)) != hipSuccess)
+            return e;
+        if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) !=
+            hipSuccess)
+            return e;
+        prep_slots[dev] = std::max(1, per_cu) * std::max(1, ncu);
     }
     PrepArgs pa;
     pa.q = fc.q; pa.k = fc.k; pa.v = fc.v; pa.alpha = fc.alpha; pa.omega = fc.omega; pa.r = fc.r;
     pa.cu = sa.cu_seqlens; pa.choff = choff; pa.carry = carry; pa.segsum = segsum;
     pa.seggam = seggam; pa.P_T = fc.P_T; pa.rec = rec; pa.N = sa.N; pa.T = sa.T; pa.H = sa.H;
-    pa.mu = fc.mu; pa.scale = fc.scale;
-    hipLaunchKernelGGL((prep_kernel<TI, PC>), grid, dim3(NT), PC::TOTAL, st, pa);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-
+    pa.nseg = nseg; pa.mu = fc.mu; pa.scale = fc.scale;
     StateArgs sta;
-    sta.rec = rec; sta.cu = sa.cu_seqlens; sta.choff = choff; sta.S0 = fc.S0; sta.S_T = fc.S_T;
-    sta.o = fc.o; sta.N = sa.N; sta.T = sa.T; sta.H = sa.H; sta.DV = DV;
+    sta.rec = rec; sta.cu = sa.cu_seqlens; sta.choff = choff; sta.o = fc.o; sta.N = sa.N;
+    sta.T = sa.T; sta.H = sa.H; sta.DV = DV; sta.nseg = nseg;
     const unsigned nblk = (unsigned)((size_t)sa.N * sa.H * (DV / BV));
-    hipLaunchKernelGGL((state_kernel<TI, SC>), dim3(nblk), dim3(NT), SC::TOTAL, st, sta);
-    return hipGetLastError();
+
+    // 3-4: per segment, prep on the caller's stream, then the state pass on the side stream
+    // (ordered after that prep and after the previous segment's state pass)
+    hipStream_t side = st;
+    if (nseg > 1 && (e = side_stream(st, side)) != hipSuccess) return e;
+    hipEvent_t ev[5] = {};
+    if (nseg > 1)
+        for (int i = 0; i <= nseg; ++i)
+            if ((e = hipEventCreateWithFlags(&ev[i], hipEventDisableTiming)) != hipSuccess) {
+                for (int j = 0; j < i; ++j) (void)hipEventDestroy(ev[j]);
+                return e;
+            }
+    for (int sg = 0; sg < nseg && e == hipSuccess; ++sg) {
+        pa.seg = sg;
+        pa.segoff = segoff + (size_t)sg * (sa.N + 1);
+        unsigned npg;
+        if (packed) {
+            npg = (unsigned)(maxch / nseg + sa.N);
+        } else {
+            const int ncs = (sa.T + C - 1) / C;
+            npg = (unsigned)((size_t)sa.N * (((size_t)(sg + 1) * ncs) / nseg - ((size_t)sg * ncs) / nseg));
+        }
+        const size_t nslot = (size_t)npg * sa.H;
+        if (nslot > 0)
+            hipLaunchKernelGGL((prep_kernel<TI, PC>),
+                               dim3((unsigned)std::min<size_t>(nslot, prep_slots[dev])), dim3(NT),
+                               PC::TOTAL, st, pa);
+        if ((e = hipGetLastError()) != hipSuccess) break;
+        if (nseg > 1) {
+            if ((e = hipEventRecord(ev[sg], st)) != hipSuccess) break;
+            if ((e = hipStreamWaitEvent(side, ev[sg], 0)) != hipSuccess) break;
+        }
+        sta.seg = sg;
+        sta.S0 = sg == 0 ? fc.S0 : Sws;
+        sta.S_T = sg == nseg - 1 ? fc.S_T : Sws;
+        hipLaunchKernelGGL((state_kernel<TI, SC>), dim3(nblk), dim3(NT), SC::TOTAL, side, sta);
+        e = hipGetLastError();
+    }
+    if (nseg > 1) {
+        // the caller's stream resumes after the last state pass
+        if (e == hipSuccess) e = hipEventRecord(ev[nseg], side);
+        if (e == hipSuccess) e = hipStreamWaitEvent(st, ev[nseg], 0);
+        for (int i = 0; i <= nseg; ++i) (void)hipEventDestroy(ev[i]);
+    }
+    return e;
 }
 
 template <class TI, int DK, int DV, int C>

@@ -136,7 +136,8 @@ __global__ __launch_bounds__(DK) void diag_summary_kernel(
 }
 
 // Pass 2: per (sequence, head, channel) exclusive scan of the summaries over chunks of cg
-// tokens. One wavefront per channel; lanes are chunks; blocks of 64 chunks carry into the next.
+// tokens. Grid (sequence x head, channel groups of 4); one wavefront per channel, lanes are
+// chunks, blocks of 64 chunks carry into the next.
 __global__ __launch_bounds__(256) void carry_scan_kernel(
     const float4* __restrict__ summ, const float* __restrict__ P0,
     const int32_t* __restrict__ cu, const int32_t* __restrict__ choff, int N, int T, int H,
@@ -149,15 +150,16 @@ __global__ __launch_bounds__(256) void carry_scan_kernel(
     const int nch = (t1 - t0 + cg - 1) / cg;
     const int g0 = cu ? choff[n] : n * ((T + cg - 1) / cg);
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int c = 4 * blockIdx.y + w;  // one channel per wavefront
+    if (c >= nchan) return;
     if (nch == 0) {  // an empty sequence keeps its initial variances
-        if (P_T)
-            for (int c = threadIdx.x; c < nchan; c += blockDim.x) {
-                const size_t pidx = ((size_t)n * H + h) * nchan + c;
-                P_T[pidx] = P0 ? P0[pidx] : 1.f;
-            }
+        if (P_T && lane == 0) {
+            const size_t pidx = ((size_t)n * H + h) * nchan + c;
+            P_T[pidx] = P0 ? P0[pidx] : 1.f;
+        }
         return;
     }
-    for (int c = w; c < nchan; c += 4) {
+    {
         const size_t pidx = ((size_t)n * H + h) * nchan + c;
         float cn = P0 ? P0[pidx] : 1.f, cd = 1.f;  // z_0 = [p_0; 1]
         for (int b0 = 0; b0 < nch; b0 += 64) {
@@ -357,8 +359,8 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, false>), grid, dim3(64), 0, st, k_, a_,
                            w_, r_, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, summ);
     }
-    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H), dim3(256), 0, st, summ, P0,
-                       sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, CG, carry, P_T);
+    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H, (nchan + 3) / 4), dim3(256), 0, st,
+                       summ, P0, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, CG, carry, P_T);
     if (variant == 0) {
         hipLaunchKernelGGL((diag_emit_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
                            carry, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, gain_out,
@@ -406,8 +408,8 @@ hipError_t launch_carry_scan(const float4* summ, const float* P0, const SeqArgs&
                              int cg, const int32_t* choff, float2* carry, float* P_T,
                              hipStream_t st)
 {
-    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H), dim3(256), 0, st, summ, P0,
-                       sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, cg, carry, P_T);
+    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H, (nchan + 3) / 4), dim3(256), 0, st,
+                       summ, P0, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, cg, carry, P_T);
     return hipGetLastError();
 }
 
