@@ -8,9 +8,10 @@ batch 4 as in its throughput probe). Inputs are seeded synthetic tensors residen
 timing starts. One step = one full forward over the batch (every stage of the path: variance
 scan, gains, chunkwise WY solve, state passing, outputs, final states).
 
-Prints one JSON line with tokens/s, the roofline position of the forward kernel (algorithmic
-bytes per launch / its HIP-event duration against the 8 TB/s HBM peak) and the CPU oracle timed
-on a bounded sample of the same workload.
+Prints one JSON line with tokens/s, the roofline position of one forward call (its kernels run
+on two streams: algorithmic bytes per call / the HIP-event duration of the call on the caller's
+stream, against the 8 TB/s HBM peak) and the CPU oracle timed on a bounded sample of the same
+workload.
 """
 
 from __future__ import annotations
@@ -49,13 +50,13 @@ def algorithmic_flops(B, T, H, dk, dv, C=64):
     return B * T * H * (6 * d * dv + 10 * C * d + C * C / 3.0)
 
 
-PROFILE = os.path.join(ROOT, "profiles", "kdn_fwd_kernel_diag_B4_T4096_H16_d128.json")
+PROFILE = os.path.join(ROOT, "profiles", "kdn_forward_diag_B4_T4096_H16_d128.json")
 
 
 def measured_traffic():
-    """HBM bytes per launch from the committed rocprofv3 counter summary (FETCH_SIZE and
-    WRITE_SIZE scaled by a plain copy of known size), or None when the summary is missing or
-    was taken from a different version of the kernel source."""
+    """HBM bytes per forward from the committed rocprofv3 counter summary (FETCH_SIZE and
+    WRITE_SIZE of every kernel of the forward, scaled by a plain copy of known size), or None
+    when the summary is missing or was taken from a different version of the kernel sources."""
     try:
         from paper_2609_07816_amd.rocprof_summary import source_hash
         with open(PROFILE) as f:
@@ -145,8 +146,10 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K steps between two synchronisations; per-launch HIP events on the stream
-    # the kernel runs on (torch's current stream, which the binding passes to the library)
+    # timed region: K steps between two synchronisations; HIP events around every forward
+    # call on torch's current stream, which the binding passes to the library (the call ends
+    # with that stream waiting for the library's second stream, so the end event follows the
+    # last kernel of the call)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
