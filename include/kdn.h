@@ -55,7 +55,9 @@ typedef enum { KDN_F32 = 0, KDN_BF16 = 1 } kdn_dtype_t;
  *   p_hat = alpha^2 * p + omega;  kappa = p_hat * k / (r + sum_i p_hat_i k_i^2)
  *   S = diag(alpha) S + kappa (v - (diag(alpha) S)^T k)^T;  o = scale * S^T q
  *   p = p_hat / (1 + mu k^2 / r * p_hat)
- * evaluated chunkwise (App. "Hardware-Efficient Chunkwise Algorithm").
+ * evaluated chunkwise (App. "Hardware-Efficient Chunkwise Algorithm"): one workgroup walks each
+ * (sequence, head, block of value columns) through its chunks in order, carrying S and the
+ * variance chain, so only the inputs, o and the final states cross device memory.
  *   q, k, alpha, omega: [B,T,H,dk]; v, o: [B,T,H,dv]; r: [B,T,H]   (dtype)
  *   S0, S_T: [N,H,dk,dv] float32;  P0, P_T: [N,H,dk] float32
  *   mu > 0 (the paper uses mu = dk); scale > 0 (the paper uses dk^-1/2).
@@ -92,11 +94,11 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
  * Device scratch (bytes) that kdn_forward_diag (variant 0) / kdn_forward_iso (variant 1) need
  * for these sizes; packed != 0 for a packed batch (cu_seqlens given), chunk as passed to the
  * forward (0 = the library's choice). Returns 0 for arguments the forward rejects. The scratch
- * carries, between the forward's passes, the variance-chain summaries and carries of every
- * chunk (App. "Hardware-Efficient Chunkwise Algorithm", eqs. chunk-gain-summary and
- * chunk-gain-carry) and every (chunk, head)'s WY factors W, Q_bar, K_tail, A_qk, U and
- * gamma_C (Sec. "Chunkwise Memory Scan"). It needs no initialisation and is dead once the
- * forward's work on the stream has finished; two forwards in flight at once need two.
+ * holds the order in which the sequences of a packed batch are walked (longest first) and, for
+ * an in-place variance update (P_T == P0), a copy of P0 taken before the walk starts. It is
+ * small (at most 4 (N + 1) + 4 N H dk bytes, rounded up to 256), needs no initialisation and
+ * is dead once the forward's work on the stream has finished; two forwards in flight at once
+ * need two.
  */
 size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
                                    int32_t dk, int32_t dv, kdn_dtype_t dtype, int32_t packed,

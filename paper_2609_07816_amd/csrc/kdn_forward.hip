@@ -1,0 +1,946 @@
+// Fused chunkwise forward of Diagonal / Isotropic KDN on gfx950.
+//
+// arXiv 2609.07816, App. "Hardware-Efficient Chunkwise Algorithm". Tokens are cut into chunks of
+// C (chunks restart at every sequence start; the last one may be partial). One workgroup walks
+// one (sequence, head, tile of BV value columns) through its chunks in order and carries both
+// recurrent states with it:
+//   - the variance chain as homogeneous Moebius pairs z = (n, d), p = n / d, one per key channel
+//     (diagonal) or one per head (isotropic): eqs. kla-box-mobius / iso-kla-box-mobius, with the
+//     carry between chunks of eq. chunk-gain-carry;
+//   - the memory S: float32 MFMA accumulators, plus a copy in operand precision in LDS that is
+//     the next chunk's MFMA operand.
+// Only the inputs, o and the final states cross HBM.
+//
+// Per chunk, with chunk-local token t and gamma_t = prod_{j<=t} alpha_j (per channel):
+//   1. variance (VALU): the chunk is cut into NW segments of C / NW tokens (one per wave); each
+//      wave composes its segment's token matrices (eq. chunk-gain-summary), the segment carries
+//      follow from the chunk carry (eq. chunk-gain-local-prefix), and each wave replays its
+//      tokens (eq. chunk-gain-emission) to get p_hat_t (diagonal) or b_hat_t and
+//      beta_t = b_hat_t / (r_t + b_hat_t ||k_t||^2) (isotropic);
+//   2. operands: K_bar = Gamma (.) K, Q_bar = scale Gamma (.) Q, P_bar = G (.) K (/) Gamma with
+//      G = p_hat (diagonal) or beta (isotropic);
+//   3. L = diag(c) + tril(K_bar P_bar^T, -1) with c_t = r_t + (K_bar P_bar^T)_tt
+//      = r_t + sum_i p_hat_ti k_ti^2 (diagonal, the innovation variance of eq. kla-box-gain) or
+//      c_t = 1 (isotropic); A = L^-1; A_qk = tril(Q_bar P_bar^T) (diagonal included: the read
+//      follows the write);
+//   4. R = A (V - K_bar S)   (row t: token t's innovation divided by c_t),
+//      O = Q_bar S + A_qk R,  S <- gamma_C (.) (S + P_bar^T R).
+// This is Sec. "Chunkwise Memory Scan" (R = U - W S with W = A K_bar and U = A V, K_tail =
+// (gamma_C / gamma) (.) kappa) with the gain's normalisation kappa_t = p_hat_t (.) k_t / c_t
+// moved into the triangular solve: the unit-lower I + T of the section becomes L, and W, U are
+// never formed.
+//
+// Dense products run on MFMA (bf16 operands with float32 accumulation for bf16 inputs, float32
+// MFMA for float32 inputs); S, the variance chain and the triangular solve stay in float32.
+#include <algorithm>
+#include <atomic>
+#include <type_traits>
+
+#include "kdn_device.h"
+
+namespace kdn {
+namespace {
+
+constexpr int NW = 8;         // waves per workgroup
+constexpr int NTH = 64 * NW;  // threads per workgroup
+
+constexpr size_t al16(size_t x) { return (x + 15) & ~(size_t)15; }
+constexpr size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t cmax(size_t a, size_t b) { return a > b ? a : b; }
+
+template <class TI> struct OpOf { using type = bf16; };
+template <> struct OpOf<float> { using type = float; };
+
+// ------------------------------------------------------------------------------------------
+// MFMA fragments read from LDS: lane (g, i) holds KF/4 consecutive k values of row i (A side)
+// or of column i (B side, stored transposed); one fragment feeds one bf16 MFMA (KF = 32 or 16)
+// or four float32 MFMAs (KF = 16). Both sides use the same k assignment, so the contraction is
+// exact whatever order the unit applies internally. Result: acc[r] = D[4 g + r][i].
+// ------------------------------------------------------------------------------------------
+template <class MT, int K> struct Frag;
+
+template <int K> struct Frag<bf16, K> {
+    static constexpr int KF = (K % 32 == 0) ? 32 : 16;
+    static constexpr int NS = K / KF;
+    using V = typename std::conditional<KF == 32, uint4, uint2>::type;
+    __device__ static V ld(const bf16* p) { return *reinterpret_cast<const V*>(p); }
+    __device__ static floatx4 mma(floatx4 acc, V a, V b)
+    {
+        if constexpr (KF == 32)
+            return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                           __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                           0, 0);
+        else
+            return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, a),
+                                                              __builtin_bit_cast(bf16x4, b), acc,
+                                                              0, 0, 0);
+    }
+};
+
+template <int K> struct Frag<float, K> {
+    static constexpr int KF = 16;
+    static constexpr int NS = K / KF;
+    using V = uint4;
+    __device__ static V ld(const float* p) { return *reinterpret_cast<const V*>(p); }
+    __device__ static floatx4 mma(floatx4 acc, V a, V b)
+    {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x),
+                                                    acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y),
+                                                    acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z),
+                                                    acc, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w),
+                                                     acc, 0, 0, 0);
+    }
+};
+
+// Four values (rows 4g..4g+3 of a result column, or four consecutive elements) in MT.
+template <class MT>
+__device__ __forceinline__ void store4(MT* dst, float x0, float x1, float x2, float x3)
+{
+    if constexpr (std::is_same<MT, float>::value) {
+        *reinterpret_cast<float4*>(dst) = make_float4(x0, x1, x2, x3);
+    } else {
+        bf16x4 v;
+        v[0] = (bf16)x0; v[1] = (bf16)x1; v[2] = (bf16)x2; v[3] = (bf16)x3;
+        *reinterpret_cast<bf16x4*>(dst) = v;
+    }
+}
+
+// N consecutive values (N = 2, 4 or 8; the destination is aligned to N elements).
+template <class MT, int N>
+__device__ __forceinline__ void storeN(MT* dst, const float* x)
+{
+    if constexpr (N == 8) store8<MT>(dst, x);
+    else if constexpr (N == 4) store4<MT>(dst, x[0], x[1], x[2], x[3]);
+    else st2<MT>(dst, x[0], x[1]);
+}
+
+// Two adjacent inputs from one raw word (bf16 pair) or a float pair.
+__device__ __forceinline__ float2 unpack2(unsigned u)
+{
+    return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xFFFF0000u));
+}
+__device__ __forceinline__ float2 unpack2(float2 v) { return v; }
+
+// z <- M z for a 2x2 matrix M = [x y; z w] (float4) acting on a homogeneous pair.
+__device__ __forceinline__ float2 mat_vec(const float4& m, float2 v)
+{
+    float n = fmaf(m.x, v.x, m.y * v.y), d = fmaf(m.z, v.x, m.w * v.y);
+    renorm2(n, d);
+    return make_float2(n, d);
+}
+
+// ------------------------------------------------------------------------------------------
+// Configuration and LDS map of one workgroup.
+// ------------------------------------------------------------------------------------------
+template <class TI, int DK_, int DV_, int BV_, int C_, int VARIANT_, bool APC_>
+struct WalkCfg {
+    using MT = typename OpOf<TI>::type;
+    using P2 = typename std::conditional<sizeof(TI) == 2, unsigned, float2>::type;
+    static constexpr int DK = DK_, DV = DV_, BV = BV_, C = C_, VARIANT = VARIANT_;
+    static constexpr bool DIAG = VARIANT_ == 0;
+    static constexpr bool APC = APC_ || DIAG;   // gates per key channel
+    static constexpr int NV = DV / BV;          // value tiles (workgroups) per head
+    static constexpr int SL = C / NW;           // tokens per variance segment (one per wave)
+    static constexpr int NP = DK / 2;           // key-channel pairs (one per lane)
+    static constexpr int NB = C / 16, NNT = BV / 16, NKT = DK / 16;
+    static constexpr int NXT = NB * NNT, XPW = (NXT + NW - 1) / NW;  // X / O tiles
+    static constexpr int NST = NKT * NNT, SPW = (NST + NW - 1) / NW;  // S tiles
+    static constexpr int NLU = NB * (NB + 1) / 2;                      // lower block pairs
+    static constexpr int PAD = 16 / (int)sizeof(MT);  // one 16-byte pad per row
+    static constexpr int LDK = DK + PAD, LDC = C + PAD, LDT = C + 4, LDI = 16 + PAD;
+    static constexpr int LDO = BV + 16 / (int)sizeof(TI);
+    static constexpr size_t SZ_OP = al16((size_t)C * LDK * sizeof(MT));
+    static constexpr size_t SZ_CC = al16((size_t)C * LDC * sizeof(MT));
+    // operands of the chunk: K_bar, Q_bar, P_bar [C][LDK] and P_bar^T [DK][LDC]
+    static constexpr size_t OFF_KB = 0;
+    static constexpr size_t OFF_QB = OFF_KB + SZ_OP;
+    static constexpr size_t OFF_PB = OFF_QB + SZ_OP;
+    static constexpr size_t OFF_PBT = OFF_PB + SZ_OP;
+    // one region holding either the chunk's triangular matrices (L float32 [C][LDT]; A, A^T,
+    // A_qk [C][LDC]) or, while the variance runs, the segment summaries
+    static constexpr size_t OFF_U = OFF_PBT + al16((size_t)DK * LDC * sizeof(MT));
+    static constexpr size_t OFF_LM = OFF_U;
+    static constexpr size_t OFF_AI = OFF_LM + al16((size_t)C * LDT * 4);
+    static constexpr size_t OFF_AIT = OFF_AI + SZ_CC;
+    static constexpr size_t OFF_AQ = OFF_AIT + SZ_CC;
+    static constexpr size_t SZ_MAT = OFF_AQ + SZ_CC - OFF_U;
+    static constexpr size_t OFF_SGA = OFF_U;                           // float4 [NW][DK]
+    static constexpr size_t OFF_SGG = OFF_SGA + (size_t)NW * DK * 16;  // float [NW][DK]
+    static constexpr size_t SZ_SEG = (size_t)NW * DK * 20;
+    static constexpr size_t OFF_INV = OFF_U + al16(cmax(SZ_MAT, SZ_SEG));
+    // S^T [BV][LDK], X^T and R^T [BV][LDC] in MT, O staging [C][LDO] in TI
+    static constexpr size_t OFF_SMT = OFF_INV + al16((size_t)NB * 16 * LDI * sizeof(MT));
+    static constexpr size_t OFF_XT = OFF_SMT + al16((size_t)BV * LDK * sizeof(MT));
+    static constexpr size_t OFF_RT = OFF_XT + al16((size_t)BV * LDC * sizeof(MT));
+    static constexpr size_t OFF_O = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));
+    // variance carry (two buffers, by chunk parity), gamma_C, r and mu / r of the chunk
+    static constexpr size_t OFF_CAR = OFF_O + al16((size_t)C * LDO * sizeof(TI));
+    static constexpr size_t OFF_GC = OFF_CAR + (size_t)2 * DK * 8;
+    static constexpr size_t OFF_R = OFF_GC + (size_t)DK * 4;
+    static constexpr size_t OFF_MR = OFF_R + (size_t)C * 4;
+    static constexpr size_t TOTAL = al16(OFF_MR + (size_t)C * 4);
+};
+
+struct WalkArgs {
+    const void *q, *k, *v, *alpha, *omega, *r;
+    const float *S0, *P0;
+    void* o;
+    float *S_T, *P_T;
+    const int32_t* cu;     // packed batches: sequence offsets, else nullptr
+    const int32_t* order;  // packed batches: sequences, longest first (nullptr: in order)
+    int N, T, H;
+    float mu, scale;
+};
+
+// Raw inputs of one chunk held by one lane, loaded a chunk ahead and kept in storage precision
+// (a conversion next to its load would make the load wait for everything issued before it).
+// Lane l of wave w holds tokens [SL w, SL w + SL) of the key-channel pair (2 l, 2 l + 1).
+template <class TI, class CF>
+struct WalkIn {
+    using P2 = typename CF::P2;
+    P2 kk[CF::SL], qq[CF::SL];
+    P2 al[CF::APC ? CF::SL : 1];    // per-channel gates
+    P2 ww[CF::DIAG ? CF::SL : 1];   // per-channel process noise (diagonal)
+    TI als[CF::APC ? 1 : CF::SL];   // one gate per head (isotropic, scalar gates)
+    TI ws[CF::DIAG ? 1 : CF::SL];   // one process noise per head (isotropic)
+    TI rr;                          // r of token tid (tid < C)
+    TI vv[CF::XPW][4];              // V at this lane's rows and column of its X tiles
+};
+
+template <class TI, class CF>
+__device__ __forceinline__ void load_main(WalkIn<TI, CF>& in, const WalkArgs& a, int c0, int L,
+                                          int h, int ch, int wave, int tid)
+{
+    using P2 = typename CF::P2;
+    constexpr int DK = CF::DK, SL = CF::SL;
+    const int H = a.H;
+    const TI *gq = (const TI*)a.q, *gk = (const TI*)a.k, *ga = (const TI*)a.alpha,
+             *gw = (const TI*)a.omega, *gr = (const TI*)a.r;
+    // rows past the end of the sequence re-read its last row; their values are masked
+    in.rr = gr[(size_t)(c0 + min(min(tid, CF::C - 1), L - 1)) * H + h];
+#pragma unroll
+    for (int j = 0; j < SL; ++j) {
+        const size_t row = (size_t)(c0 + min(SL * wave + j, L - 1)) * H + h;
+        const size_t e = row * DK + ch;
+        in.kk[j] = *reinterpret_cast<const P2*>(gk + e);
+        in.qq[j] = *reinterpret_cast<const P2*>(gq + e);
+        if constexpr (CF::APC) in.al[j] = *reinterpret_cast<const P2*>(ga + e);
+        else in.als[j] = ga[row];
+        if constexpr (CF::DIAG) in.ww[j] = *reinterpret_cast<const P2*>(gw + e);
+        else in.ws[j] = gw[row];
+    }
+}
+
+template <class TI, class CF>
+__device__ __forceinline__ void load_v(WalkIn<TI, CF>& in, const WalkArgs& a, int c0, int L,
+                                       int h, int col0, int wave, int lane)
+{
+    const int H = a.H, li = lane & 15, lg = lane >> 4;
+    const TI* gv = (const TI*)a.v;
+#pragma unroll
+    for (int j = 0; j < CF::XPW; ++j) {
+        const int x = min(wave + NW * j, CF::NXT - 1);
+        const int mt = x % CF::NB, nt = x / CF::NB;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            const size_t row = (size_t)(c0 + min(16 * mt + 4 * lg + rr, L - 1)) * H + h;
+            in.vv[j][rr] = gv[row * CF::DV + col0 + 16 * nt + li];
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// The walk: one workgroup per (sequence, head, value tile).
+// ------------------------------------------------------------------------------------------
+template <class TI, class CF>
+__global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
+{
+    using MT = typename CF::MT;
+    using FK = Frag<MT, CF::DK>;
+    using FC = Frag<MT, CF::C>;
+    constexpr int DK = CF::DK, DV = CF::DV, BV = CF::BV, C = CF::C, SL = CF::SL, NP = CF::NP;
+    constexpr int NB = CF::NB, LDK = CF::LDK, LDC = CF::LDC, LDT = CF::LDT, LDO = CF::LDO;
+    constexpr bool DIAG = CF::DIAG, APC = CF::APC;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    MT* Kb = (MT*)(smem + CF::OFF_KB);
+    MT* Qb = (MT*)(smem + CF::OFF_QB);
+    MT* Pb = (MT*)(smem + CF::OFF_PB);
+    MT* PbT = (MT*)(smem + CF::OFF_PBT);
+    float* Lm = (float*)(smem + CF::OFF_LM);
+    MT* Ai = (MT*)(smem + CF::OFF_AI);
+    MT* AiT = (MT*)(smem + CF::OFF_AIT);
+    MT* Aq = (MT*)(smem + CF::OFF_AQ);
+    float4* segA = (float4*)(smem + CF::OFF_SGA);
+    float* segG = (float*)(smem + CF::OFF_SGG);
+    MT* Inv = (MT*)(smem + CF::OFF_INV);
+    MT* SmT = (MT*)(smem + CF::OFF_SMT);
+    MT* XT = (MT*)(smem + CF::OFF_XT);
+    MT* RT = (MT*)(smem + CF::OFF_RT);
+    TI* Ost = (TI*)(smem + CF::OFF_O);
+    float2* carry = (float2*)(smem + CF::OFF_CAR);
+    float* gC = (float*)(smem + CF::OFF_GC);
+    float* s_r = (float*)(smem + CF::OFF_R);
+    float* s_mr = (float*)(smem + CF::OFF_MR);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int li = lane & 15, lg = lane >> 4;
+
+    // block -> (sequence-head slot, value tile): the NV tiles of one head get block indices
+    // congruent modulo 8, so round-robin dispatch puts them on one XCD, where they share the
+    // L2 copy of the head's inputs
+    const int NH = a.N * a.H;
+    const int xcd = (int)(blockIdx.x % 8), rest = (int)(blockIdx.x / 8);
+    const int vt = rest % CF::NV, slot = (rest / CF::NV) * 8 + xcd;
+    if (slot >= NH) return;
+    const int H = a.H;
+    const int n = a.order ? a.order[slot / H] : slot / H;
+    const int h = slot % H;
+    if (n < 0 || n >= a.N) return;
+    const int nh = n * H + h;
+    const int col0 = vt * BV;
+    int t0, t1;
+    seq_range(a.cu, n, a.T, t0, t1);
+    const int nch = (t1 - t0 + C - 1) / C;
+    TI* go = (TI*)a.o;
+
+    const int pc = min(lane, NP - 1), ch = 2 * pc;  // this lane's key-channel pair
+    const bool vact = lane < NP;                    // lane owns a pair in the variance phase
+
+    // ---- initial states ----------------------------------------------------------------
+    floatx4 Sacc[CF::SPW];
+#pragma unroll
+    for (int j = 0; j < CF::SPW; ++j) {
+        const int x = wave + NW * j;
+        Sacc[j] = zero4();
+        if (x < CF::NST) {
+            const int it = x % CF::NKT, nt = x / CF::NKT;
+            if (a.S0) {
+                const float* src = a.S0 + (size_t)nh * DK * DV;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    Sacc[j][rr] = src[(size_t)(16 * it + 4 * lg + rr) * DV + col0 + 16 * nt + li];
+            }
+            store4<MT>(SmT + (16 * nt + li) * LDK + 16 * it + 4 * lg, Sacc[j][0], Sacc[j][1],
+                       Sacc[j][2], Sacc[j][3]);
+        }
+    }
+    if (DIAG ? tid < DK : tid == 0)
+        carry[tid] = make_float2(a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f, 1.f);
+
+    if (nch == 0) {  // empty sequence: the states pass through
+        if (a.P_T && vt == 0 && (DIAG ? tid < DK : tid == 0))
+            a.P_T[(size_t)nh * (DIAG ? DK : 1) + tid] =
+                a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f;
+    }
+
+    WalkIn<TI, CF> in;
+    if (nch > 0) {
+        const int L0 = min(C, t1 - t0);
+        load_main<TI, CF>(in, a, t0, L0, h, ch, wave, tid);
+        load_v<TI, CF>(in, a, t0, L0, h, col0, wave, lane);
+        if (tid < C) {
+            const float rv = to_f32(in.rr);
+            s_r[tid] = tid < L0 ? rv : 1.f;
+            s_mr[tid] = tid < L0 ? a.mu / rv : 0.f;
+        }
+    }
+    __syncthreads();
+
+    floatx4 Oacc[CF::XPW];
+    for (int m = 0; m < nch; ++m) {
+        const int c0 = t0 + m * C, L = min(C, t1 - c0);
+        const bool last = m == nch - 1;
+        const int par = m & 1;
+        const int c0n = last ? c0 : c0 + C, Ln = last ? L : min(C, t1 - c0n);
+
+        // ==== 1-2. variance replay and operands ==========================================
+        if constexpr (DIAG) {
+            float av[2][SL], a2[2][SL], wv[2][SL], uu[2][SL], kv[2][SL], qv[2][SL];
+#pragma unroll
+            for (int j = 0; j < SL; ++j) {
+                const int t = SL * wave + j;
+                float2 A = unpack2(in.al[j]), K = unpack2(in.kk[j]), Wv = unpack2(in.ww[j]),
+                       Q = unpack2(in.qq[j]);
+                if (t >= L) {  // past the end: no decay, no noise, zero key and query
+                    A = make_float2(1.f, 1.f);
+                    K = Wv = Q = make_float2(0.f, 0.f);
+                }
+                const float mr = s_mr[t];
+                av[0][j] = A.x; av[1][j] = A.y;
+                a2[0][j] = A.x * A.x; a2[1][j] = A.y * A.y;
+                wv[0][j] = Wv.x; wv[1][j] = Wv.y;
+                kv[0][j] = K.x; kv[1][j] = K.y;
+                qv[0][j] = Q.x; qv[1][j] = Q.y;
+                uu[0][j] = K.x * K.x * mr; uu[1][j] = K.y * K.y * mr;
+            }
+            if (vact) {
+                // the segment's Moebius product (later tokens on the left) and decay product
+                float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
+                float g0 = 1.f, g1 = 1.f;
+#pragma unroll
+                for (int j = 0; j < SL; ++j) {
+                    mob_left(m0, a2[0][j], wv[0][j], uu[0][j]);
+                    mob_left(m1, a2[1][j], wv[1][j], uu[1][j]);
+                    g0 *= av[0][j];
+                    g1 *= av[1][j];
+                    if (j & 1) {
+                        renorm4(m0[0], m0[1], m0[2], m0[3]);
+                        renorm4(m1[0], m1[1], m1[2], m1[3]);
+                    }
+                }
+                segA[wave * DK + ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
+                segA[wave * DK + ch + 1] = make_float4(m1[0], m1[1], m1[2], m1[3]);
+                *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
+            }
+            __syncthreads();
+            if (vact) {
+                // carry into this segment: the chunk carry through the earlier segments
+                float2 z0 = carry[par * DK + ch], z1 = carry[par * DK + ch + 1];
+                float g0 = 1.f, g1 = 1.f;
+                for (int ps = 0; ps < wave; ++ps) {
+                    z0 = mat_vec(segA[ps * DK + ch], z0);
+                    z1 = mat_vec(segA[ps * DK + ch + 1], z1);
+                    const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
+                    g0 *= gg.x;
+                    g1 *= gg.y;
+                }
+                float n0 = z0.x, d0 = z0.y, n1 = z1.x, d1 = z1.y;
+                float pb0[SL], pb1[SL];
+#pragma unroll
+                for (int j = 0; j < SL; ++j) {
+                    const int t = SL * wave + j;
+                    g0 *= av[0][j];
+                    g1 *= av[1][j];
+                    const float nn0 = fmaf(a2[0][j], n0, wv[0][j] * d0);  // p_hat = nn / d
+                    const float nn1 = fmaf(a2[1][j], n1, wv[1][j] * d1);
+                    pb0[j] = nn0 * kv[0][j] * __builtin_amdgcn_rcpf(d0 * g0);  // p_hat k / gamma
+                    pb1[j] = nn1 * kv[1][j] * __builtin_amdgcn_rcpf(d1 * g1);
+                    d0 = fmaf(uu[0][j], nn0, d0);
+                    d1 = fmaf(uu[1][j], nn1, d1);
+                    n0 = nn0;
+                    n1 = nn1;
+                    if (j & 1) {
+                        renorm2(n0, d0);
+                        renorm2(n1, d1);
+                    }
+                    st2<MT>(Kb + t * LDK + ch, g0 * kv[0][j], g1 * kv[1][j]);
+                    st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv[0][j], a.scale * g1 * qv[1][j]);
+                    st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
+                }
+                storeN<MT, SL>(PbT + ch * LDC + SL * wave, pb0);
+                storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
+                if (wave == NW - 1) {
+                    renorm2(n0, d0);
+                    renorm2(n1, d1);
+                    carry[(par ^ 1) * DK + ch] = make_float2(n0, d0);
+                    carry[(par ^ 1) * DK + ch + 1] = make_float2(n1, d1);
+                    *reinterpret_cast<float2*>(gC + ch) = make_float2(g0, g1);
+                    if (last && a.P_T && vt == 0)  // the sequence's final variances n / d
+                        *reinterpret_cast<float2*>(a.P_T + (size_t)nh * DK + ch) =
+                            make_float2(n0 / d0, n1 / d1);
+                }
+            }
+        } else {
+            // isotropic: per-token ||k||^2 and mean_i alpha_i^2 by wave reductions; one scalar
+            // chain per head, which every lane of a wave runs alike
+            float kv[2][SL], qv[2][SL], ga[2][SL], aa[SL], wt[SL], ut[SL], nk[SL], rt[SL];
+#pragma unroll
+            for (int j = 0; j < SL; ++j) {
+                const int t = SL * wave + j;
+                const bool ok = t < L;
+                float2 K = unpack2(in.kk[j]), Q = unpack2(in.qq[j]);
+                float2 A = make_float2(1.f, 1.f);
+                if constexpr (APC) A = unpack2(in.al[j]);
+                if (!ok) {
+                    K = Q = make_float2(0.f, 0.f);
+                    A = make_float2(1.f, 1.f);
+                }
+                const float as = (ok && !APC) ? to_f32(in.als[APC ? 0 : j]) : 1.f;
+                kv[0][j] = K.x; kv[1][j] = K.y;
+                qv[0][j] = Q.x; qv[1][j] = Q.y;
+                ga[0][j] = APC ? A.x : as;
+                ga[1][j] = APC ? A.y : as;
+                float sk = vact ? fmaf(K.x, K.x, K.y * K.y) : 0.f;
+                nk[j] = wave_sum(sk);
+                if constexpr (APC) {
+                    const float sa = vact ? fmaf(A.x, A.x, A.y * A.y) : 0.f;
+                    aa[j] = wave_sum(sa) * (1.f / (float)DK);
+                } else {
+                    aa[j] = as * as;
+                }
+                wt[j] = ok ? to_f32(in.ws[DIAG ? 0 : j]) : 0.f;
+                rt[j] = s_r[t];
+                ut[j] = nk[j] * s_mr[t] * (1.f / (float)DK);
+            }
+            {
+                float mm[4] = {1.f, 0.f, 0.f, 1.f};
+                float g0 = 1.f, g1 = 1.f;
+#pragma unroll
+                for (int j = 0; j < SL; ++j) {
+                    mob_left(mm, aa[j], wt[j], ut[j]);
+                    g0 *= ga[0][j];
+                    g1 *= ga[1][j];
+                    if (j & 1) renorm4(mm[0], mm[1], mm[2], mm[3]);
+                }
+                if (lane == 0) segA[wave * DK] = make_float4(mm[0], mm[1], mm[2], mm[3]);
+                if (vact) *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
+            }
+            __syncthreads();
+            {
+                float2 z = carry[par * DK];
+                float g0 = 1.f, g1 = 1.f;
+                for (int ps = 0; ps < wave; ++ps) {
+                    z = mat_vec(segA[ps * DK], z);
+                    const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
+                    g0 *= gg.x;
+                    g1 *= gg.y;
+                }
+                float nz = z.x, dz = z.y;
+                float pb0[SL], pb1[SL];
+#pragma unroll
+                for (int j = 0; j < SL; ++j) {
+                    const int t = SL * wave + j;
+                    g0 *= ga[0][j];
+                    g1 *= ga[1][j];
+                    const float nn = fmaf(aa[j], nz, wt[j] * dz);    // b_hat = nn / dz
+                    const float beta = nn / fmaf(dz, rt[j], nn * nk[j]);
+                    pb0[j] = beta * kv[0][j] * __builtin_amdgcn_rcpf(g0);
+                    pb1[j] = beta * kv[1][j] * __builtin_amdgcn_rcpf(g1);
+                    dz = fmaf(ut[j], nn, dz);
+                    nz = nn;
+                    if (j & 1) renorm2(nz, dz);
+                    if (vact) {
+                        st2<MT>(Kb + t * LDK + ch, g0 * kv[0][j], g1 * kv[1][j]);
+                        st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv[0][j],
+                                a.scale * g1 * qv[1][j]);
+                        st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
+                    }
+                }
+                if (vact) {
+                    storeN<MT, SL>(PbT + ch * LDC + SL * wave, pb0);
+                    storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
+                }
+                if (wave == NW - 1) {
+                    renorm2(nz, dz);
+                    if (lane == 0) {
+                        carry[(par ^ 1) * DK] = make_float2(nz, dz);
+                        if (last && a.P_T && vt == 0) a.P_T[nh] = nz / dz;
+                    }
+                    if (vact) *reinterpret_cast<float2*>(gC + ch) = make_float2(g0, g1);
+                }
+            }
+        }
+        __syncthreads();
+        // the next chunk's inputs (this lane is done with the current ones except V)
+        load_main<TI, CF>(in, a, c0n, Ln, h, ch, wave, tid);
+
+        // ==== 3. L = diag(c) + tril(K_bar P_bar^T, -1) and A_qk = tril(Q_bar P_bar^T) =====
+        for (int u = wave; u < CF::NLU; u += NW) {
+            int ib = 0, jb = u;  // enumerate (ib >= jb) in row order
+            while (jb > ib) { jb -= ib + 1; ++ib; }
+            floatx4 tacc = zero4(), qacc = zero4();
+            mm_kc2<MT, DK>(Kb + 16 * ib * LDK, Qb + 16 * ib * LDK, LDK, Pb + 16 * jb * LDK, LDK,
+                           tacc, qacc, lane);
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int row = 4 * lg + rr, R = 16 * ib + row, Cc = 16 * jb + li;
+                if (ib > jb) {
+                    Lm[R * LDT + Cc] = tacc[rr];
+                    Aq[R * LDC + Cc] = from_f32<MT>(qacc[rr]);
+                } else {
+                    const float cdiag = DIAG ? s_r[R] + tacc[rr] : 1.f;
+                    Lm[R * LDT + Cc] = row > li ? tacc[rr] : (row == li ? cdiag : 0.f);
+                    Aq[R * LDC + Cc] = from_f32<MT>(row >= li ? qacc[rr] : 0.f);
+                }
+            }
+        }
+        // zero the blocks above the diagonal of A_qk and A (16-byte stores)
+        {
+            constexpr int VPB = 16 * (int)sizeof(MT) / 16;  // 16-byte vectors per block row
+            constexpr int NUP = NB * (NB - 1) / 2;
+            if constexpr (NUP > 0)
+                for (int idx = tid; idx < 2 * NUP * 16 * VPB; idx += NTH) {
+                    const int which = idx / (NUP * 16 * VPB), rem = idx % (NUP * 16 * VPB);
+                    int blk = rem / (16 * VPB);
+                    const int row16 = (rem / VPB) % 16, vec = rem % VPB;
+                    int ib = 0;  // blk -> (ib < jb)
+                    while (blk >= NB - 1 - ib) { blk -= NB - 1 - ib; ++ib; }
+                    const int jb = ib + 1 + blk;
+                    MT* base = which ? Ai : Aq;
+                    *reinterpret_cast<uint4*>(base + (16 * ib + row16) * LDC + 16 * jb +
+                                              vec * (16 / (int)sizeof(MT))) =
+                        make_uint4(0, 0, 0, 0);
+                }
+        }
+        __syncthreads();
+
+        // ==== 3'. A = L^-1: diagonal blocks by forward substitution (lane = block, column) ==
+        if (wave == 0 && (lane >> 4) < NB) {
+            const int b = lane >> 4, j = li;
+            const float* Lb = Lm + (16 * b) * LDT + 16 * b;
+            float x[16];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                float trow[16];
+#pragma unroll
+                for (int v4 = 0; v4 < (i + 4) / 4; ++v4) {
+                    const float4 q4 = *reinterpret_cast<const float4*>(Lb + i * LDT + 4 * v4);
+                    trow[4 * v4] = q4.x; trow[4 * v4 + 1] = q4.y;
+                    trow[4 * v4 + 2] = q4.z; trow[4 * v4 + 3] = q4.w;
+                }
+                float sum = 0.f;
+#pragma unroll
+                for (int kq = 0; kq < i; ++kq) sum = fmaf(trow[kq], x[kq], sum);
+                x[i] = i < j ? 0.f : ((i == j ? 1.f : 0.f) - sum) / trow[i];
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) Ai[(16 * b + i) * LDC + 16 * b + j] = from_f32<MT>(x[i]);
+            store8<MT>(AiT + (16 * b + j) * LDC + 16 * b, x);
+            store8<MT>(AiT + (16 * b + j) * LDC + 16 * b + 8, x + 8);
+        }
+        __syncthreads();
+        // off-diagonal blocks, one block diagonal d = ib - jb at a time:
+        //   A_ij = -A_ii sum_{j<=k<i} L_ik A_kj
+#pragma unroll
+        for (int d = 1; d < NB; ++d) {
+            if (wave < NB - d) {
+                const int jb = wave, ib = jb + d;
+                floatx4 acc = zero4();
+                for (int kb = jb; kb < ib; ++kb)
+                    acc = mm16_tv<MT>(Lm + (16 * ib) * LDT + 16 * kb, LDT,
+                                      AiT + (16 * jb) * LDC + 16 * kb, LDC, acc, lane);
+                MT* tmpT = Inv + wave * 16 * CF::LDI;  // transposed: the next B operand
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    tmpT[li * CF::LDI + 4 * lg + rr] = from_f32<MT>(acc[rr]);
+                wave_lds_sync();
+                const floatx4 res = mm_kc<MT, 16>(Ai + (16 * ib) * LDC + 16 * ib, LDC, tmpT,
+                                                  CF::LDI, zero4(), lane);
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
+                    Ai[row * LDC + col] = from_f32<MT>(-res[rr]);
+                    AiT[col * LDC + row] = from_f32<MT>(-res[rr]);
+                }
+            }
+            __syncthreads();
+        }
+
+        // ==== 4. state: X = V - K_bar S and Q_bar S ======================================
+#pragma unroll
+        for (int j = 0; j < CF::XPW; ++j) {
+            const int x = wave + NW * j;
+            Oacc[j] = zero4();
+            if (x < CF::NXT) {
+                const int mt = x % NB, nt = x / NB;
+                floatx4 xacc = zero4();
+#pragma unroll
+                for (int s = 0; s < FK::NS; ++s) {
+                    const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                    const typename FK::V b = FK::ld(SmT + (16 * nt + li) * LDK + k0);
+                    xacc = FK::mma(xacc, FK::ld(Kb + (16 * mt + li) * LDK + k0), b);
+                    Oacc[j] = FK::mma(Oacc[j], FK::ld(Qb + (16 * mt + li) * LDK + k0), b);
+                }
+                float xv[4];
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int t = 16 * mt + 4 * lg + rr;
+                    xv[rr] = (t < L ? to_f32(in.vv[j][rr]) : 0.f) - xacc[rr];
+                }
+                store4<MT>(XT + (16 * nt + li) * LDC + 16 * mt + 4 * lg, xv[0], xv[1], xv[2],
+                           xv[3]);
+            }
+        }
+        __syncthreads();
+        load_v<TI, CF>(in, a, c0n, Ln, h, col0, wave, lane);
+
+        // R = A X (A is lower triangular: row block mt needs k < 16 (mt + 1))
+#pragma unroll
+        for (int j = 0; j < CF::XPW; ++j) {
+            const int x = wave + NW * j;
+            if (x < CF::NXT) {
+                const int mt = x % NB, nt = x / NB;
+                floatx4 racc = zero4();
+#pragma unroll
+                for (int s = 0; s < FC::NS; ++s) {
+                    if (FC::KF * s < 16 * (mt + 1)) {
+                        const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+                        racc = FC::mma(racc, FC::ld(Ai + (16 * mt + li) * LDC + k0),
+                                       FC::ld(XT + (16 * nt + li) * LDC + k0));
+                    }
+                }
+                store4<MT>(RT + (16 * nt + li) * LDC + 16 * mt + 4 * lg, racc[0], racc[1],
+                           racc[2], racc[3]);
+            }
+        }
+        __syncthreads();
+
+        // O = Q_bar S + A_qk R (staged for 16-byte stores); S <- gamma_C (.) (S + P_bar^T R)
+#pragma unroll
+        for (int j = 0; j < CF::XPW; ++j) {
+            const int x = wave + NW * j;
+            if (x < CF::NXT) {
+                const int mt = x % NB, nt = x / NB;
+#pragma unroll
+                for (int s = 0; s < FC::NS; ++s) {
+                    if (FC::KF * s < 16 * (mt + 1)) {
+                        const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+                        Oacc[j] = FC::mma(Oacc[j], FC::ld(Aq + (16 * mt + li) * LDC + k0),
+                                          FC::ld(RT + (16 * nt + li) * LDC + k0));
+                    }
+                }
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    Ost[(16 * mt + 4 * lg + rr) * LDO + 16 * nt + li] = from_f32<TI>(Oacc[j][rr]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < CF::SPW; ++j) {
+            const int x = wave + NW * j;
+            if (x < CF::NST) {
+                const int it = x % CF::NKT, nt = x / CF::NKT;
+#pragma unroll
+                for (int s = 0; s < FC::NS; ++s) {
+                    const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+                    Sacc[j] = FC::mma(Sacc[j], FC::ld(PbT + (16 * it + li) * LDC + k0),
+                                      FC::ld(RT + (16 * nt + li) * LDC + k0));
+                }
+                const float4 gc = *reinterpret_cast<const float4*>(gC + 16 * it + 4 * lg);
+                Sacc[j][0] *= gc.x;
+                Sacc[j][1] *= gc.y;
+                Sacc[j][2] *= gc.z;
+                Sacc[j][3] *= gc.w;
+                store4<MT>(SmT + (16 * nt + li) * LDK + 16 * it + 4 * lg, Sacc[j][0], Sacc[j][1],
+                           Sacc[j][2], Sacc[j][3]);
+            }
+        }
+        // r of the next chunk (every reader of this chunk's r is past the barrier above)
+        if (tid < C) {
+            const float rv = to_f32(in.rr);
+            s_r[tid] = tid < Ln ? rv : 1.f;
+            s_mr[tid] = tid < Ln ? a.mu / rv : 0.f;
+        }
+        __syncthreads();
+
+        // this chunk's O rows, 16-byte stores (rows past the end are not written)
+        {
+            constexpr int VE = 16 / (int)sizeof(TI), VPR = BV / VE;
+            for (int idx = tid; idx < C * VPR; idx += NTH) {
+                const int t = idx / VPR, e = (idx % VPR) * VE;
+                if (t < L)
+                    *reinterpret_cast<uint4*>(go + ((size_t)(c0 + t) * H + h) * DV + col0 + e) =
+                        *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
+            }
+        }
+    }
+
+    if (a.S_T) {
+        float* dst = a.S_T + (size_t)nh * DK * DV;
+#pragma unroll
+        for (int j = 0; j < CF::SPW; ++j) {
+            const int x = wave + NW * j;
+            if (x < CF::NST) {
+                const int it = x % CF::NKT, nt = x / CF::NKT;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    dst[(size_t)(16 * it + 4 * lg + rr) * DV + col0 + 16 * nt + li] = Sacc[j][rr];
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// Packed batches: the sequences in the order they are walked, longest first (a rank sort in
+// one workgroup; larger batches keep their own order).
+// ------------------------------------------------------------------------------------------
+constexpr int ORDER_MAX = 4096;
+
+__global__ __launch_bounds__(1024) void order_kernel(const int32_t* __restrict__ cu, int N,
+                                                     int32_t* __restrict__ order)
+{
+    __shared__ int32_t len[ORDER_MAX];
+    for (int i = threadIdx.x; i < N; i += blockDim.x) len[i] = max(0, cu[i + 1] - cu[i]);
+    __syncthreads();
+    for (int i = threadIdx.x; i < N; i += blockDim.x) {
+        const int li = len[i];
+        int rank = 0;
+        for (int j = 0; j < N; ++j) {
+            const int lj = len[j];
+            rank += (lj > li) || (lj == li && j < i);
+        }
+        order[rank] = i;
+    }
+}
+
+__global__ void copy_floats_kernel(const float* __restrict__ src, float* __restrict__ dst,
+                                   size_t n)
+{
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+// ------------------------------------------------------------------------------------------
+// host side
+// ------------------------------------------------------------------------------------------
+template <class TI, int DK, int DV, int C>
+constexpr bool walk_fits()
+{
+    constexpr int BV = DV >= 32 ? 32 : DV;
+    return WalkCfg<TI, DK, DV, BV, C, 0, true>::TOTAL <= 160 * 1024 &&
+           WalkCfg<TI, DK, DV, BV, C, 1, false>::TOTAL <= 160 * 1024;
+}
+
+// Workspace: the walk order of a packed batch (int32 [N]) and, when the caller updates P in
+// place (P_T == P0), a copy of P0 that every value tile of a head reads at its start while the
+// first tile to finish may already have written P_T.
+struct WsMap {
+    size_t order, p0, total;
+};
+
+inline WsMap ws_map(int variant, bool packed, int N, int H, int dk)
+{
+    WsMap m;
+    m.order = 0;
+    m.p0 = packed ? al256((size_t)N * 4) : 0;
+    m.total = m.p0 + al256((size_t)N * H * (variant == 0 ? dk : 1) * 4);
+    return m;
+}
+
+template <class TI, int DK, int DV, int C, int VARIANT, bool APC>
+hipError_t run_t(const FwdCall& fc, hipStream_t st)
+{
+    constexpr int BV = DV >= 32 ? 32 : DV;
+    using CF = WalkCfg<TI, DK, DV, BV, C, VARIANT, APC>;
+    static std::atomic<bool> attr_done{false};
+    hipError_t e;
+    if (!attr_done.load()) {
+        if ((e = hipFuncSetAttribute((const void*)walk_kernel<TI, CF>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)CF::TOTAL)) != hipSuccess)
+            return e;
+        attr_done.store(true);
+    }
+    const SeqArgs& sa = fc.sa;
+    const bool packed = sa.cu_seqlens != nullptr;
+    const WsMap wm = ws_map(VARIANT, packed, sa.N, sa.H, DK);
+    char* ws = (char*)fc.workspace;
+    WalkArgs a;
+    a.q = fc.q; a.k = fc.k; a.v = fc.v; a.alpha = fc.alpha; a.omega = fc.omega; a.r = fc.r;
+    a.S0 = fc.S0; a.P0 = fc.P0; a.o = fc.o; a.S_T = fc.S_T; a.P_T = fc.P_T;
+    a.cu = sa.cu_seqlens; a.order = nullptr;
+    a.N = sa.N; a.T = sa.T; a.H = sa.H; a.mu = fc.mu; a.scale = fc.scale;
+    if (packed && sa.N <= ORDER_MAX) {
+        int32_t* order = (int32_t*)(ws + wm.order);
+        hipLaunchKernelGGL(order_kernel, dim3(1), dim3(1024), 0, st, sa.cu_seqlens, sa.N, order);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        a.order = order;
+    }
+    if (fc.P0 && fc.P_T == fc.P0) {
+        float* p0 = (float*)(ws + wm.p0);
+        const size_t np = (size_t)sa.N * sa.H * (VARIANT == 0 ? DK : 1);
+        hipLaunchKernelGGL(copy_floats_kernel, dim3((unsigned)std::min<size_t>((np + 255) / 256, 1024)),
+                           dim3(256), 0, st, fc.P0, p0, np);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        a.P0 = p0;
+    }
+    const size_t nh8 = ((size_t)sa.N * sa.H + 7) / 8 * 8;
+    const size_t nblk = nh8 * CF::NV;
+    if (nblk == 0) return hipSuccess;
+    hipLaunchKernelGGL((walk_kernel<TI, CF>), dim3((unsigned)nblk), dim3(NTH), CF::TOTAL, st, a);
+    return hipGetLastError();
+}
+
+template <class TI, int DK, int DV, int C>
+hipError_t run_variant(const FwdCall& fc, hipStream_t st)
+{
+    if constexpr (!walk_fits<TI, DK, DV, C>()) {
+        return hipErrorInvalidConfiguration;
+    } else {
+        if (fc.variant == 0) return run_t<TI, DK, DV, C, 0, true>(fc, st);
+        if (fc.apc) return run_t<TI, DK, DV, C, 1, true>(fc, st);
+        return run_t<TI, DK, DV, C, 1, false>(fc, st);
+    }
+}
+
+// Compile-time dispatch over (dtype, dk, dv, chunk) calling F::template go<TI, DK, DV, C>().
+template <class F>
+auto dispatch(kdn_dtype_t dtype, int dk, int dv, int chunk, F f)
+    -> decltype(f.template go<float, 16, 16, 16>())
+{
+#define KDN_C(TI, DK, DV)                                                   \
+    switch (chunk) {                                                        \
+    case 16: return f.template go<TI, DK, DV, 16>();                        \
+    case 32: return f.template go<TI, DK, DV, 32>();                        \
+    default: return f.template go<TI, DK, DV, 64>();                        \
+    }
+#define KDN_V(TI, DK)                                                       \
+    switch (dv) {                                                           \
+    case 16: KDN_C(TI, DK, 16)                                              \
+    case 32: KDN_C(TI, DK, 32)                                              \
+    case 64: KDN_C(TI, DK, 64)                                              \
+    default: KDN_C(TI, DK, 128)                                             \
+    }
+#define KDN_K(TI)                                                           \
+    switch (dk) {                                                           \
+    case 16: KDN_V(TI, 16)                                                  \
+    case 32: KDN_V(TI, 32)                                                  \
+    case 64: KDN_V(TI, 64)                                                  \
+    default: KDN_V(TI, 128)                                                 \
+    }
+    if (dtype == KDN_F32) {
+        KDN_K(float)
+    } else {
+        KDN_K(bf16)
+    }
+#undef KDN_K
+#undef KDN_V
+#undef KDN_C
+    return f.template go<float, 16, 16, 16>();  // not reached
+}
+
+struct FitsF {
+    template <class TI, int DK, int DV, int C> bool go() const { return walk_fits<TI, DK, DV, C>(); }
+};
+struct RunF {
+    const FwdCall* fc;
+    hipStream_t st;
+    template <class TI, int DK, int DV, int C> hipError_t go() const
+    {
+        return run_variant<TI, DK, DV, C>(*fc, st);
+    }
+};
+
+}  // namespace
+
+bool chunked_supported(kdn_dtype_t dtype, int dk, int dv, int chunk)
+{
+    if (chunk != 16 && chunk != 32 && chunk != 64) return false;
+    return dispatch(dtype, dk, dv, chunk, FitsF{});
+}
+
+int chunked_default_chunk(kdn_dtype_t dtype, int dk, int dv)
+{
+    for (int c = 64; c >= 16; c >>= 1)
+        if (chunked_supported(dtype, dk, dv, c)) return c;
+    return 16;
+}
+
+size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
+                               int dv, kdn_dtype_t dtype, int chunk)
+{
+    (void)B; (void)T; (void)dv; (void)dtype; (void)chunk;
+    return ws_map(variant, packed, N, H, dk).total;
+}
+
+hipError_t launch_chunked(const FwdCall& fc, hipStream_t stream)
+{
+    FwdCall c = fc;
+    if (c.chunk == 0) c.chunk = chunked_default_chunk(c.dtype, c.dk, c.dv);
+    return dispatch(c.dtype, c.dk, c.dv, c.chunk, RunF{&c, stream});
+}
+
+}  // namespace kdn

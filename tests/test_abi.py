@@ -107,19 +107,17 @@ def test_forward_workspace(L):
 
 
 def test_workspace_queries(L):
+    # fixed length: a staging copy of P0 (one float per (sequence, head, channel)), rounded up
+    # to 256 bytes; a packed batch adds the walk order (one int32 per sequence)
     full = L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 1, 0, 0)
-    # the WY factors of every (chunk, head) dominate: W, Q_bar, K_tail (C x dk each), A_qk
-    # (C x C) and U (C x dv) in bf16 per chunk of 64 tokens, i.e. at least (3*128+64+128)*2 B
-    # per token-head
-    assert full >= 4 * 4096 * 16 * (3 * 128 + 64 + 128) * 2
-    assert full < 2 * 4 * 4096 * 16 * (3 * 128 + 64 + 128) * 2
-    # fp32 factors take twice the bytes; a packed batch adds at most one partial chunk per
-    # sequence; rejected arguments give 0
-    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 0, 0, 32) > full
-    assert L.kdn_forward_workspace_bytes(0, 4, 1, 16384, 16, 128, 128, 1, 1, 0) >= full
+    assert full == 4 * 16 * 128 * 4
+    assert L.kdn_forward_workspace_bytes(1, 4, 4, 4096, 16, 128, 128, 1, 0, 0) == 256
+    assert L.kdn_forward_workspace_bytes(0, 32, 1, 135000, 16, 128, 128, 1, 1, 0) \
+        == 256 + 32 * 16 * 128 * 4
+    # rejected arguments give 0
     assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 0, 0, 64) == 0
     assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 48, 128, 1, 0, 0) == 0
-    assert L.kdn_forward_workspace_bytes(1, 4, 4, 4096, 16, 128, 128, 1, 0, 0) < full
+    assert L.kdn_forward_workspace_bytes(0, 0, 4, 4096, 16, 128, 128, 1, 0, 0) == 0
     small = L.kdn_gain_workspace_bytes(0, 1, 1, 64, 1, 128)
     big = L.kdn_gain_workspace_bytes(0, 4, 4, 4096, 16, 128)
     assert big > small > 0

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 import bruteforce as bf
-from chunk_model import chunk_forward
+from chunk_model import chunk_forward, chunk_forward_lsolve
 
 pytestmark = pytest.mark.filterwarnings("ignore::RuntimeWarning")
 
@@ -414,6 +414,29 @@ def test_chunk_wy_form_equals_oracle(C):
                     scale=0.25)
     o, S = chunk_forward(x["q"], x["k"], x["v"], x["a"], iso["beta"][:, None] * x["k"], S0, C,
                          0.25)
+    np.testing.assert_allclose(o, iso["o"], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(S, iso["S"], rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("C", [4, 16, 64])
+def test_chunk_lsolve_form_equals_oracle(C):
+    """The form of the fused kernel: the gain normalisation moved into a lower-triangular
+    solve with diagonal r + sum_i p_hat_i k_i^2 (Sec. "Chunkwise Memory Scan" with
+    kappa = p_hat (.) k / den, eq. kla-box-gain)."""
+    g = rng(33)
+    T, dk, dv = 150, 16, 6
+    x = random_step_inputs(g, dk, dv, T)
+    x["k"] /= np.linalg.norm(x["k"], axis=1, keepdims=True)
+    x["a"] = 1 / (1 + np.exp(-(g.standard_normal((T, dk)) + 2)))
+    S0 = g.standard_normal((dk, dv)) * 0.1
+    out = diag_chain(x["q"], x["k"], x["v"], x["a"], x["w"], x["r"], S0, mu=16.0, scale=0.25)
+    o, S = chunk_forward_lsolve(x["q"], x["k"], x["v"], x["a"], (out["phat"], x["r"]), True, S0,
+                                C, 0.25)
+    np.testing.assert_allclose(o, out["o"], rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(S, out["S"], rtol=1e-10, atol=1e-12)
+    iso = iso_chain(x["q"], x["k"], x["v"], x["a"], x["w"][:, 0], x["r"], S0, mu=16.0,
+                    scale=0.25)
+    o, S = chunk_forward_lsolve(x["q"], x["k"], x["v"], x["a"], iso["beta"], False, S0, C, 0.25)
     np.testing.assert_allclose(o, iso["o"], rtol=1e-10, atol=1e-12)
     np.testing.assert_allclose(S, iso["S"], rtol=1e-10, atol=1e-12)
 
