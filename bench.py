@@ -8,10 +8,9 @@ batch 4 as in its throughput probe). Inputs are seeded synthetic tensors residen
 timing starts. One step = one full forward over the batch (every stage of the path: variance
 scan, gains, chunkwise WY solve, state passing, outputs, final states).
 
-Prints one JSON line with tokens/s, the roofline position of one forward call (its kernels run
-on two streams: algorithmic bytes per call / the HIP-event duration of the call on the caller's
-stream, against the 8 TB/s HBM peak) and the CPU oracle timed on a bounded sample of the same
-workload.
+Prints one JSON line with tokens/s, the roofline position of one forward call (algorithmic bytes
+per call / the HIP-event duration of the call on the caller's stream, against the 8 TB/s HBM
+peak) and the CPU oracle timed on a bounded sample of the same workload.
 """
 
 from __future__ import annotations
@@ -147,9 +146,8 @@ def main():
     torch.cuda.synchronize()
 
     # timed region: K steps between two synchronisations; HIP events around every forward
-    # call on torch's current stream, which the binding passes to the library (the call ends
-    # with that stream waiting for the library's second stream, so the end event follows the
-    # last kernel of the call)
+    # call on torch's current stream, which the binding passes to the library (every kernel of
+    # the call runs on that stream)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -190,8 +188,8 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(),
-                     "kernel": "forward = chunk summaries + carry scan + WY prep + state "
-                               "passing (bf16, dk=dv=128, chunk 64, state dv tile 32)",
+                     "kernel": "walk_kernel: one workgroup per (sequence, head, 32 value "
+                               "columns) walks the chunks (bf16, dk=dv=128, chunk 64)",
                      "algorithmic_bytes_per_launch": abytes,
                      "kernel_ms_mean": round(kmean, 4), "kernel_ms_median": round(kmed, 4),
                      "mfma_frac": round(aflops / (kmean * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,

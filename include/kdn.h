@@ -21,7 +21,8 @@
  *   P [N,H,dk] for the diagonal variant, [N,H] for the isotropic one.
  * - S0 == NULL means S0 = 0; P0 == NULL means P0 = 1 (p_0 = 1, b_0 = 1). S_T / P_T may be NULL
  *   (not written) and may alias S0 / P0 exactly (in-place state update).
- * - Supported head sizes: dk, dv in {16, 32, 64, 128}.
+ * - Supported head sizes: dk, dv in {16, 32, 64, 128}. The forward takes input tensors smaller
+ *   than 2 GiB each (KDN_ERR_UNSUPPORTED otherwise).
  * - Device-side contract (not checked on the host, which never reads device data):
  *   cu_seqlens non-decreasing with cu_seqlens[0] == 0 and cu_seqlens[N] == T; 0 < alpha <= 1;
  *   omega >= 0; r > 0. Kernels never write outside the caller's buffers even when it is broken.
@@ -41,7 +42,8 @@ extern "C" {
 typedef enum {
     KDN_OK = 0,
     KDN_ERR_INVALID_ARG = 1, /* null required pointer, bad size, mu <= 0, scale <= 0, aliasing */
-    KDN_ERR_UNSUPPORTED = 2, /* dk or dv outside {16, 32, 64, 128}, or an unsupported chunk   */
+    KDN_ERR_UNSUPPORTED = 2, /* dk or dv outside {16, 32, 64, 128}, an unsupported chunk, or a
+                                forward input tensor of 2 GiB or more                         */
     KDN_ERR_WORKSPACE = 3,   /* workspace smaller than the matching *_workspace_bytes query    */
     KDN_ERR_HIP = 4          /* a HIP launch failed; kdn_last_error() carries the HIP message  */
 } kdn_status_t;

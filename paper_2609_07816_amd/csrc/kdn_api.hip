@@ -84,6 +84,9 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
                     "dtype, dk=%d and dv=%d (use 0 for the largest that fits)", chunk, dk, dv);
     const size_t ntok = (size_t)B * T * H, es = esize(dtype);
     const size_t nk = ntok * dk * es, nv = ntok * dv * es;
+    if (nk >= ((size_t)1 << 31) || nv >= ((size_t)1 << 31))
+        return fail(KDN_ERR_UNSUPPORTED, "each input tensor must be smaller than 2 GiB (the "
+                    "forward addresses it with 32-bit offsets)");
     const size_t na = (variant == 0 || apc) ? nk : ntok * es;
     const size_t nw = variant == 0 ? nk : ntok * es;
     const void* ins[6] = {q, k, v, alpha, omega, r};

@@ -95,6 +95,42 @@ template <int K> struct Frag<float, K> {
     }
 };
 
+// 16 x 16 x 16 products from register fragments: lane (g, i) holds A[i][4g..4g+3] (A side) or
+// B[4g..4g+3][i] (B side). A result tile (lane (g, i): rows 4g..4g+3 of column i) is therefore
+// already a B fragment of the next product.
+template <class MT> struct F16;
+template <> struct F16<bf16> {
+    using V = uint2;
+    __device__ static V pack(float x0, float x1, float x2, float x3)
+    {
+        bf16x4 v;
+        v[0] = (bf16)x0; v[1] = (bf16)x1; v[2] = (bf16)x2; v[3] = (bf16)x3;
+        return __builtin_bit_cast(V, v);
+    }
+    __device__ static V ld(const bf16* p) { return *reinterpret_cast<const V*>(p); }
+    __device__ static floatx4 mma(floatx4 acc, V a, V b)
+    {
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, a),
+                                                          __builtin_bit_cast(bf16x4, b), acc, 0,
+                                                          0, 0);
+    }
+};
+template <> struct F16<float> {
+    using V = float4;
+    __device__ static V pack(float x0, float x1, float x2, float x3)
+    {
+        return make_float4(x0, x1, x2, x3);
+    }
+    __device__ static V ld(const float* p) { return *reinterpret_cast<const V*>(p); }
+    __device__ static floatx4 mma(floatx4 acc, V a, V b)
+    {
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, acc, 0, 0, 0);
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, acc, 0, 0, 0);
+    }
+};
+
 // Four values (rows 4g..4g+3 of a result column, or four consecutive elements) in MT.
 template <class MT>
 __device__ __forceinline__ void store4(MT* dst, float x0, float x1, float x2, float x3)
@@ -105,6 +141,19 @@ __device__ __forceinline__ void store4(MT* dst, float x0, float x1, float x2, fl
         bf16x4 v;
         v[0] = (bf16)x0; v[1] = (bf16)x1; v[2] = (bf16)x2; v[3] = (bf16)x3;
         *reinterpret_cast<bf16x4*>(dst) = v;
+    }
+}
+
+// Four consecutive values in MT as floats (8- or 16-byte aligned source).
+template <class MT>
+__device__ __forceinline__ float4 ld4f(const MT* src)
+{
+    if constexpr (std::is_same<MT, float>::value) {
+        return *reinterpret_cast<const float4*>(src);
+    } else {
+        const uint2 u = *reinterpret_cast<const uint2*>(src);
+        return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                           __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
     }
 }
 
@@ -124,11 +173,31 @@ __device__ __forceinline__ float2 unpack2(unsigned u)
 }
 __device__ __forceinline__ float2 unpack2(float2 v) { return v; }
 
+// Power-of-two rescale of non-negative homogeneous values (the variance pairs and the Moebius
+// products of non-negative token matrices): exact, keeps every ratio, and brings the largest
+// entry into [0.5, 1). The exponent instruction gives 0 for 0, Inf and NaN, which leaves such
+// values unchanged.
+__device__ __forceinline__ void rescale2(float& n, float& d)
+{
+    const int e = -__builtin_amdgcn_frexp_expf(fmaxf(n, d));
+    n = ldexpf(n, e);
+    d = ldexpf(d, e);
+}
+
+__device__ __forceinline__ void rescale4(float* m)
+{
+    const int e = -__builtin_amdgcn_frexp_expf(fmaxf(fmaxf(m[0], m[1]), fmaxf(m[2], m[3])));
+    m[0] = ldexpf(m[0], e);
+    m[1] = ldexpf(m[1], e);
+    m[2] = ldexpf(m[2], e);
+    m[3] = ldexpf(m[3], e);
+}
+
 // z <- M z for a 2x2 matrix M = [x y; z w] (float4) acting on a homogeneous pair.
 __device__ __forceinline__ float2 mat_vec(const float4& m, float2 v)
 {
     float n = fmaf(m.x, v.x, m.y * v.y), d = fmaf(m.z, v.x, m.w * v.y);
-    renorm2(n, d);
+    rescale2(n, d);
     return make_float2(n, d);
 }
 
@@ -147,10 +216,11 @@ struct WalkCfg {
     static constexpr int NP = DK / 2;           // key-channel pairs (one per lane)
     static constexpr int NB = C / 16, NNT = BV / 16, NKT = DK / 16;
     static constexpr int NXT = NB * NNT, XPW = (NXT + NW - 1) / NW;  // X / O tiles
+    static_assert(XPW == 1, "one X / O tile per wave at most");
     static constexpr int NST = NKT * NNT, SPW = (NST + NW - 1) / NW;  // S tiles
     static constexpr int NLU = NB * (NB + 1) / 2;                      // lower block pairs
     static constexpr int PAD = 16 / (int)sizeof(MT);  // one 16-byte pad per row
-    static constexpr int LDK = DK + PAD, LDC = C + PAD, LDT = C + 4, LDI = 16 + PAD;
+    static constexpr int LDK = DK + PAD, LDC = C + PAD, LDT = C + 4;
     static constexpr int LDO = BV + 16 / (int)sizeof(TI);
     static constexpr size_t SZ_OP = al16((size_t)C * LDK * sizeof(MT));
     static constexpr size_t SZ_CC = al16((size_t)C * LDC * sizeof(MT));
@@ -159,20 +229,21 @@ struct WalkCfg {
     static constexpr size_t OFF_QB = OFF_KB + SZ_OP;
     static constexpr size_t OFF_PB = OFF_QB + SZ_OP;
     static constexpr size_t OFF_PBT = OFF_PB + SZ_OP;
-    // one region holding either the chunk's triangular matrices (L float32 [C][LDT]; A, A^T,
-    // A_qk [C][LDC]) or, while the variance runs, the segment summaries
+    // one region holding either the chunk's triangular matrices (L float32 [C][LDT]; the
+    // diagonal blocks of L^-1 and A_qk [C][LDC]) or, while the variance runs, the segment
+    // summaries
     static constexpr size_t OFF_U = OFF_PBT + al16((size_t)DK * LDC * sizeof(MT));
     static constexpr size_t OFF_LM = OFF_U;
     static constexpr size_t OFF_AI = OFF_LM + al16((size_t)C * LDT * 4);
-    static constexpr size_t OFF_AIT = OFF_AI + SZ_CC;
-    static constexpr size_t OFF_AQ = OFF_AIT + SZ_CC;
+    static constexpr size_t OFF_AQ = OFF_AI + SZ_CC;
     static constexpr size_t SZ_MAT = OFF_AQ + SZ_CC - OFF_U;
     static constexpr size_t OFF_SGA = OFF_U;                           // float4 [NW][DK]
     static constexpr size_t OFF_SGG = OFF_SGA + (size_t)NW * DK * 16;  // float [NW][DK]
-    static constexpr size_t SZ_SEG = (size_t)NW * DK * 20;
-    static constexpr size_t OFF_INV = OFF_U + al16(cmax(SZ_MAT, SZ_SEG));
+    static constexpr size_t OFF_ZS = OFF_SGG + (size_t)NW * DK * 4;    // float2 [NW][DK]
+    static constexpr size_t OFF_GS = OFF_ZS + (size_t)NW * DK * 8;     // float [NW][DK]
+    static constexpr size_t SZ_SEG = (size_t)NW * DK * 32;
     // S^T [BV][LDK], X^T and R^T [BV][LDC] in MT, O staging [C][LDO] in TI
-    static constexpr size_t OFF_SMT = OFF_INV + al16((size_t)NB * 16 * LDI * sizeof(MT));
+    static constexpr size_t OFF_SMT = OFF_U + al16(cmax(SZ_MAT, SZ_SEG));
     static constexpr size_t OFF_XT = OFF_SMT + al16((size_t)BV * LDK * sizeof(MT));
     static constexpr size_t OFF_RT = OFF_XT + al16((size_t)BV * LDC * sizeof(MT));
     static constexpr size_t OFF_O = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));
@@ -193,6 +264,47 @@ struct WalkArgs {
     const int32_t* order;  // packed batches: sequences, longest first (nullptr: in order)
     int N, T, H;
     float mu, scale;
+    uint32_t bytes_k, bytes_v, bytes_h;  // bytes of q / k / per-channel gates, of v, of r
+};
+
+// ------------------------------------------------------------------------------------------
+// Buffer loads: 32-bit byte offsets against a descriptor of the whole tensor; the unit checks
+// the range and returns 0 past the end, so rows past the end of a sequence need no clamping
+// (they belong to the next sequence or read 0, and are masked where they are used).
+// ------------------------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+template <class T> __device__ __forceinline__ T bload(rsrc_t r, uint32_t off);
+template <> __device__ __forceinline__ unsigned bload<unsigned>(rsrc_t r, uint32_t off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+}
+template <> __device__ __forceinline__ float bload<float>(rsrc_t r, uint32_t off)
+{
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+template <> __device__ __forceinline__ float2 bload<float2>(rsrc_t r, uint32_t off)
+{
+    const auto u = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+    return make_float2(__uint_as_float(u[0]), __uint_as_float(u[1]));
+}
+template <> __device__ __forceinline__ bf16 bload<bf16>(rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(bf16, __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0));
+}
+
+// Descriptors and byte strides of one workgroup's inputs.
+struct WalkSrc {
+    rsrc_t q, k, v, al, om, r;
+    uint32_t rowk, rowv, rowh;     // bytes per token row: channel tensors, v, per-head scalars
+    uint32_t lane_k, lane_h;       // this lane's byte offset within a row (channel pair; head)
+    uint32_t lane_v;               // this lane's byte offset within a row of v (its X tile)
 };
 
 // Raw inputs of one chunk held by one lane, loaded a chunk ahead and kept in storage precision
@@ -210,44 +322,82 @@ struct WalkIn {
     TI vv[CF::XPW][4];              // V at this lane's rows and column of its X tiles
 };
 
-template <class TI, class CF>
-__device__ __forceinline__ void load_main(WalkIn<TI, CF>& in, const WalkArgs& a, int c0, int L,
-                                          int h, int ch, int wave, int tid)
+// The next chunk's raw inputs in two groups issued at different points of the current chunk
+// (a wave that issues all of them at once stalls until the memory pipeline drains): group 0
+// holds k, the gates and r, group 1 the process noise and q.
+template <int G, class TI, class CF>
+__device__ __forceinline__ void load_main(WalkIn<TI, CF>& in, const WalkSrc& sr, uint32_t c0,
+                                          int wave, int tid)
 {
     using P2 = typename CF::P2;
-    constexpr int DK = CF::DK, SL = CF::SL;
-    const int H = a.H;
-    const TI *gq = (const TI*)a.q, *gk = (const TI*)a.k, *ga = (const TI*)a.alpha,
-             *gw = (const TI*)a.omega, *gr = (const TI*)a.r;
-    // rows past the end of the sequence re-read its last row; their values are masked
-    in.rr = gr[(size_t)(c0 + min(min(tid, CF::C - 1), L - 1)) * H + h];
+    constexpr int SL = CF::SL;
+    if constexpr (G == 0)
+        in.rr = bload<TI>(sr.r, (c0 + (uint32_t)min(tid, CF::C - 1)) * sr.rowh + sr.lane_h);
 #pragma unroll
     for (int j = 0; j < SL; ++j) {
-        const size_t row = (size_t)(c0 + min(SL * wave + j, L - 1)) * H + h;
-        const size_t e = row * DK + ch;
-        in.kk[j] = *reinterpret_cast<const P2*>(gk + e);
-        in.qq[j] = *reinterpret_cast<const P2*>(gq + e);
-        if constexpr (CF::APC) in.al[j] = *reinterpret_cast<const P2*>(ga + e);
-        else in.als[j] = ga[row];
-        if constexpr (CF::DIAG) in.ww[j] = *reinterpret_cast<const P2*>(gw + e);
-        else in.ws[j] = gw[row];
+        const uint32_t tok = c0 + (uint32_t)(SL * wave + j);
+        const uint32_t e = tok * sr.rowk + sr.lane_k, eh = tok * sr.rowh + sr.lane_h;
+        if constexpr (G == 0) {
+            in.kk[j] = bload<P2>(sr.k, e);
+            if constexpr (CF::APC) in.al[j] = bload<P2>(sr.al, e);
+            else in.als[j] = bload<TI>(sr.al, eh);
+        } else {
+            in.qq[j] = bload<P2>(sr.q, e);
+            if constexpr (CF::DIAG) in.ww[j] = bload<P2>(sr.om, e);
+            else in.ws[j] = bload<TI>(sr.om, eh);
+        }
     }
 }
 
 template <class TI, class CF>
-__device__ __forceinline__ void load_v(WalkIn<TI, CF>& in, const WalkArgs& a, int c0, int L,
-                                       int h, int col0, int wave, int lane)
+__device__ __forceinline__ void load_v(WalkIn<TI, CF>& in, const WalkSrc& sr, uint32_t c0,
+                                       int wave, int lane)
 {
-    const int H = a.H, li = lane & 15, lg = lane >> 4;
-    const TI* gv = (const TI*)a.v;
+    const int lg = lane >> 4;
 #pragma unroll
     for (int j = 0; j < CF::XPW; ++j) {
         const int x = min(wave + NW * j, CF::NXT - 1);
-        const int mt = x % CF::NB, nt = x / CF::NB;
+        const int mt = x % CF::NB;
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            const size_t row = (size_t)(c0 + min(16 * mt + 4 * lg + rr, L - 1)) * H + h;
-            in.vv[j][rr] = gv[row * CF::DV + col0 + 16 * nt + li];
+        for (int rr = 0; rr < 4; ++rr)
+            in.vv[j][rr] = bload<TI>(sr.v, (c0 + (uint32_t)(16 * mt + 4 * lg + rr)) * sr.rowv +
+                                               sr.lane_v);
+    }
+}
+
+// Carry of the variance chain into each segment of the chunk, and the decay from the chunk
+// start to each segment: lane l < 16 of wave w takes key channel 16 w + l and walks the chunk
+// carry through the segment summaries in order (eq. chunk-gain-local-prefix). The isotropic
+// variant has one chain per head, which every lane walks alike.
+template <class CF>
+__device__ __forceinline__ void segment_carries(const float4* segA, const float* segG,
+                                                const float2* carry_in, float2* zs, float* gs,
+                                                int wave, int lane)
+{
+    constexpr int DK = CF::DK;
+    const int c = 16 * wave + lane;
+    if (lane < 16 && c < DK) {
+        const int cz = CF::DIAG ? c : 0;
+        float2 z = carry_in[cz];
+        float g = 1.f;
+#pragma unroll
+        for (int p0 = 0; p0 < NW; p0 += 4) {  // summaries read four at a time
+            float4 sa[4];
+            float sg[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                sa[q] = segA[min(p0 + q, NW - 2) * DK + cz];
+                sg[q] = segG[min(p0 + q, NW - 2) * DK + c];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                zs[(p0 + q) * DK + c] = z;
+                gs[(p0 + q) * DK + c] = g;
+                if (p0 + q < NW - 1) {
+                    z = mat_vec(sa[q], z);
+                    g *= sg[q];
+                }
+            }
         }
     }
 }
@@ -271,11 +421,11 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     MT* PbT = (MT*)(smem + CF::OFF_PBT);
     float* Lm = (float*)(smem + CF::OFF_LM);
     MT* Ai = (MT*)(smem + CF::OFF_AI);
-    MT* AiT = (MT*)(smem + CF::OFF_AIT);
     MT* Aq = (MT*)(smem + CF::OFF_AQ);
     float4* segA = (float4*)(smem + CF::OFF_SGA);
     float* segG = (float*)(smem + CF::OFF_SGG);
-    MT* Inv = (MT*)(smem + CF::OFF_INV);
+    float2* zs = (float2*)(smem + CF::OFF_ZS);  // variance carry into each segment
+    float* gs = (float*)(smem + CF::OFF_GS);    // decay from the chunk start to each segment
     MT* SmT = (MT*)(smem + CF::OFF_SMT);
     MT* XT = (MT*)(smem + CF::OFF_XT);
     MT* RT = (MT*)(smem + CF::OFF_RT);
@@ -309,6 +459,24 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     const int pc = min(lane, NP - 1), ch = 2 * pc;  // this lane's key-channel pair
     const bool vact = lane < NP;                    // lane owns a pair in the variance phase
 
+    WalkSrc sr;
+    {
+        constexpr uint32_t es = sizeof(TI);
+        sr.q = make_rsrc(a.q, a.bytes_k);
+        sr.k = make_rsrc(a.k, a.bytes_k);
+        sr.v = make_rsrc(a.v, a.bytes_v);
+        sr.al = make_rsrc(a.alpha, APC ? a.bytes_k : a.bytes_h);
+        sr.om = make_rsrc(a.omega, DIAG ? a.bytes_k : a.bytes_h);
+        sr.r = make_rsrc(a.r, a.bytes_h);
+        sr.rowk = (uint32_t)H * DK * es;
+        sr.rowv = (uint32_t)H * DV * es;
+        sr.rowh = (uint32_t)H * es;
+        sr.lane_k = ((uint32_t)h * DK + ch) * es;
+        sr.lane_h = (uint32_t)h * es;
+        const int nt = min(wave, CF::NXT - 1) / NB;  // every wave holds one X tile at most
+        sr.lane_v = ((uint32_t)h * DV + col0 + 16 * nt + li) * es;
+    }
+
     // ---- initial states ----------------------------------------------------------------
     floatx4 Sacc[CF::SPW];
 #pragma unroll
@@ -339,8 +507,9 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     WalkIn<TI, CF> in;
     if (nch > 0) {
         const int L0 = min(C, t1 - t0);
-        load_main<TI, CF>(in, a, t0, L0, h, ch, wave, tid);
-        load_v<TI, CF>(in, a, t0, L0, h, col0, wave, lane);
+        load_main<0, TI, CF>(in, sr, t0, wave, tid);
+        load_main<1, TI, CF>(in, sr, t0, wave, tid);
+        load_v<TI, CF>(in, sr, t0, wave, lane);
         if (tid < C) {
             const float rv = to_f32(in.rr);
             s_r[tid] = tid < L0 ? rv : 1.f;
@@ -358,37 +527,37 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
 
         // ==== 1-2. variance replay and operands ==========================================
         if constexpr (DIAG) {
-            float av[2][SL], a2[2][SL], wv[2][SL], uu[2][SL], kv[2][SL], qv[2][SL];
-#pragma unroll
-            for (int j = 0; j < SL; ++j) {
-                const int t = SL * wave + j;
-                float2 A = unpack2(in.al[j]), K = unpack2(in.kk[j]), Wv = unpack2(in.ww[j]),
-                       Q = unpack2(in.qq[j]);
-                if (t >= L) {  // past the end: no decay, no noise, zero key and query
+            // token j of this lane's segment, unpacked where it is used (the packed words are
+            // half the registers); past the end: no decay, no noise, zero key and query
+            const int Lw = L - SL * wave;
+            auto tok = [&](int j, float2& A, float2& K, float2& Wv, float2& Q) {
+                A = unpack2(in.al[j]);
+                K = unpack2(in.kk[j]);
+                Wv = unpack2(in.ww[j]);
+                Q = unpack2(in.qq[j]);
+                if (j >= Lw) {
                     A = make_float2(1.f, 1.f);
                     K = Wv = Q = make_float2(0.f, 0.f);
                 }
-                const float mr = s_mr[t];
-                av[0][j] = A.x; av[1][j] = A.y;
-                a2[0][j] = A.x * A.x; a2[1][j] = A.y * A.y;
-                wv[0][j] = Wv.x; wv[1][j] = Wv.y;
-                kv[0][j] = K.x; kv[1][j] = K.y;
-                qv[0][j] = Q.x; qv[1][j] = Q.y;
-                uu[0][j] = K.x * K.x * mr; uu[1][j] = K.y * K.y * mr;
-            }
+            };
+            float mr[SL];
+#pragma unroll
+            for (int j = 0; j < SL; ++j) mr[j] = s_mr[SL * wave + j];
             if (vact) {
                 // the segment's Moebius product (later tokens on the left) and decay product
                 float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
                 float g0 = 1.f, g1 = 1.f;
 #pragma unroll
                 for (int j = 0; j < SL; ++j) {
-                    mob_left(m0, a2[0][j], wv[0][j], uu[0][j]);
-                    mob_left(m1, a2[1][j], wv[1][j], uu[1][j]);
-                    g0 *= av[0][j];
-                    g1 *= av[1][j];
-                    if (j & 1) {
-                        renorm4(m0[0], m0[1], m0[2], m0[3]);
-                        renorm4(m1[0], m1[1], m1[2], m1[3]);
+                    float2 A, K, Wv, Q;
+                    tok(j, A, K, Wv, Q);
+                    mob_left(m0, A.x * A.x, Wv.x, K.x * K.x * mr[j]);
+                    mob_left(m1, A.y * A.y, Wv.y, K.y * K.y * mr[j]);
+                    g0 *= A.x;
+                    g1 *= A.y;
+                    if ((j & 3) == 3 || j == SL - 1) {
+                        rescale4(m0);
+                        rescale4(m1);
                     }
                 }
                 segA[wave * DK + ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
@@ -396,45 +565,41 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                 *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
             }
             __syncthreads();
+            segment_carries<CF>(segA, segG, carry + par * DK, zs, gs, wave, lane);
+            __syncthreads();
             if (vact) {
-                // carry into this segment: the chunk carry through the earlier segments
-                float2 z0 = carry[par * DK + ch], z1 = carry[par * DK + ch + 1];
-                float g0 = 1.f, g1 = 1.f;
-                for (int ps = 0; ps < wave; ++ps) {
-                    z0 = mat_vec(segA[ps * DK + ch], z0);
-                    z1 = mat_vec(segA[ps * DK + ch + 1], z1);
-                    const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
-                    g0 *= gg.x;
-                    g1 *= gg.y;
-                }
+                const float2 z0 = zs[wave * DK + ch], z1 = zs[wave * DK + ch + 1];
+                float g0 = gs[wave * DK + ch], g1 = gs[wave * DK + ch + 1];
                 float n0 = z0.x, d0 = z0.y, n1 = z1.x, d1 = z1.y;
                 float pb0[SL], pb1[SL];
 #pragma unroll
                 for (int j = 0; j < SL; ++j) {
                     const int t = SL * wave + j;
-                    g0 *= av[0][j];
-                    g1 *= av[1][j];
-                    const float nn0 = fmaf(a2[0][j], n0, wv[0][j] * d0);  // p_hat = nn / d
-                    const float nn1 = fmaf(a2[1][j], n1, wv[1][j] * d1);
-                    pb0[j] = nn0 * kv[0][j] * __builtin_amdgcn_rcpf(d0 * g0);  // p_hat k / gamma
-                    pb1[j] = nn1 * kv[1][j] * __builtin_amdgcn_rcpf(d1 * g1);
-                    d0 = fmaf(uu[0][j], nn0, d0);
-                    d1 = fmaf(uu[1][j], nn1, d1);
+                    float2 A, K, Wv, Q;
+                    tok(j, A, K, Wv, Q);
+                    g0 *= A.x;
+                    g1 *= A.y;
+                    const float nn0 = fmaf(A.x * A.x, n0, Wv.x * d0);  // p_hat d
+                    const float nn1 = fmaf(A.y * A.y, n1, Wv.y * d1);
+                    pb0[j] = nn0 * K.x * __builtin_amdgcn_rcpf(d0 * g0);  // p_hat k / gamma
+                    pb1[j] = nn1 * K.y * __builtin_amdgcn_rcpf(d1 * g1);
+                    d0 = fmaf(K.x * K.x * mr[j], nn0, d0);
+                    d1 = fmaf(K.y * K.y * mr[j], nn1, d1);
                     n0 = nn0;
                     n1 = nn1;
-                    if (j & 1) {
-                        renorm2(n0, d0);
-                        renorm2(n1, d1);
+                    if ((j & 3) == 3 || j == SL - 1) {
+                        rescale2(n0, d0);
+                        rescale2(n1, d1);
                     }
-                    st2<MT>(Kb + t * LDK + ch, g0 * kv[0][j], g1 * kv[1][j]);
-                    st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv[0][j], a.scale * g1 * qv[1][j]);
+                    st2<MT>(Kb + t * LDK + ch, g0 * K.x, g1 * K.y);
+                    st2<MT>(Qb + t * LDK + ch, a.scale * g0 * Q.x, a.scale * g1 * Q.y);
                     st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
                 }
                 storeN<MT, SL>(PbT + ch * LDC + SL * wave, pb0);
                 storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
                 if (wave == NW - 1) {
-                    renorm2(n0, d0);
-                    renorm2(n1, d1);
+                    rescale2(n0, d0);
+                    rescale2(n1, d1);
                     carry[(par ^ 1) * DK + ch] = make_float2(n0, d0);
                     carry[(par ^ 1) * DK + ch + 1] = make_float2(n1, d1);
                     *reinterpret_cast<float2*>(gC + ch) = make_float2(g0, g1);
@@ -483,21 +648,17 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     mob_left(mm, aa[j], wt[j], ut[j]);
                     g0 *= ga[0][j];
                     g1 *= ga[1][j];
-                    if (j & 1) renorm4(mm[0], mm[1], mm[2], mm[3]);
+                    if ((j & 3) == 3 || j == SL - 1) rescale4(mm);
                 }
                 if (lane == 0) segA[wave * DK] = make_float4(mm[0], mm[1], mm[2], mm[3]);
                 if (vact) *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
             }
             __syncthreads();
+            segment_carries<CF>(segA, segG, carry + par * DK, zs, gs, wave, lane);
+            __syncthreads();
             {
-                float2 z = carry[par * DK];
-                float g0 = 1.f, g1 = 1.f;
-                for (int ps = 0; ps < wave; ++ps) {
-                    z = mat_vec(segA[ps * DK], z);
-                    const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
-                    g0 *= gg.x;
-                    g1 *= gg.y;
-                }
+                const float2 z = zs[wave * DK + ch];
+                float g0 = gs[wave * DK + ch], g1 = gs[wave * DK + ch + 1];
                 float nz = z.x, dz = z.y;
                 float pb0[SL], pb1[SL];
 #pragma unroll
@@ -511,7 +672,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     pb1[j] = beta * kv[1][j] * __builtin_amdgcn_rcpf(g1);
                     dz = fmaf(ut[j], nn, dz);
                     nz = nn;
-                    if (j & 1) renorm2(nz, dz);
+                    if ((j & 3) == 3 || j == SL - 1) rescale2(nz, dz);
                     if (vact) {
                         st2<MT>(Kb + t * LDK + ch, g0 * kv[0][j], g1 * kv[1][j]);
                         st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv[0][j],
@@ -524,7 +685,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
                 }
                 if (wave == NW - 1) {
-                    renorm2(nz, dz);
+                    rescale2(nz, dz);
                     if (lane == 0) {
                         carry[(par ^ 1) * DK] = make_float2(nz, dz);
                         if (last && a.P_T && vt == 0) a.P_T[nh] = nz / dz;
@@ -534,8 +695,6 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             }
         }
         __syncthreads();
-        // the next chunk's inputs (this lane is done with the current ones except V)
-        load_main<TI, CF>(in, a, c0n, Ln, h, ch, wave, tid);
 
         // ==== 3. L = diag(c) + tril(K_bar P_bar^T, -1) and A_qk = tril(Q_bar P_bar^T) =====
         for (int u = wave; u < CF::NLU; u += NW) {
@@ -557,77 +716,68 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                 }
             }
         }
-        // zero the blocks above the diagonal of A_qk and A (16-byte stores)
+        // zero the blocks above the diagonal of A_qk (16-byte stores)
         {
             constexpr int VPB = 16 * (int)sizeof(MT) / 16;  // 16-byte vectors per block row
             constexpr int NUP = NB * (NB - 1) / 2;
             if constexpr (NUP > 0)
-                for (int idx = tid; idx < 2 * NUP * 16 * VPB; idx += NTH) {
-                    const int which = idx / (NUP * 16 * VPB), rem = idx % (NUP * 16 * VPB);
+                for (int idx = tid; idx < NUP * 16 * VPB; idx += NTH) {
+                    const int rem = idx;
                     int blk = rem / (16 * VPB);
                     const int row16 = (rem / VPB) % 16, vec = rem % VPB;
                     int ib = 0;  // blk -> (ib < jb)
                     while (blk >= NB - 1 - ib) { blk -= NB - 1 - ib; ++ib; }
                     const int jb = ib + 1 + blk;
-                    MT* base = which ? Ai : Aq;
-                    *reinterpret_cast<uint4*>(base + (16 * ib + row16) * LDC + 16 * jb +
+                    *reinterpret_cast<uint4*>(Aq + (16 * ib + row16) * LDC + 16 * jb +
                                               vec * (16 / (int)sizeof(MT))) =
                         make_uint4(0, 0, 0, 0);
                 }
         }
         __syncthreads();
 
-        // ==== 3'. A = L^-1: diagonal blocks by forward substitution (lane = block, column) ==
-        if (wave == 0 && (lane >> 4) < NB) {
-            const int b = lane >> 4, j = li;
+        // ==== 3'. diagonal blocks of L^-1, one row per lane (lane = block, row i) ==========
+        // Row i of A_bb = L_bb^-1 solves a^T L_bb = e_i^T: a_i = 1 / L_ii, and going down the
+        // rows m = i, i-1, ..., 0 every finished a_m adds a_m L_m,k to the sums of the k < m
+        // (right-looking backward substitution, two dependent operations per row; the next
+        // row of L is read while the current one is used). The last wave does this while the
+        // others issue their loads of the next chunk.
+        if (wave == NW - 1 && (lane >> 4) < NB) {
+            const int b = lane >> 4, i = li;
             const float* Lb = Lm + (16 * b) * LDT + 16 * b;
-            float x[16];
+            float s[16], y[16], row[2][16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                float trow[16];
+            for (int kq = 0; kq < 16; ++kq) s[kq] = 0.f;
 #pragma unroll
-                for (int v4 = 0; v4 < (i + 4) / 4; ++v4) {
-                    const float4 q4 = *reinterpret_cast<const float4*>(Lb + i * LDT + 4 * v4);
-                    trow[4 * v4] = q4.x; trow[4 * v4 + 1] = q4.y;
-                    trow[4 * v4 + 2] = q4.z; trow[4 * v4 + 3] = q4.w;
-                }
-                float sum = 0.f;
-#pragma unroll
-                for (int kq = 0; kq < i; ++kq) sum = fmaf(trow[kq], x[kq], sum);
-                x[i] = i < j ? 0.f : ((i == j ? 1.f : 0.f) - sum) / trow[i];
+            for (int v4 = 0; v4 < 4; ++v4) {
+                const float4 q4 = *reinterpret_cast<const float4*>(Lb + 15 * LDT + 4 * v4);
+                row[1][4 * v4] = q4.x; row[1][4 * v4 + 1] = q4.y;
+                row[1][4 * v4 + 2] = q4.z; row[1][4 * v4 + 3] = q4.w;
             }
 #pragma unroll
-            for (int i = 0; i < 16; ++i) Ai[(16 * b + i) * LDC + 16 * b + j] = from_f32<MT>(x[i]);
-            store8<MT>(AiT + (16 * b + j) * LDC + 16 * b, x);
-            store8<MT>(AiT + (16 * b + j) * LDC + 16 * b + 8, x + 8);
+            for (int mq = 15; mq >= 0; --mq) {
+                float* cur = row[mq & 1];
+                if (mq > 0) {
+                    float* nx = row[(mq - 1) & 1];
+#pragma unroll
+                    for (int v4 = 0; v4 < (mq + 3) / 4; ++v4) {
+                        const float4 q4 =
+                            *reinterpret_cast<const float4*>(Lb + (mq - 1) * LDT + 4 * v4);
+                        nx[4 * v4] = q4.x; nx[4 * v4 + 1] = q4.y;
+                        nx[4 * v4 + 2] = q4.z; nx[4 * v4 + 3] = q4.w;
+                    }
+                }
+                const float ym = ((mq == i ? 1.f : 0.f) - s[mq]) * __builtin_amdgcn_rcpf(cur[mq]);
+                y[mq] = mq > i ? 0.f : ym;
+#pragma unroll
+                for (int kq = 0; kq < mq; ++kq) s[kq] = fmaf(y[mq], cur[kq], s[kq]);
+            }
+            store8<MT>(Ai + (16 * b + i) * LDC + 16 * b, y);
+            store8<MT>(Ai + (16 * b + i) * LDC + 16 * b + 8, y + 8);
+        } else if (wave != NW - 1) {
+            load_main<0, TI, CF>(in, sr, c0n, wave, tid);
+            load_main<1, TI, CF>(in, sr, c0n, wave, tid);
         }
         __syncthreads();
-        // off-diagonal blocks, one block diagonal d = ib - jb at a time:
-        //   A_ij = -A_ii sum_{j<=k<i} L_ik A_kj
-#pragma unroll
-        for (int d = 1; d < NB; ++d) {
-            if (wave < NB - d) {
-                const int jb = wave, ib = jb + d;
-                floatx4 acc = zero4();
-                for (int kb = jb; kb < ib; ++kb)
-                    acc = mm16_tv<MT>(Lm + (16 * ib) * LDT + 16 * kb, LDT,
-                                      AiT + (16 * jb) * LDC + 16 * kb, LDC, acc, lane);
-                MT* tmpT = Inv + wave * 16 * CF::LDI;  // transposed: the next B operand
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    tmpT[li * CF::LDI + 4 * lg + rr] = from_f32<MT>(acc[rr]);
-                wave_lds_sync();
-                const floatx4 res = mm_kc<MT, 16>(Ai + (16 * ib) * LDC + 16 * ib, LDC, tmpT,
-                                                  CF::LDI, zero4(), lane);
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int row = 16 * ib + 4 * lg + rr, col = 16 * jb + li;
-                    Ai[row * LDC + col] = from_f32<MT>(-res[rr]);
-                    AiT[col * LDC + row] = from_f32<MT>(-res[rr]);
-                }
-            }
-            __syncthreads();
-        }
 
         // ==== 4. state: X = V - K_bar S and Q_bar S ======================================
 #pragma unroll
@@ -655,26 +805,44 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             }
         }
         __syncthreads();
-        load_v<TI, CF>(in, a, c0n, Ln, h, col0, wave, lane);
+        load_v<TI, CF>(in, sr, c0n, wave, lane);
 
-        // R = A X (A is lower triangular: row block mt needs k < 16 (mt + 1))
+        // R = L^-1 X by block forward substitution, one wave per 16-column tile of the value
+        // block: R_b = A_bb (X_b - sum_{c<b} L_bc R_c), with A_bb the diagonal block inverses.
+        // The chain stays in registers (a result tile is the B fragment of the next product);
+        // R^T goes to LDS for the output and state products. The last wave issues its loads of
+        // the next chunk meanwhile.
+        if (wave < CF::NNT) {
+            using G = F16<MT>;
+            const int nt = wave;
+            typename G::V ad[NB], lo[NB > 1 ? NB * (NB - 1) / 2 : 1];
 #pragma unroll
-        for (int j = 0; j < CF::XPW; ++j) {
-            const int x = wave + NW * j;
-            if (x < CF::NXT) {
-                const int mt = x % NB, nt = x / NB;
-                floatx4 racc = zero4();
+            for (int b = 0; b < NB; ++b) {
+                ad[b] = G::ld(Ai + (16 * b + li) * LDC + 16 * b + 4 * lg);
 #pragma unroll
-                for (int s = 0; s < FC::NS; ++s) {
-                    if (FC::KF * s < 16 * (mt + 1)) {
-                        const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-                        racc = FC::mma(racc, FC::ld(Ai + (16 * mt + li) * LDC + k0),
-                                       FC::ld(XT + (16 * nt + li) * LDC + k0));
-                    }
+                for (int c = 0; c < b; ++c) {
+                    const float4 l4 =
+                        *reinterpret_cast<const float4*>(Lm + (16 * b + li) * LDT + 16 * c + 4 * lg);
+                    lo[b * (b - 1) / 2 + c] = G::pack(l4.x, l4.y, l4.z, l4.w);
                 }
-                store4<MT>(RT + (16 * nt + li) * LDC + 16 * mt + 4 * lg, racc[0], racc[1],
-                           racc[2], racc[3]);
             }
+            floatx4 Rr[NB];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                floatx4 acc = zero4();
+#pragma unroll
+                for (int c = 0; c < b; ++c)
+                    acc = G::mma(acc, lo[b * (b - 1) / 2 + c],
+                                 G::pack(Rr[c][0], Rr[c][1], Rr[c][2], Rr[c][3]));
+                const float4 xb = ld4f<MT>(XT + (16 * nt + li) * LDC + 16 * b + 4 * lg);
+                Rr[b] = G::mma(zero4(), ad[b],
+                               G::pack(xb.x - acc[0], xb.y - acc[1], xb.z - acc[2], xb.w - acc[3]));
+                store4<MT>(RT + (16 * nt + li) * LDC + 16 * b + 4 * lg, Rr[b][0], Rr[b][1],
+                           Rr[b][2], Rr[b][3]);
+            }
+        } else if (wave == NW - 1) {
+            load_main<0, TI, CF>(in, sr, c0n, wave, tid);
+            load_main<1, TI, CF>(in, sr, c0n, wave, tid);
         }
         __syncthreads();
 
@@ -833,6 +1001,10 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
     a.S0 = fc.S0; a.P0 = fc.P0; a.o = fc.o; a.S_T = fc.S_T; a.P_T = fc.P_T;
     a.cu = sa.cu_seqlens; a.order = nullptr;
     a.N = sa.N; a.T = sa.T; a.H = sa.H; a.mu = fc.mu; a.scale = fc.scale;
+    const size_t ntok = (size_t)sa.B * sa.T * sa.H;
+    a.bytes_k = (uint32_t)(ntok * DK * sizeof(TI));
+    a.bytes_v = (uint32_t)(ntok * DV * sizeof(TI));
+    a.bytes_h = (uint32_t)(ntok * sizeof(TI));
     if (packed && sa.N <= ORDER_MAX) {
         int32_t* order = (int32_t*)(ws + wm.order);
         hipLaunchKernelGGL(order_kernel, dim3(1), dim3(1024), 0, st, sa.cu_seqlens, sa.N, order);

@@ -57,7 +57,7 @@ def test_forward_argument_errors(L, variant):
     assert fwd(L, variant, dv=256) == kdn.KDN_ERR_UNSUPPORTED
     assert fwd(L, variant, chunk=24) == kdn.KDN_ERR_UNSUPPORTED
     assert fwd(L, variant, dtype=0, dk=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
-    assert fwd(L, variant, dtype=0, dk=64, dv=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, dtype=0, dk=128, dv=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
     # output aliasing an input
     p = [P(i) for i in range(7)]
     p[6] = p[2]
