@@ -202,8 +202,14 @@ __device__ __forceinline__ float2 mat_vec(const float4& m, float2 v)
 }
 
 // ------------------------------------------------------------------------------------------
-// Configuration and LDS map of one workgroup.
+// Configuration and LDS map of one workgroup. Waves 0..3 (the variance waves) run the variance
+// chain and form the operands of chunk m + 1 while waves 4..7 (the matrix waves) run the
+// triangular solve and the state update of chunk m; the two groups meet at four barriers per
+// chunk, and every SIMD hosts one wave of each, so VALU and MFMA work overlap.
 // ------------------------------------------------------------------------------------------
+constexpr int NVW = 4;  // variance waves: one segment of C / 4 tokens each
+constexpr int NMW = 4;  // matrix waves
+
 template <class TI, int DK_, int DV_, int BV_, int C_, int VARIANT_, bool APC_>
 struct WalkCfg {
     using MT = typename OpOf<TI>::type;
@@ -212,47 +218,48 @@ struct WalkCfg {
     static constexpr bool DIAG = VARIANT_ == 0;
     static constexpr bool APC = APC_ || DIAG;   // gates per key channel
     static constexpr int NV = DV / BV;          // value tiles (workgroups) per head
-    static constexpr int SL = C / NW;           // tokens per variance segment (one per wave)
+    static constexpr int SL = C / NVW;          // tokens per variance segment
     static constexpr int NP = DK / 2;           // key-channel pairs (one per lane)
     static constexpr int NB = C / 16, NNT = BV / 16, NKT = DK / 16;
-    static constexpr int NXT = NB * NNT, XPW = (NXT + NW - 1) / NW;  // X / O tiles
-    static_assert(XPW == 1, "one X / O tile per wave at most");
-    static constexpr int NST = NKT * NNT, SPW = (NST + NW - 1) / NW;  // S tiles
-    static constexpr int NLU = NB * (NB + 1) / 2;                      // lower block pairs
+    static constexpr int NXT = NB * NNT;                                // X / O tiles
+    static constexpr int RPW = (NB + NMW - 1) / NMW;  // row blocks per matrix wave
+    static constexpr int XPW = RPW * NNT;             // X / O tiles per matrix wave
+    static constexpr int JT1 = (SL * 3 + 7) / 8, JT2 = (SL * 6 + 7) / 8;  // replay thirds
+    static constexpr int NST = NKT * NNT, SPW = (NST + NMW - 1) / NMW;  // S tiles
+    static constexpr int NLU = NB * (NB + 1) / 2;                       // lower block pairs
+    static constexpr int NOFF = NB > 1 ? NB * (NB - 1) / 2 : 1;         // below the diagonal
     static constexpr int PAD = 16 / (int)sizeof(MT);  // one 16-byte pad per row
-    static constexpr int LDK = DK + PAD, LDC = C + PAD, LDT = C + 4;
+    static constexpr int LDK = DK + PAD, LDC = C + PAD, LDE = 16 + PAD, LDD = 20;
     static constexpr int LDO = BV + 16 / (int)sizeof(TI);
     static constexpr size_t SZ_OP = al16((size_t)C * LDK * sizeof(MT));
-    static constexpr size_t SZ_CC = al16((size_t)C * LDC * sizeof(MT));
-    // operands of the chunk: K_bar, Q_bar, P_bar [C][LDK] and P_bar^T [DK][LDC]
+    static constexpr size_t SZ_PT = al16((size_t)DK * LDC * sizeof(MT));
+    static constexpr size_t SZ_BL = al16((size_t)16 * LDE * sizeof(MT));
+    // operands of a chunk: K_bar, Q_bar, P_bar [C][LDK]; P_bar^T [DK][LDC] in two buffers
+    // (chunk parity: the variance waves write chunk m + 1's while the matrix waves read m's)
     static constexpr size_t OFF_KB = 0;
     static constexpr size_t OFF_QB = OFF_KB + SZ_OP;
     static constexpr size_t OFF_PB = OFF_QB + SZ_OP;
     static constexpr size_t OFF_PBT = OFF_PB + SZ_OP;
-    // one region holding either the chunk's triangular matrices (L float32 [C][LDT]; the
-    // diagonal blocks of L^-1 and A_qk [C][LDC]) or, while the variance runs, the segment
-    // summaries
-    static constexpr size_t OFF_U = OFF_PBT + al16((size_t)DK * LDC * sizeof(MT));
-    static constexpr size_t OFF_LM = OFF_U;
-    static constexpr size_t OFF_AI = OFF_LM + al16((size_t)C * LDT * 4);
-    static constexpr size_t OFF_AQ = OFF_AI + SZ_CC;
-    static constexpr size_t SZ_MAT = OFF_AQ + SZ_CC - OFF_U;
-    static constexpr size_t OFF_SGA = OFF_U;                           // float4 [NW][DK]
-    static constexpr size_t OFF_SGG = OFF_SGA + (size_t)NW * DK * 16;  // float [NW][DK]
-    static constexpr size_t OFF_ZS = OFF_SGG + (size_t)NW * DK * 4;    // float2 [NW][DK]
-    static constexpr size_t OFF_GS = OFF_ZS + (size_t)NW * DK * 8;     // float [NW][DK]
-    static constexpr size_t SZ_SEG = (size_t)NW * DK * 32;
+    // L's diagonal blocks (float32 [NB][16][LDD]) and the blocks below them (MT, MFMA
+    // operands), the diagonal blocks of L^-1 and A_qk [C][LDC]
+    static constexpr size_t OFF_LD = OFF_PBT + 2 * SZ_PT;
+    static constexpr size_t OFF_LO = OFF_LD + al16((size_t)NB * 16 * LDD * 4);
+    static constexpr size_t OFF_AI = OFF_LO + NOFF * SZ_BL;
+    static constexpr size_t OFF_AQ = OFF_AI + NB * SZ_BL;
+    // the variance waves' segment summaries and their decay products
+    static constexpr size_t OFF_SGA = OFF_AQ + al16((size_t)C * LDC * sizeof(MT));
+    static constexpr size_t OFF_SGG = OFF_SGA + (size_t)NVW * DK * 16;
     // S^T [BV][LDK], X^T and R^T [BV][LDC] in MT, O staging [C][LDO] in TI
-    static constexpr size_t OFF_SMT = OFF_U + al16(cmax(SZ_MAT, SZ_SEG));
+    static constexpr size_t OFF_SMT = OFF_SGG + (size_t)NVW * DK * 4;
     static constexpr size_t OFF_XT = OFF_SMT + al16((size_t)BV * LDK * sizeof(MT));
     static constexpr size_t OFF_RT = OFF_XT + al16((size_t)BV * LDC * sizeof(MT));
     static constexpr size_t OFF_O = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));
-    // variance carry (two buffers, by chunk parity), gamma_C, r and mu / r of the chunk
+    // by chunk parity: variance carry into the chunk, gamma_C, r and mu / r
     static constexpr size_t OFF_CAR = OFF_O + al16((size_t)C * LDO * sizeof(TI));
     static constexpr size_t OFF_GC = OFF_CAR + (size_t)2 * DK * 8;
-    static constexpr size_t OFF_R = OFF_GC + (size_t)DK * 4;
-    static constexpr size_t OFF_MR = OFF_R + (size_t)C * 4;
-    static constexpr size_t TOTAL = al16(OFF_MR + (size_t)C * 4);
+    static constexpr size_t OFF_R = OFF_GC + (size_t)2 * DK * 4;
+    static constexpr size_t OFF_MR = OFF_R + (size_t)2 * C * 4;
+    static constexpr size_t TOTAL = al16(OFF_MR + (size_t)2 * C * 4);
 };
 
 struct WalkArgs {
@@ -299,111 +306,120 @@ template <> __device__ __forceinline__ bf16 bload<bf16>(rsrc_t r, uint32_t off)
     return __builtin_bit_cast(bf16, __builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0));
 }
 
+// One stored value held in a register of its own: a bf16 is kept zero-extended in 32 bits, so
+// values loaded ahead are never packed two to a register (packing would wait for the load).
+template <class TI> struct Raw1;
+template <> struct Raw1<bf16> {
+    using type = unsigned;
+    static __device__ __forceinline__ unsigned load(rsrc_t r, uint32_t off)
+    {
+        return (unsigned)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+    }
+    static __device__ __forceinline__ float f32(unsigned u) { return __uint_as_float(u << 16); }
+};
+template <> struct Raw1<float> {
+    using type = float;
+    static __device__ __forceinline__ float load(rsrc_t r, uint32_t off)
+    {
+        return bload<float>(r, off);
+    }
+    static __device__ __forceinline__ float f32(float x) { return x; }
+};
+
 // Descriptors and byte strides of one workgroup's inputs.
 struct WalkSrc {
     rsrc_t q, k, v, al, om, r;
-    uint32_t rowk, rowv, rowh;     // bytes per token row: channel tensors, v, per-head scalars
-    uint32_t lane_k, lane_h;       // this lane's byte offset within a row (channel pair; head)
-    uint32_t lane_v;               // this lane's byte offset within a row of v (its X tile)
+    uint32_t rowk, rowv, rowh;  // bytes per token row: channel tensors, v, per-head scalars
+    uint32_t lane_k, lane_h;    // this lane's byte offset within a row (channel pair; head)
+    uint32_t col_v;             // byte offset of the workgroup's first value column in a row
 };
 
-// Raw inputs of one chunk held by one lane, loaded a chunk ahead and kept in storage precision
-// (a conversion next to its load would make the load wait for everything issued before it).
-// Lane l of wave w holds tokens [SL w, SL w + SL) of the key-channel pair (2 l, 2 l + 1).
+// Raw inputs of one chunk held by a variance lane (lane l of wave w: tokens [SL w, SL w + SL)
+// of the key-channel pair (2 l, 2 l + 1)), loaded ahead and kept in storage precision (a
+// conversion next to its load would make the load wait for everything issued before it).
 template <class TI, class CF>
 struct WalkIn {
     using P2 = typename CF::P2;
     P2 kk[CF::SL], qq[CF::SL];
     P2 al[CF::APC ? CF::SL : 1];    // per-channel gates
     P2 ww[CF::DIAG ? CF::SL : 1];   // per-channel process noise (diagonal)
-    TI als[CF::APC ? 1 : CF::SL];   // one gate per head (isotropic, scalar gates)
-    TI ws[CF::DIAG ? 1 : CF::SL];   // one process noise per head (isotropic)
-    TI rr;                          // r of token tid (tid < C)
-    TI vv[CF::XPW][4];              // V at this lane's rows and column of its X tiles
+    using R1 = typename Raw1<TI>::type;
+    R1 als[CF::APC ? 1 : CF::SL];   // one gate per head (isotropic, scalar gates)
+    R1 ws[CF::DIAG ? 1 : CF::SL];   // one process noise per head (isotropic)
+    R1 rr;                          // r of token tid of the next chunk (tid < C)
 };
 
-// The next chunk's raw inputs in two groups issued at different points of the current chunk
-// (a wave that issues all of them at once stalls until the memory pipeline drains): group 0
-// holds k, the gates and r, group 1 the process noise and q.
-template <int G, class TI, class CF>
-__device__ __forceinline__ void load_main(WalkIn<TI, CF>& in, const WalkSrc& sr, uint32_t c0,
-                                          int wave, int tid)
+// Tokens [J0, J1) of a variance lane's segment of the chunk starting at token c0.
+template <int J0, int J1, class TI, class CF>
+__device__ __forceinline__ void load_part(WalkIn<TI, CF>& in, const WalkSrc& sr, uint32_t c0,
+                                          int vw)
 {
     using P2 = typename CF::P2;
-    constexpr int SL = CF::SL;
-    if constexpr (G == 0)
-        in.rr = bload<TI>(sr.r, (c0 + (uint32_t)min(tid, CF::C - 1)) * sr.rowh + sr.lane_h);
 #pragma unroll
-    for (int j = 0; j < SL; ++j) {
-        const uint32_t tok = c0 + (uint32_t)(SL * wave + j);
+    for (int j = J0; j < J1; ++j) {
+        const uint32_t tok = c0 + (uint32_t)(CF::SL * vw + j);
         const uint32_t e = tok * sr.rowk + sr.lane_k, eh = tok * sr.rowh + sr.lane_h;
-        if constexpr (G == 0) {
-            in.kk[j] = bload<P2>(sr.k, e);
-            if constexpr (CF::APC) in.al[j] = bload<P2>(sr.al, e);
-            else in.als[j] = bload<TI>(sr.al, eh);
-        } else {
-            in.qq[j] = bload<P2>(sr.q, e);
-            if constexpr (CF::DIAG) in.ww[j] = bload<P2>(sr.om, e);
-            else in.ws[j] = bload<TI>(sr.om, eh);
-        }
+        in.kk[j] = bload<P2>(sr.k, e);
+        in.qq[j] = bload<P2>(sr.q, e);
+        if constexpr (CF::APC) in.al[j] = bload<P2>(sr.al, e);
+        else in.als[j] = Raw1<TI>::load(sr.al, eh);
+        if constexpr (CF::DIAG) in.ww[j] = bload<P2>(sr.om, e);
+        else in.ws[j] = Raw1<TI>::load(sr.om, eh);
     }
 }
 
-template <class TI, class CF>
-__device__ __forceinline__ void load_v(WalkIn<TI, CF>& in, const WalkSrc& sr, uint32_t c0,
-                                       int wave, int lane)
+// Token j of a variance lane's segment in float32. In a chunk that may end early (MK), a
+// token past the end of the sequence (j >= Lw) reads as no decay, no noise and zero key and
+// query, so it leaves the variance and the memory unchanged and gives zero operand rows. The
+// registers loaded ahead are only read here, never overwritten.
+struct TokIn {
+    float2 K, Q, A, W;
+};
+template <bool MK, class TI, class CF>
+__device__ __forceinline__ TokIn tok_in(const WalkIn<TI, CF>& in, int j, int Lw)
 {
-    const int lg = lane >> 4;
+    const bool pad = MK && j >= Lw;
+    const float2 z = make_float2(0.f, 0.f);
+    TokIn r;
+    r.K = pad ? z : unpack2(in.kk[j]);
+    r.Q = pad ? z : unpack2(in.qq[j]);
+    if constexpr (CF::APC) {
+        r.A = pad ? make_float2(1.f, 1.f) : unpack2(in.al[j]);
+    } else {
+        const float as = pad ? 1.f : Raw1<TI>::f32(in.als[CF::APC ? 0 : j]);
+        r.A = make_float2(as, as);
+    }
+    if constexpr (CF::DIAG) {
+        r.W = pad ? z : unpack2(in.ww[j]);
+    } else {
+        const float w = pad ? 0.f : Raw1<TI>::f32(in.ws[CF::DIAG ? 0 : j]);
+        r.W = make_float2(w, w);
+    }
+    return r;
+}
+
+// V at the rows and column of a matrix lane's X tiles: tile j of matrix wave mw is row block
+// mw + 4 (j / NNT), column tile j % NNT.
+template <class TI, class CF>
+__device__ __forceinline__ void load_v(typename Raw1<TI>::type (&vv)[CF::XPW][4], const WalkSrc& sr,
+                                       uint32_t c0,
+                                       int mw, int lane)
+{
+    const int li = lane & 15, lg = lane >> 4;
 #pragma unroll
     for (int j = 0; j < CF::XPW; ++j) {
-        const int x = min(wave + NW * j, CF::NXT - 1);
-        const int mt = x % CF::NB;
+        const int ib = min(mw + NMW * (j / CF::NNT), CF::NB - 1), nt = j % CF::NNT;
+        const uint32_t col = sr.col_v + (uint32_t)(16 * nt + li) * (uint32_t)sizeof(TI);
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr)
-            in.vv[j][rr] = bload<TI>(sr.v, (c0 + (uint32_t)(16 * mt + 4 * lg + rr)) * sr.rowv +
-                                               sr.lane_v);
-    }
-}
-
-// Carry of the variance chain into each segment of the chunk, and the decay from the chunk
-// start to each segment: lane l < 16 of wave w takes key channel 16 w + l and walks the chunk
-// carry through the segment summaries in order (eq. chunk-gain-local-prefix). The isotropic
-// variant has one chain per head, which every lane walks alike.
-template <class CF>
-__device__ __forceinline__ void segment_carries(const float4* segA, const float* segG,
-                                                const float2* carry_in, float2* zs, float* gs,
-                                                int wave, int lane)
-{
-    constexpr int DK = CF::DK;
-    const int c = 16 * wave + lane;
-    if (lane < 16 && c < DK) {
-        const int cz = CF::DIAG ? c : 0;
-        float2 z = carry_in[cz];
-        float g = 1.f;
-#pragma unroll
-        for (int p0 = 0; p0 < NW; p0 += 4) {  // summaries read four at a time
-            float4 sa[4];
-            float sg[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                sa[q] = segA[min(p0 + q, NW - 2) * DK + cz];
-                sg[q] = segG[min(p0 + q, NW - 2) * DK + c];
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                zs[(p0 + q) * DK + c] = z;
-                gs[(p0 + q) * DK + c] = g;
-                if (p0 + q < NW - 1) {
-                    z = mat_vec(sa[q], z);
-                    g *= sg[q];
-                }
-            }
-        }
+            vv[j][rr] =
+                Raw1<TI>::load(sr.v, (c0 + (uint32_t)(16 * ib + 4 * lg + rr)) * sr.rowv + col);
     }
 }
 
 // ------------------------------------------------------------------------------------------
-// The walk: one workgroup per (sequence, head, value tile).
+// The walk: one workgroup per (sequence, head, value tile). Iteration it runs the variance
+// waves on chunk it and the matrix waves on chunk it - 1.
 // ------------------------------------------------------------------------------------------
 template <class TI, class CF>
 __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
@@ -411,32 +427,39 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     using MT = typename CF::MT;
     using FK = Frag<MT, CF::DK>;
     using FC = Frag<MT, CF::C>;
-    constexpr int DK = CF::DK, DV = CF::DV, BV = CF::BV, C = CF::C, SL = CF::SL, NP = CF::NP;
-    constexpr int NB = CF::NB, LDK = CF::LDK, LDC = CF::LDC, LDT = CF::LDT, LDO = CF::LDO;
+    using G = F16<MT>;
+    constexpr int DK = CF::DK, DV = CF::DV, BV = CF::BV, C = CF::C, SL = CF::SL;
+    constexpr int NP = CF::NP, NB = CF::NB, LDK = CF::LDK, LDC = CF::LDC, LDE = CF::LDE;
+    constexpr int LDD = CF::LDD, LDO = CF::LDO;
     constexpr bool DIAG = CF::DIAG, APC = CF::APC;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     MT* Kb = (MT*)(smem + CF::OFF_KB);
     MT* Qb = (MT*)(smem + CF::OFF_QB);
     MT* Pb = (MT*)(smem + CF::OFF_PB);
-    MT* PbT = (MT*)(smem + CF::OFF_PBT);
-    float* Lm = (float*)(smem + CF::OFF_LM);
+    MT* PbT0 = (MT*)(smem + CF::OFF_PBT);  // [2][DK][LDC]
+    float* Ld = (float*)(smem + CF::OFF_LD);
+    MT* Lo = (MT*)(smem + CF::OFF_LO);
     MT* Ai = (MT*)(smem + CF::OFF_AI);
     MT* Aq = (MT*)(smem + CF::OFF_AQ);
     float4* segA = (float4*)(smem + CF::OFF_SGA);
     float* segG = (float*)(smem + CF::OFF_SGG);
-    float2* zs = (float2*)(smem + CF::OFF_ZS);  // variance carry into each segment
-    float* gs = (float*)(smem + CF::OFF_GS);    // decay from the chunk start to each segment
     MT* SmT = (MT*)(smem + CF::OFF_SMT);
     MT* XT = (MT*)(smem + CF::OFF_XT);
     MT* RT = (MT*)(smem + CF::OFF_RT);
     TI* Ost = (TI*)(smem + CF::OFF_O);
-    float2* carry = (float2*)(smem + CF::OFF_CAR);
-    float* gC = (float*)(smem + CF::OFF_GC);
-    float* s_r = (float*)(smem + CF::OFF_R);
-    float* s_mr = (float*)(smem + CF::OFF_MR);
+    float2* carry = (float2*)(smem + CF::OFF_CAR);  // [2][DK]
+    float* gC = (float*)(smem + CF::OFF_GC);        // [2][DK]
+    float* s_r = (float*)(smem + CF::OFF_R);        // [2][C]
+    float* s_mr = (float*)(smem + CF::OFF_MR);      // [2][C]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int li = lane & 15, lg = lane >> 4;
+    // the wave index in a scalar register: the variance / matrix split is a uniform branch,
+    // so each wave runs exactly one of the two loops below (with four barriers per chunk each)
+    const int wu = __builtin_amdgcn_readfirstlane(wave);
+    const bool vgrp = wu < NVW;   // variance wave (else matrix wave)
+    const int vw = wu, mw = wu - NVW;
+    const int mtid = tid - 64 * NVW;  // thread index within the matrix waves
 
     // block -> (sequence-head slot, value tile): the NV tiles of one head get block indices
     // congruent modulo 8, so round-robin dispatch puts them on one XCD, where they share the
@@ -456,8 +479,8 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     const int nch = (t1 - t0 + C - 1) / C;
     TI* go = (TI*)a.o;
 
-    const int pc = min(lane, NP - 1), ch = 2 * pc;  // this lane's key-channel pair
-    const bool vact = lane < NP;                    // lane owns a pair in the variance phase
+    const int pc = min(lane, NP - 1), ch = 2 * pc;  // a variance lane's key-channel pair
+    const bool vact = lane < NP;                    // the lane owns a pair
 
     WalkSrc sr;
     {
@@ -473,448 +496,512 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
         sr.rowh = (uint32_t)H * es;
         sr.lane_k = ((uint32_t)h * DK + ch) * es;
         sr.lane_h = (uint32_t)h * es;
-        const int nt = min(wave, CF::NXT - 1) / NB;  // every wave holds one X tile at most
-        sr.lane_v = ((uint32_t)h * DV + col0 + 16 * nt + li) * es;
+        sr.col_v = ((uint32_t)h * DV + col0) * es;
     }
 
     // ---- initial states ----------------------------------------------------------------
-    floatx4 Sacc[CF::SPW];
+    floatx4 Sacc[CF::SPW];  // matrix waves: S tiles (it, nt) = (x % NKT, x / NKT), x = mw + 4 j
+    if (!vgrp) {
 #pragma unroll
-    for (int j = 0; j < CF::SPW; ++j) {
-        const int x = wave + NW * j;
-        Sacc[j] = zero4();
-        if (x < CF::NST) {
-            const int it = x % CF::NKT, nt = x / CF::NKT;
-            if (a.S0) {
-                const float* src = a.S0 + (size_t)nh * DK * DV;
+        for (int j = 0; j < CF::SPW; ++j) {
+            const int x = mw + NMW * j;
+            Sacc[j] = zero4();
+            if (x < CF::NST) {
+                const int it = x % CF::NKT, nt = x / CF::NKT;
+                if (a.S0) {
+                    const float* src = a.S0 + (size_t)nh * DK * DV;
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    Sacc[j][rr] = src[(size_t)(16 * it + 4 * lg + rr) * DV + col0 + 16 * nt + li];
+                    for (int rr = 0; rr < 4; ++rr)
+                        Sacc[j][rr] =
+                            src[(size_t)(16 * it + 4 * lg + rr) * DV + col0 + 16 * nt + li];
+                }
+                store4<MT>(SmT + (16 * nt + li) * LDK + 16 * it + 4 * lg, Sacc[j][0],
+                           Sacc[j][1], Sacc[j][2], Sacc[j][3]);
             }
-            store4<MT>(SmT + (16 * nt + li) * LDK + 16 * it + 4 * lg, Sacc[j][0], Sacc[j][1],
-                       Sacc[j][2], Sacc[j][3]);
         }
     }
     if (DIAG ? tid < DK : tid == 0)
         carry[tid] = make_float2(a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f, 1.f);
-
-    if (nch == 0) {  // empty sequence: the states pass through
-        if (a.P_T && vt == 0 && (DIAG ? tid < DK : tid == 0))
-            a.P_T[(size_t)nh * (DIAG ? DK : 1) + tid] =
-                a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f;
-    }
+    if (nch == 0 && a.P_T && vt == 0 && (DIAG ? tid < DK : tid == 0))  // empty sequence
+        a.P_T[(size_t)nh * (DIAG ? DK : 1) + tid] =
+            a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f;
 
     WalkIn<TI, CF> in;
+    typename Raw1<TI>::type vv[CF::XPW][4];
+    floatx4 Oacc[CF::XPW];
     if (nch > 0) {
-        const int L0 = min(C, t1 - t0);
-        load_main<0, TI, CF>(in, sr, t0, wave, tid);
-        load_main<1, TI, CF>(in, sr, t0, wave, tid);
-        load_v<TI, CF>(in, sr, t0, wave, lane);
-        if (tid < C) {
-            const float rv = to_f32(in.rr);
-            s_r[tid] = tid < L0 ? rv : 1.f;
-            s_mr[tid] = tid < L0 ? a.mu / rv : 0.f;
+        if (vgrp) {
+            load_part<0, SL, TI, CF>(in, sr, t0, vw);
+            if (tid < C) {
+                const float rv =
+                    to_f32(bload<TI>(sr.r, (uint32_t)(t0 + tid) * sr.rowh + sr.lane_h));
+                const bool ok = tid < t1 - t0;
+                s_r[tid] = ok ? rv : 1.f;
+                s_mr[tid] = ok ? a.mu / rv : 0.f;
+            }
+        } else {
+            load_v<TI, CF>(vv, sr, t0, mw, lane);
         }
     }
     __syncthreads();
 
-    floatx4 Oacc[CF::XPW];
-    for (int m = 0; m < nch; ++m) {
-        const int c0 = t0 + m * C, L = min(C, t1 - c0);
-        const bool last = m == nch - 1;
-        const int par = m & 1;
-        const int c0n = last ? c0 : c0 + C, Ln = last ? L : min(C, t1 - c0n);
+    if (vgrp) {
+        // ===== variance waves: chunk it; wave w takes tokens [SL w, SL w + SL) ===============
+        float kn[DIAG ? 1 : SL], ka[DIAG ? 1 : SL];  // isotropic: ||k_t||^2 and mean alpha^2
+        for (int it = 0; it <= nch; ++it) {
+            const int mv = it;
+            const bool vwork = mv < nch, vlast = mv == nch - 1;
+            const int pv = mv & 1;
+            const int c0v = t0 + mv * C, Lv = min(C, t1 - c0v);
+            const int Lw = Lv - SL * vw;  // tokens of this wave's segment in the chunk
+            const float* s_rv = s_r + pv * C;
+            const float* s_mrv = s_mr + pv * C;
+            MT* PbTv = PbT0 + (size_t)pv * DK * LDC;
+            const uint32_t c0n = (uint32_t)(c0v + C);  // the next chunk
 
-        // ==== 1-2. variance replay and operands ==========================================
-        if constexpr (DIAG) {
-            // token j of this lane's segment, unpacked where it is used (the packed words are
-            // half the registers); past the end: no decay, no noise, zero key and query
-            const int Lw = L - SL * wave;
-            auto tok = [&](int j, float2& A, float2& K, float2& Wv, float2& Q) {
-                A = unpack2(in.al[j]);
-                K = unpack2(in.kk[j]);
-                Wv = unpack2(in.ww[j]);
-                Q = unpack2(in.qq[j]);
-                if (j >= Lw) {
-                    A = make_float2(1.f, 1.f);
-                    K = Wv = Q = make_float2(0.f, 0.f);
+            // ---- phase A: the segment's Moebius product and decay product ------------------
+            auto summary = [&](auto mk_c) {
+                constexpr bool MK = decltype(mk_c)::value;
+                if constexpr (DIAG) {
+                    if (vact) {
+                        float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
+                        float g0 = 1.f, g1 = 1.f;
+#pragma unroll
+                        for (int j = 0; j < SL; ++j) {
+                            const TokIn x = tok_in<MK>(in, j, Lw);
+                            const float mr = s_mrv[SL * vw + j];
+                            mob_left(m0, x.A.x * x.A.x, x.W.x, x.K.x * x.K.x * mr);
+                            mob_left(m1, x.A.y * x.A.y, x.W.y, x.K.y * x.K.y * mr);
+                            g0 *= x.A.x;
+                            g1 *= x.A.y;
+                            if ((j & 3) == 3 || j == SL - 1) {
+                                rescale4(m0);
+                                rescale4(m1);
+                            }
+                        }
+                        segA[vw * DK + ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
+                        segA[vw * DK + ch + 1] = make_float4(m1[0], m1[1], m1[2], m1[3]);
+                        *reinterpret_cast<float2*>(segG + vw * DK + ch) = make_float2(g0, g1);
+                    }
+                } else {
+                    // per-token ||k||^2 and mean_i alpha_i^2 by wave reductions, kept for the
+                    // replay; one scalar chain per head, which every lane runs alike
+                    float mm[4] = {1.f, 0.f, 0.f, 1.f};
+                    float g0 = 1.f, g1 = 1.f;
+#pragma unroll
+                    for (int j = 0; j < SL; ++j) {
+                        const TokIn x = tok_in<MK>(in, j, Lw);
+                        kn[j] = wave_sum(vact ? fmaf(x.K.x, x.K.x, x.K.y * x.K.y) : 0.f);
+                        if constexpr (APC)
+                            ka[j] = wave_sum(vact ? fmaf(x.A.x, x.A.x, x.A.y * x.A.y) : 0.f) *
+                                    (1.f / (float)DK);
+                        else
+                            ka[j] = x.A.x * x.A.x;
+                        g0 *= x.A.x;
+                        g1 *= x.A.y;
+                        const float ut = kn[j] * s_mrv[SL * vw + j] * (1.f / (float)DK);
+                        mob_left(mm, ka[j], x.W.x, ut);
+                        if ((j & 3) == 3 || j == SL - 1) rescale4(mm);
+                    }
+                    if (lane == 0) segA[vw * DK] = make_float4(mm[0], mm[1], mm[2], mm[3]);
+                    if (vact) *reinterpret_cast<float2*>(segG + vw * DK + ch) = make_float2(g0, g1);
                 }
             };
-            float mr[SL];
+            if (vwork) {
+                if (Lw < SL) summary(std::true_type());  // a partial last chunk only
+                else summary(std::false_type());
+                // r of the next chunk, written to LDS at the end of the iteration (past the end
+                // of the sequence the value is never used)
+                if (tid < C) in.rr = Raw1<TI>::load(sr.r, (c0n + (uint32_t)tid) * sr.rowh + sr.lane_h);
+            }
+            __syncthreads();
+
+            // ---- phases B, C, D: the carry into the segment, then the replay in thirds -----
+            // variance chain state (n, d) per channel (one per head for the isotropic variant)
+            // and the decay since the chunk start, carried from third to third
+            float n0 = 0.f, d0 = 1.f, n1 = 0.f, d1 = 1.f, g0 = 1.f, g1 = 1.f;
+            float pb0[SL], pb1[SL];
+            auto replay_mk = [&](auto ja_c, auto jb_c, auto mk_c) {
+                constexpr int JA = decltype(ja_c)::value, JB = decltype(jb_c)::value;
+                constexpr bool MK = decltype(mk_c)::value;
 #pragma unroll
-            for (int j = 0; j < SL; ++j) mr[j] = s_mr[SL * wave + j];
-            if (vact) {
-                // the segment's Moebius product (later tokens on the left) and decay product
-                float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
-                float g0 = 1.f, g1 = 1.f;
-#pragma unroll
-                for (int j = 0; j < SL; ++j) {
-                    float2 A, K, Wv, Q;
-                    tok(j, A, K, Wv, Q);
-                    mob_left(m0, A.x * A.x, Wv.x, K.x * K.x * mr[j]);
-                    mob_left(m1, A.y * A.y, Wv.y, K.y * K.y * mr[j]);
+                for (int j = JA; j < JB; ++j) {
+                    const int t = SL * vw + j;
+                    const TokIn x = tok_in<MK>(in, j, Lw);
+                    const float2 K = x.K, Q = x.Q, A = x.A;
                     g0 *= A.x;
                     g1 *= A.y;
-                    if ((j & 3) == 3 || j == SL - 1) {
-                        rescale4(m0);
-                        rescale4(m1);
+                    if constexpr (DIAG) {
+                        const float mr = s_mrv[t];
+                        const float nn0 = fmaf(A.x * A.x, n0, x.W.x * d0);  // p_hat d
+                        const float nn1 = fmaf(A.y * A.y, n1, x.W.y * d1);
+                        pb0[j] = nn0 * K.x * __builtin_amdgcn_rcpf(d0 * g0);  // p_hat k / gamma
+                        pb1[j] = nn1 * K.y * __builtin_amdgcn_rcpf(d1 * g1);
+                        d0 = fmaf(K.x * K.x * mr, nn0, d0);
+                        d1 = fmaf(K.y * K.y * mr, nn1, d1);
+                        n0 = nn0;
+                        n1 = nn1;
+                        if ((j & 3) == 3 || j == SL - 1) {
+                            rescale2(n0, d0);
+                            rescale2(n1, d1);
+                        }
+                    } else {
+                        const float nn = fmaf(ka[j], n0, x.W.x * d0);  // b_hat d
+                        const float beta = nn / fmaf(d0, s_rv[t], nn * kn[j]);
+                        pb0[j] = beta * K.x * __builtin_amdgcn_rcpf(g0);
+                        pb1[j] = beta * K.y * __builtin_amdgcn_rcpf(g1);
+                        d0 = fmaf(kn[j] * s_mrv[t] * (1.f / (float)DK), nn, d0);
+                        n0 = nn;
+                        if ((j & 3) == 3 || j == SL - 1) rescale2(n0, d0);
                     }
-                }
-                segA[wave * DK + ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
-                segA[wave * DK + ch + 1] = make_float4(m1[0], m1[1], m1[2], m1[3]);
-                *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
-            }
-            __syncthreads();
-            segment_carries<CF>(segA, segG, carry + par * DK, zs, gs, wave, lane);
-            __syncthreads();
-            if (vact) {
-                const float2 z0 = zs[wave * DK + ch], z1 = zs[wave * DK + ch + 1];
-                float g0 = gs[wave * DK + ch], g1 = gs[wave * DK + ch + 1];
-                float n0 = z0.x, d0 = z0.y, n1 = z1.x, d1 = z1.y;
-                float pb0[SL], pb1[SL];
-#pragma unroll
-                for (int j = 0; j < SL; ++j) {
-                    const int t = SL * wave + j;
-                    float2 A, K, Wv, Q;
-                    tok(j, A, K, Wv, Q);
-                    g0 *= A.x;
-                    g1 *= A.y;
-                    const float nn0 = fmaf(A.x * A.x, n0, Wv.x * d0);  // p_hat d
-                    const float nn1 = fmaf(A.y * A.y, n1, Wv.y * d1);
-                    pb0[j] = nn0 * K.x * __builtin_amdgcn_rcpf(d0 * g0);  // p_hat k / gamma
-                    pb1[j] = nn1 * K.y * __builtin_amdgcn_rcpf(d1 * g1);
-                    d0 = fmaf(K.x * K.x * mr[j], nn0, d0);
-                    d1 = fmaf(K.y * K.y * mr[j], nn1, d1);
-                    n0 = nn0;
-                    n1 = nn1;
-                    if ((j & 3) == 3 || j == SL - 1) {
-                        rescale2(n0, d0);
-                        rescale2(n1, d1);
-                    }
-                    st2<MT>(Kb + t * LDK + ch, g0 * K.x, g1 * K.y);
-                    st2<MT>(Qb + t * LDK + ch, a.scale * g0 * Q.x, a.scale * g1 * Q.y);
-                    st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
-                }
-                storeN<MT, SL>(PbT + ch * LDC + SL * wave, pb0);
-                storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
-                if (wave == NW - 1) {
-                    rescale2(n0, d0);
-                    rescale2(n1, d1);
-                    carry[(par ^ 1) * DK + ch] = make_float2(n0, d0);
-                    carry[(par ^ 1) * DK + ch + 1] = make_float2(n1, d1);
-                    *reinterpret_cast<float2*>(gC + ch) = make_float2(g0, g1);
-                    if (last && a.P_T && vt == 0)  // the sequence's final variances n / d
-                        *reinterpret_cast<float2*>(a.P_T + (size_t)nh * DK + ch) =
-                            make_float2(n0 / d0, n1 / d1);
-                }
-            }
-        } else {
-            // isotropic: per-token ||k||^2 and mean_i alpha_i^2 by wave reductions; one scalar
-            // chain per head, which every lane of a wave runs alike
-            float kv[2][SL], qv[2][SL], ga[2][SL], aa[SL], wt[SL], ut[SL], nk[SL], rt[SL];
-#pragma unroll
-            for (int j = 0; j < SL; ++j) {
-                const int t = SL * wave + j;
-                const bool ok = t < L;
-                float2 K = unpack2(in.kk[j]), Q = unpack2(in.qq[j]);
-                float2 A = make_float2(1.f, 1.f);
-                if constexpr (APC) A = unpack2(in.al[j]);
-                if (!ok) {
-                    K = Q = make_float2(0.f, 0.f);
-                    A = make_float2(1.f, 1.f);
-                }
-                const float as = (ok && !APC) ? to_f32(in.als[APC ? 0 : j]) : 1.f;
-                kv[0][j] = K.x; kv[1][j] = K.y;
-                qv[0][j] = Q.x; qv[1][j] = Q.y;
-                ga[0][j] = APC ? A.x : as;
-                ga[1][j] = APC ? A.y : as;
-                float sk = vact ? fmaf(K.x, K.x, K.y * K.y) : 0.f;
-                nk[j] = wave_sum(sk);
-                if constexpr (APC) {
-                    const float sa = vact ? fmaf(A.x, A.x, A.y * A.y) : 0.f;
-                    aa[j] = wave_sum(sa) * (1.f / (float)DK);
-                } else {
-                    aa[j] = as * as;
-                }
-                wt[j] = ok ? to_f32(in.ws[DIAG ? 0 : j]) : 0.f;
-                rt[j] = s_r[t];
-                ut[j] = nk[j] * s_mr[t] * (1.f / (float)DK);
-            }
-            {
-                float mm[4] = {1.f, 0.f, 0.f, 1.f};
-                float g0 = 1.f, g1 = 1.f;
-#pragma unroll
-                for (int j = 0; j < SL; ++j) {
-                    mob_left(mm, aa[j], wt[j], ut[j]);
-                    g0 *= ga[0][j];
-                    g1 *= ga[1][j];
-                    if ((j & 3) == 3 || j == SL - 1) rescale4(mm);
-                }
-                if (lane == 0) segA[wave * DK] = make_float4(mm[0], mm[1], mm[2], mm[3]);
-                if (vact) *reinterpret_cast<float2*>(segG + wave * DK + ch) = make_float2(g0, g1);
-            }
-            __syncthreads();
-            segment_carries<CF>(segA, segG, carry + par * DK, zs, gs, wave, lane);
-            __syncthreads();
-            {
-                const float2 z = zs[wave * DK + ch];
-                float g0 = gs[wave * DK + ch], g1 = gs[wave * DK + ch + 1];
-                float nz = z.x, dz = z.y;
-                float pb0[SL], pb1[SL];
-#pragma unroll
-                for (int j = 0; j < SL; ++j) {
-                    const int t = SL * wave + j;
-                    g0 *= ga[0][j];
-                    g1 *= ga[1][j];
-                    const float nn = fmaf(aa[j], nz, wt[j] * dz);    // b_hat = nn / dz
-                    const float beta = nn / fmaf(dz, rt[j], nn * nk[j]);
-                    pb0[j] = beta * kv[0][j] * __builtin_amdgcn_rcpf(g0);
-                    pb1[j] = beta * kv[1][j] * __builtin_amdgcn_rcpf(g1);
-                    dz = fmaf(ut[j], nn, dz);
-                    nz = nn;
-                    if ((j & 3) == 3 || j == SL - 1) rescale2(nz, dz);
                     if (vact) {
-                        st2<MT>(Kb + t * LDK + ch, g0 * kv[0][j], g1 * kv[1][j]);
-                        st2<MT>(Qb + t * LDK + ch, a.scale * g0 * qv[0][j],
-                                a.scale * g1 * qv[1][j]);
+                        st2<MT>(Kb + t * LDK + ch, g0 * K.x, g1 * K.y);
+                        st2<MT>(Qb + t * LDK + ch, a.scale * g0 * Q.x, a.scale * g1 * Q.y);
                         st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
                     }
                 }
-                if (vact) {
-                    storeN<MT, SL>(PbT + ch * LDC + SL * wave, pb0);
-                    storeN<MT, SL>(PbT + (ch + 1) * LDC + SL * wave, pb1);
-                }
-                if (wave == NW - 1) {
-                    rescale2(nz, dz);
-                    if (lane == 0) {
-                        carry[(par ^ 1) * DK] = make_float2(nz, dz);
-                        if (last && a.P_T && vt == 0) a.P_T[nh] = nz / dz;
-                    }
-                    if (vact) *reinterpret_cast<float2*>(gC + ch) = make_float2(g0, g1);
-                }
-            }
-        }
-        __syncthreads();
+            };
+            // tokens [JA, JB) of the segment; the masked form only in a partial last chunk
+            auto replay = [&](auto ja_c, auto jb_c) {
+                if (Lw < SL) replay_mk(ja_c, jb_c, std::true_type());
+                else replay_mk(ja_c, jb_c, std::false_type());
+            };
+            using J0 = std::integral_constant<int, 0>;
+            using J1 = std::integral_constant<int, CF::JT1>;
+            using J2 = std::integral_constant<int, CF::JT2>;
+            using J3 = std::integral_constant<int, SL>;
 
-        // ==== 3. L = diag(c) + tril(K_bar P_bar^T, -1) and A_qk = tril(Q_bar P_bar^T) =====
-        for (int u = wave; u < CF::NLU; u += NW) {
-            int ib = 0, jb = u;  // enumerate (ib >= jb) in row order
-            while (jb > ib) { jb -= ib + 1; ++ib; }
-            floatx4 tacc = zero4(), qacc = zero4();
-            mm_kc2<MT, DK>(Kb + 16 * ib * LDK, Qb + 16 * ib * LDK, LDK, Pb + 16 * jb * LDK, LDK,
-                           tacc, qacc, lane);
+            // ---- phase B: the carry into the segment, the first third of the replay --------
+            if (vwork) {
+                // the chunk carry through the earlier segments' summaries
+                // (eq. chunk-gain-local-prefix)
+                if constexpr (DIAG) {
+                    float2 z0 = carry[pv * DK + ch], z1 = carry[pv * DK + ch + 1];
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const int row = 4 * lg + rr, R = 16 * ib + row, Cc = 16 * jb + li;
-                if (ib > jb) {
-                    Lm[R * LDT + Cc] = tacc[rr];
-                    Aq[R * LDC + Cc] = from_f32<MT>(qacc[rr]);
+                    for (int ps = 0; ps < NVW - 1; ++ps) {
+                        if (ps < vw) {
+                            z0 = mat_vec(segA[ps * DK + ch], z0);
+                            z1 = mat_vec(segA[ps * DK + ch + 1], z1);
+                            const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
+                            g0 *= gg.x;
+                            g1 *= gg.y;
+                        }
+                    }
+                    n0 = z0.x; d0 = z0.y; n1 = z1.x; d1 = z1.y;
                 } else {
-                    const float cdiag = DIAG ? s_r[R] + tacc[rr] : 1.f;
-                    Lm[R * LDT + Cc] = row > li ? tacc[rr] : (row == li ? cdiag : 0.f);
-                    Aq[R * LDC + Cc] = from_f32<MT>(row >= li ? qacc[rr] : 0.f);
+                    float2 z = carry[pv * DK];
+#pragma unroll
+                    for (int ps = 0; ps < NVW - 1; ++ps) {
+                        if (ps < vw) {
+                            z = mat_vec(segA[ps * DK], z);
+                            const float2 gg = *reinterpret_cast<const float2*>(segG + ps * DK + ch);
+                            g0 *= gg.x;
+                            g1 *= gg.y;
+                        }
+                    }
+                    n0 = z.x; d0 = z.y;
                 }
+                replay(J0(), J1());
+                load_part<0, CF::JT1, TI, CF>(in, sr, c0n, vw);
             }
-        }
-        // zero the blocks above the diagonal of A_qk (16-byte stores)
-        {
-            constexpr int VPB = 16 * (int)sizeof(MT) / 16;  // 16-byte vectors per block row
-            constexpr int NUP = NB * (NB - 1) / 2;
-            if constexpr (NUP > 0)
-                for (int idx = tid; idx < NUP * 16 * VPB; idx += NTH) {
-                    const int rem = idx;
-                    int blk = rem / (16 * VPB);
-                    const int row16 = (rem / VPB) % 16, vec = rem % VPB;
-                    int ib = 0;  // blk -> (ib < jb)
-                    while (blk >= NB - 1 - ib) { blk -= NB - 1 - ib; ++ib; }
-                    const int jb = ib + 1 + blk;
-                    *reinterpret_cast<uint4*>(Aq + (16 * ib + row16) * LDC + 16 * jb +
-                                              vec * (16 / (int)sizeof(MT))) =
-                        make_uint4(0, 0, 0, 0);
-                }
-        }
-        __syncthreads();
+            __syncthreads();
 
-        // ==== 3'. diagonal blocks of L^-1, one row per lane (lane = block, row i) ==========
-        // Row i of A_bb = L_bb^-1 solves a^T L_bb = e_i^T: a_i = 1 / L_ii, and going down the
-        // rows m = i, i-1, ..., 0 every finished a_m adds a_m L_m,k to the sums of the k < m
-        // (right-looking backward substitution, two dependent operations per row; the next
-        // row of L is read while the current one is used). The last wave does this while the
-        // others issue their loads of the next chunk.
-        if (wave == NW - 1 && (lane >> 4) < NB) {
-            const int b = lane >> 4, i = li;
-            const float* Lb = Lm + (16 * b) * LDT + 16 * b;
-            float s[16], y[16], row[2][16];
-#pragma unroll
-            for (int kq = 0; kq < 16; ++kq) s[kq] = 0.f;
-#pragma unroll
-            for (int v4 = 0; v4 < 4; ++v4) {
-                const float4 q4 = *reinterpret_cast<const float4*>(Lb + 15 * LDT + 4 * v4);
-                row[1][4 * v4] = q4.x; row[1][4 * v4 + 1] = q4.y;
-                row[1][4 * v4 + 2] = q4.z; row[1][4 * v4 + 3] = q4.w;
+            // ---- phase C: the second third ---------------------------------------------------
+            if (vwork) {
+                replay(J1(), J2());
+                load_part<CF::JT1, CF::JT2, TI, CF>(in, sr, c0n, vw);
             }
-#pragma unroll
-            for (int mq = 15; mq >= 0; --mq) {
-                float* cur = row[mq & 1];
-                if (mq > 0) {
-                    float* nx = row[(mq - 1) & 1];
-#pragma unroll
-                    for (int v4 = 0; v4 < (mq + 3) / 4; ++v4) {
-                        const float4 q4 =
-                            *reinterpret_cast<const float4*>(Lb + (mq - 1) * LDT + 4 * v4);
-                        nx[4 * v4] = q4.x; nx[4 * v4 + 1] = q4.y;
-                        nx[4 * v4 + 2] = q4.z; nx[4 * v4 + 3] = q4.w;
+            __syncthreads();
+
+            // ---- phase D: the last third; P_bar^T; the chunk's carry and decay --------------
+            if (vwork) {
+                replay(J2(), J3());
+                if (vact) {
+                    storeN<MT, (SL < 8 ? SL : 8)>(PbTv + ch * LDC + SL * vw, pb0);
+                    storeN<MT, (SL < 8 ? SL : 8)>(PbTv + (ch + 1) * LDC + SL * vw, pb1);
+                    if constexpr (SL > 8) {
+                        storeN<MT, 8>(PbTv + ch * LDC + SL * vw + 8, pb0 + 8);
+                        storeN<MT, 8>(PbTv + (ch + 1) * LDC + SL * vw + 8, pb1 + 8);
                     }
                 }
-                const float ym = ((mq == i ? 1.f : 0.f) - s[mq]) * __builtin_amdgcn_rcpf(cur[mq]);
-                y[mq] = mq > i ? 0.f : ym;
-#pragma unroll
-                for (int kq = 0; kq < mq; ++kq) s[kq] = fmaf(y[mq], cur[kq], s[kq]);
-            }
-            store8<MT>(Ai + (16 * b + i) * LDC + 16 * b, y);
-            store8<MT>(Ai + (16 * b + i) * LDC + 16 * b + 8, y + 8);
-        } else if (wave != NW - 1) {
-            load_main<0, TI, CF>(in, sr, c0n, wave, tid);
-            load_main<1, TI, CF>(in, sr, c0n, wave, tid);
-        }
-        __syncthreads();
-
-        // ==== 4. state: X = V - K_bar S and Q_bar S ======================================
-#pragma unroll
-        for (int j = 0; j < CF::XPW; ++j) {
-            const int x = wave + NW * j;
-            Oacc[j] = zero4();
-            if (x < CF::NXT) {
-                const int mt = x % NB, nt = x / NB;
-                floatx4 xacc = zero4();
-#pragma unroll
-                for (int s = 0; s < FK::NS; ++s) {
-                    const int k0 = FK::KF * s + (FK::KF / 4) * lg;
-                    const typename FK::V b = FK::ld(SmT + (16 * nt + li) * LDK + k0);
-                    xacc = FK::mma(xacc, FK::ld(Kb + (16 * mt + li) * LDK + k0), b);
-                    Oacc[j] = FK::mma(Oacc[j], FK::ld(Qb + (16 * mt + li) * LDK + k0), b);
+                if (vw == NVW - 1) {  // the last segment closes the chunk
+                    rescale2(n0, d0);
+                    if constexpr (DIAG) {
+                        rescale2(n1, d1);
+                        if (vact) {
+                            carry[(pv ^ 1) * DK + ch] = make_float2(n0, d0);
+                            carry[(pv ^ 1) * DK + ch + 1] = make_float2(n1, d1);
+                            if (vlast && a.P_T && vt == 0)  // the final variances n / d
+                                *reinterpret_cast<float2*>(a.P_T + (size_t)nh * DK + ch) =
+                                    make_float2(n0 / d0, n1 / d1);
+                        }
+                    } else if (lane == 0) {
+                        carry[(pv ^ 1) * DK] = make_float2(n0, d0);
+                        if (vlast && a.P_T && vt == 0) a.P_T[nh] = n0 / d0;
+                    }
+                    if (vact) *reinterpret_cast<float2*>(gC + pv * DK + ch) = make_float2(g0, g1);
                 }
-                float xv[4];
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int t = 16 * mt + 4 * lg + rr;
-                    xv[rr] = (t < L ? to_f32(in.vv[j][rr]) : 0.f) - xacc[rr];
-                }
-                store4<MT>(XT + (16 * nt + li) * LDC + 16 * mt + 4 * lg, xv[0], xv[1], xv[2],
-                           xv[3]);
-            }
-        }
-        __syncthreads();
-        load_v<TI, CF>(in, sr, c0n, wave, lane);
-
-        // R = L^-1 X by block forward substitution, one wave per 16-column tile of the value
-        // block: R_b = A_bb (X_b - sum_{c<b} L_bc R_c), with A_bb the diagonal block inverses.
-        // The chain stays in registers (a result tile is the B fragment of the next product);
-        // R^T goes to LDS for the output and state products. The last wave issues its loads of
-        // the next chunk meanwhile.
-        if (wave < CF::NNT) {
-            using G = F16<MT>;
-            const int nt = wave;
-            typename G::V ad[NB], lo[NB > 1 ? NB * (NB - 1) / 2 : 1];
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                ad[b] = G::ld(Ai + (16 * b + li) * LDC + 16 * b + 4 * lg);
-#pragma unroll
-                for (int c = 0; c < b; ++c) {
-                    const float4 l4 =
-                        *reinterpret_cast<const float4*>(Lm + (16 * b + li) * LDT + 16 * c + 4 * lg);
-                    lo[b * (b - 1) / 2 + c] = G::pack(l4.x, l4.y, l4.z, l4.w);
+                load_part<CF::JT2, SL, TI, CF>(in, sr, c0n, vw);
+                if (!vlast) {
+                    if (tid < C) {  // r and mu / r of the next chunk
+                        const float rv = Raw1<TI>::f32(in.rr);
+                        const bool ok = tid < t1 - (int)c0n;
+                        s_r[(pv ^ 1) * C + tid] = ok ? rv : 1.f;
+                        s_mr[(pv ^ 1) * C + tid] = ok ? a.mu / rv : 0.f;
+                    }
                 }
             }
-            floatx4 Rr[NB];
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                floatx4 acc = zero4();
-#pragma unroll
-                for (int c = 0; c < b; ++c)
-                    acc = G::mma(acc, lo[b * (b - 1) / 2 + c],
-                                 G::pack(Rr[c][0], Rr[c][1], Rr[c][2], Rr[c][3]));
-                const float4 xb = ld4f<MT>(XT + (16 * nt + li) * LDC + 16 * b + 4 * lg);
-                Rr[b] = G::mma(zero4(), ad[b],
-                               G::pack(xb.x - acc[0], xb.y - acc[1], xb.z - acc[2], xb.w - acc[3]));
-                store4<MT>(RT + (16 * nt + li) * LDC + 16 * b + 4 * lg, Rr[b][0], Rr[b][1],
-                           Rr[b][2], Rr[b][3]);
-            }
-        } else if (wave == NW - 1) {
-            load_main<0, TI, CF>(in, sr, c0n, wave, tid);
-            load_main<1, TI, CF>(in, sr, c0n, wave, tid);
+            __syncthreads();
         }
-        __syncthreads();
+    } else {
+        // ===== matrix waves: chunk it - 1; wave mw owns row blocks mw, mw + 4, ... ===========
+        for (int it = 0; it <= nch; ++it) {
+            const int m = it - 1;
+            const bool mwork = m >= 0;
+            const int pm = m & 1;
+            const int c0m = t0 + m * C, Lm = min(C, t1 - c0m);
+            const float* s_rm = s_r + pm * C;
+            MT* PbTm = PbT0 + (size_t)pm * DK * LDC;
 
-        // O = Q_bar S + A_qk R (staged for 16-byte stores); S <- gamma_C (.) (S + P_bar^T R)
-#pragma unroll
-        for (int j = 0; j < CF::XPW; ++j) {
-            const int x = wave + NW * j;
-            if (x < CF::NXT) {
-                const int mt = x % NB, nt = x / NB;
-#pragma unroll
-                for (int s = 0; s < FC::NS; ++s) {
-                    if (FC::KF * s < 16 * (mt + 1)) {
-                        const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-                        Oacc[j] = FC::mma(Oacc[j], FC::ld(Aq + (16 * mt + li) * LDC + k0),
-                                          FC::ld(RT + (16 * nt + li) * LDC + k0));
+            // ---- phase A: the previous chunk's O rows; per owned row block: L and A_qk, and
+            // X = V - K_bar S (to LDS, transposed) with Q_bar S kept for the output -----------
+            if (mwork) {
+                if (m >= 1) {  // a full chunk: only the last one can be partial
+                    constexpr int VE = 16 / (int)sizeof(TI), VPR = BV / VE;
+                    const int c0p = c0m - C;
+#pragma unroll 1
+                    for (int idx = mtid; idx < C * VPR; idx += 64 * NMW) {
+                        const int t = idx / VPR, e = (idx % VPR) * VE;
+                        *reinterpret_cast<uint4*>(go + ((size_t)(c0p + t) * H + h) * DV + col0 +
+                                                  e) =
+                            *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
                     }
                 }
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    Ost[(16 * mt + 4 * lg + rr) * LDO + 16 * nt + li] = from_f32<TI>(Oacc[j][rr]);
-            }
-        }
+                for (int rw = 0; rw < CF::RPW; ++rw) {
+                    const int ib = mw + NMW * rw;
+                    if (ib < NB) {
+                        typename FK::V kf[FK::NS], qf[FK::NS];
 #pragma unroll
-        for (int j = 0; j < CF::SPW; ++j) {
-            const int x = wave + NW * j;
-            if (x < CF::NST) {
-                const int it = x % CF::NKT, nt = x / CF::NKT;
+                        for (int s = 0; s < FK::NS; ++s) {
+                            const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                            kf[s] = FK::ld(Kb + (16 * ib + li) * LDK + k0);
+                            qf[s] = FK::ld(Qb + (16 * ib + li) * LDK + k0);
+                        }
+                        for (int jb = 0; jb <= ib; ++jb) {
+                            floatx4 tacc = zero4(), qacc = zero4();
 #pragma unroll
-                for (int s = 0; s < FC::NS; ++s) {
-                    const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-                    Sacc[j] = FC::mma(Sacc[j], FC::ld(PbT + (16 * it + li) * LDC + k0),
-                                      FC::ld(RT + (16 * nt + li) * LDC + k0));
+                            for (int s = 0; s < FK::NS; ++s) {
+                                const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                                const typename FK::V pf = FK::ld(Pb + (16 * jb + li) * LDK + k0);
+                                tacc = FK::mma(tacc, kf[s], pf);
+                                qacc = FK::mma(qacc, qf[s], pf);
+                            }
+                            if (ib > jb) {
+                                MT* lo = Lo + (ib * (ib - 1) / 2 + jb) * 16 * LDE;
+#pragma unroll
+                                for (int rr = 0; rr < 4; ++rr) {
+                                    const int row = 4 * lg + rr;
+                                    lo[row * LDE + li] = from_f32<MT>(tacc[rr]);
+                                    Aq[(16 * ib + row) * LDC + 16 * jb + li] =
+                                        from_f32<MT>(qacc[rr]);
+                                }
+                            } else {
+                                float* ld = Ld + ib * 16 * LDD;
+#pragma unroll
+                                for (int rr = 0; rr < 4; ++rr) {
+                                    const int row = 4 * lg + rr;
+                                    const float cdiag =
+                                        DIAG ? s_rm[16 * ib + row] + tacc[rr] : 1.f;
+                                    ld[row * LDD + li] =
+                                        row > li ? tacc[rr] : (row == li ? cdiag : 0.f);
+                                    Aq[(16 * ib + row) * LDC + 16 * jb + li] =
+                                        from_f32<MT>(row >= li ? qacc[rr] : 0.f);
+                                }
+                            }
+                        }
+                        // the blocks of A_qk right of the diagonal are zero (16-byte stores)
+                        {
+                            constexpr int VPB = 16 * (int)sizeof(MT) / 16;
+                            for (int idx = lane; idx < (NB - 1 - ib) * 16 * VPB; idx += 64) {
+                                const int jb = ib + 1 + idx / (16 * VPB);
+                                const int row16 = (idx / VPB) % 16, vec = idx % VPB;
+                                *reinterpret_cast<uint4*>(Aq + (16 * ib + row16) * LDC + 16 * jb +
+                                                          vec * (16 / (int)sizeof(MT))) =
+                                    make_uint4(0, 0, 0, 0);
+                            }
+                        }
+#pragma unroll
+                        for (int nt = 0; nt < CF::NNT; ++nt) {
+                            const int j = rw * CF::NNT + nt;
+                            floatx4 xacc = zero4();
+                            Oacc[j] = zero4();
+#pragma unroll
+                            for (int s = 0; s < FK::NS; ++s) {
+                                const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                                const typename FK::V b = FK::ld(SmT + (16 * nt + li) * LDK + k0);
+                                xacc = FK::mma(xacc, kf[s], b);
+                                Oacc[j] = FK::mma(Oacc[j], qf[s], b);
+                            }
+                            float xv[4];
+#pragma unroll
+                            for (int rr = 0; rr < 4; ++rr) {
+                                const int t = 16 * ib + 4 * lg + rr;
+                                xv[rr] = (t < Lm ? Raw1<TI>::f32(vv[j][rr]) : 0.f) - xacc[rr];
+                            }
+                            store4<MT>(XT + (16 * nt + li) * LDC + 16 * ib + 4 * lg, xv[0],
+                                       xv[1], xv[2], xv[3]);
+                        }
+                    }
                 }
-                const float4 gc = *reinterpret_cast<const float4*>(gC + 16 * it + 4 * lg);
-                Sacc[j][0] *= gc.x;
-                Sacc[j][1] *= gc.y;
-                Sacc[j][2] *= gc.z;
-                Sacc[j][3] *= gc.w;
-                store4<MT>(SmT + (16 * nt + li) * LDK + 16 * it + 4 * lg, Sacc[j][0], Sacc[j][1],
-                           Sacc[j][2], Sacc[j][3]);
+                load_v<TI, CF>(vv, sr, (uint32_t)(c0m + C), mw, lane);  // unused past the end
             }
-        }
-        // r of the next chunk (every reader of this chunk's r is past the barrier above)
-        if (tid < C) {
-            const float rv = to_f32(in.rr);
-            s_r[tid] = tid < Ln ? rv : 1.f;
-            s_mr[tid] = tid < Ln ? a.mu / rv : 0.f;
-        }
-        __syncthreads();
+            __syncthreads();
 
-        // this chunk's O rows, 16-byte stores (rows past the end are not written)
-        {
+            // ---- phase B: the diagonal blocks of L^-1 -----------------------------------------
+            // Row i of A_bb = L_bb^-1 solves a^T L_bb = e_i^T: a_i = 1 / L_ii, and going down
+            // the rows m = i, i-1, ..., 0 every finished a_m adds a_m L_m,k to the sums of the
+            // k < m (right-looking backward substitution; the next row of L is read while the
+            // current one is used). Lane (b, i) takes row i of block b.
+            if (mwork && mw == 0 && (lane >> 4) < NB) {
+                const int b = lane >> 4, i = li;
+                const float* Lb = Ld + b * 16 * LDD;
+                float sacc[16], y[16], row[2][16];
+#pragma unroll
+                for (int kq = 0; kq < 16; ++kq) sacc[kq] = 0.f;
+#pragma unroll
+                for (int v4 = 0; v4 < 4; ++v4) {
+                    const float4 q4 = *reinterpret_cast<const float4*>(Lb + 15 * LDD + 4 * v4);
+                    row[1][4 * v4] = q4.x; row[1][4 * v4 + 1] = q4.y;
+                    row[1][4 * v4 + 2] = q4.z; row[1][4 * v4 + 3] = q4.w;
+                }
+#pragma unroll
+                for (int mq = 15; mq >= 0; --mq) {
+                    float* cur = row[mq & 1];
+                    if (mq > 0) {
+                        float* nx = row[(mq - 1) & 1];
+#pragma unroll
+                        for (int v4 = 0; v4 < (mq + 3) / 4; ++v4) {
+                            const float4 q4 =
+                                *reinterpret_cast<const float4*>(Lb + (mq - 1) * LDD + 4 * v4);
+                            nx[4 * v4] = q4.x; nx[4 * v4 + 1] = q4.y;
+                            nx[4 * v4 + 2] = q4.z; nx[4 * v4 + 3] = q4.w;
+                        }
+                    }
+                    const float ym =
+                        ((mq == i ? 1.f : 0.f) - sacc[mq]) * __builtin_amdgcn_rcpf(cur[mq]);
+                    y[mq] = mq > i ? 0.f : ym;
+#pragma unroll
+                    for (int kq = 0; kq < mq; ++kq) sacc[kq] = fmaf(y[mq], cur[kq], sacc[kq]);
+                }
+                store8<MT>(Ai + (b * 16 + i) * LDE, y);
+                store8<MT>(Ai + (b * 16 + i) * LDE + 8, y + 8);
+            }
+            __syncthreads();
+
+            // ---- phase C: R = L^-1 X by block forward substitution ------------------------
+            // One wave per 16-column tile of the value block: R_b = A_bb (X_b - sum_{c<b} L_bc
+            // R_c). The chain stays in registers (a result tile is the B fragment of the next
+            // product); R^T goes to LDS.
+            if (mwork && mw < CF::NNT) {
+                const int nt = mw;
+                typename G::V ad[NB], lo[CF::NOFF];
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    ad[b] = G::ld(Ai + (b * 16 + li) * LDE + 4 * lg);
+#pragma unroll
+                    for (int c = 0; c < b; ++c) {
+                        const int idx = b * (b - 1) / 2 + c;
+                        lo[idx] = G::ld(Lo + (idx * 16 + li) * LDE + 4 * lg);
+                    }
+                }
+                floatx4 Rr[NB];
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    floatx4 acc = zero4();
+#pragma unroll
+                    for (int c = 0; c < b; ++c)
+                        acc = G::mma(acc, lo[b * (b - 1) / 2 + c],
+                                     G::pack(Rr[c][0], Rr[c][1], Rr[c][2], Rr[c][3]));
+                    const float4 xb = ld4f<MT>(XT + (16 * nt + li) * LDC + 16 * b + 4 * lg);
+                    Rr[b] = G::mma(zero4(), ad[b],
+                                   G::pack(xb.x - acc[0], xb.y - acc[1], xb.z - acc[2],
+                                           xb.w - acc[3]));
+                    store4<MT>(RT + (16 * nt + li) * LDC + 16 * b + 4 * lg, Rr[b][0], Rr[b][1],
+                               Rr[b][2], Rr[b][3]);
+                }
+            }
+            __syncthreads();
+
+            // ---- phase D: O = Q_bar S + A_qk R (staged for the next iteration's stores) and
+            // S <- gamma_C (.) (S + P_bar^T R) ------------------------------------------------
+            if (mwork) {
+#pragma unroll
+                for (int j = 0; j < CF::XPW; ++j) {
+                    const int ib = mw + NMW * (j / CF::NNT), nt = j % CF::NNT;
+                    if (ib < NB) {
+#pragma unroll
+                        for (int s = 0; s < FC::NS; ++s) {
+                            if (FC::KF * s < 16 * (ib + 1)) {
+                                const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+                                Oacc[j] = FC::mma(Oacc[j], FC::ld(Aq + (16 * ib + li) * LDC + k0),
+                                                  FC::ld(RT + (16 * nt + li) * LDC + k0));
+                            }
+                        }
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr)
+                            Ost[(16 * ib + 4 * lg + rr) * LDO + 16 * nt + li] =
+                                from_f32<TI>(Oacc[j][rr]);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < CF::SPW; ++j) {
+                    const int x = mw + NMW * j;
+                    if (x < CF::NST) {
+                        const int ik = x % CF::NKT, nt = x / CF::NKT;
+#pragma unroll
+                        for (int s = 0; s < FC::NS; ++s) {
+                            const int k0 = FC::KF * s + (FC::KF / 4) * lg;
+                            Sacc[j] = FC::mma(Sacc[j], FC::ld(PbTm + (16 * ik + li) * LDC + k0),
+                                              FC::ld(RT + (16 * nt + li) * LDC + k0));
+                        }
+                        const float4 gc =
+                            *reinterpret_cast<const float4*>(gC + pm * DK + 16 * ik + 4 * lg);
+                        Sacc[j][0] *= gc.x;
+                        Sacc[j][1] *= gc.y;
+                        Sacc[j][2] *= gc.z;
+                        Sacc[j][3] *= gc.w;
+                        store4<MT>(SmT + (16 * nt + li) * LDK + 16 * ik + 4 * lg, Sacc[j][0],
+                                   Sacc[j][1], Sacc[j][2], Sacc[j][3]);
+                    }
+                }
+            }
+            __syncthreads();
+        }
+
+        if (nch > 0) {  // the last chunk's O rows
             constexpr int VE = 16 / (int)sizeof(TI), VPR = BV / VE;
-            for (int idx = tid; idx < C * VPR; idx += NTH) {
+            const int c0p = t0 + (nch - 1) * C, Lp = t1 - c0p;
+#pragma unroll 1
+            for (int idx = mtid; idx < C * VPR; idx += 64 * NMW) {
                 const int t = idx / VPR, e = (idx % VPR) * VE;
-                if (t < L)
-                    *reinterpret_cast<uint4*>(go + ((size_t)(c0 + t) * H + h) * DV + col0 + e) =
+                if (t < Lp)
+                    *reinterpret_cast<uint4*>(go + ((size_t)(c0p + t) * H + h) * DV + col0 + e) =
                         *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
             }
         }
-    }
-
-    if (a.S_T) {
-        float* dst = a.S_T + (size_t)nh * DK * DV;
+        if (a.S_T) {
+            float* dst = a.S_T + (size_t)nh * DK * DV;
 #pragma unroll
-        for (int j = 0; j < CF::SPW; ++j) {
-            const int x = wave + NW * j;
-            if (x < CF::NST) {
-                const int it = x % CF::NKT, nt = x / CF::NKT;
+            for (int j = 0; j < CF::SPW; ++j) {
+                const int x = mw + NMW * j;
+                if (x < CF::NST) {
+                    const int ik = x % CF::NKT, nt = x / CF::NKT;
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr)
-                    dst[(size_t)(16 * it + 4 * lg + rr) * DV + col0 + 16 * nt + li] = Sacc[j][rr];
+                    for (int rr = 0; rr < 4; ++rr)
+                        dst[(size_t)(16 * ik + 4 * lg + rr) * DV + col0 + 16 * nt + li] =
+                            Sacc[j][rr];
+                }
             }
         }
     }
