@@ -520,6 +520,11 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             }
         }
     }
+    if (!vgrp) {  // the blocks of A_qk right of the diagonal stay zero
+        constexpr int NVEC = C * LDC * (int)sizeof(MT) / 16;
+        for (int idx = mtid; idx < NVEC; idx += 64 * NMW)
+            reinterpret_cast<uint4*>(Aq)[idx] = make_uint4(0, 0, 0, 0);
+    }
     if (DIAG ? tid < DK : tid == 0)
         carry[tid] = make_float2(a.P0 ? a.P0[(size_t)nh * (DIAG ? DK : 1) + tid] : 1.f, 1.f);
     if (nch == 0 && a.P_T && vt == 0 && (DIAG ? tid < DK : tid == 0))  // empty sequence
@@ -766,16 +771,51 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             // ---- phase A: the previous chunk's O rows; per owned row block: L and A_qk, and
             // X = V - K_bar S (to LDS, transposed) with Q_bar S kept for the output -----------
             if (mwork) {
-                if (m >= 1) {  // a full chunk: only the last one can be partial
-                    constexpr int VE = 16 / (int)sizeof(TI), VPR = BV / VE;
-                    const int c0p = c0m - C;
-#pragma unroll 1
-                    for (int idx = mtid; idx < C * VPR; idx += 64 * NMW) {
-                        const int t = idx / VPR, e = (idx % VPR) * VE;
-                        *reinterpret_cast<uint4*>(go + ((size_t)(c0p + t) * H + h) * DV + col0 +
-                                                  e) =
-                            *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
+                // one block pair (ib, jb) of L and A_qk from the row block's K_bar and Q_bar
+                // fragments
+                auto lq_unit = [&](int ib, int jb, const typename FK::V* kf,
+                                   const typename FK::V* qf) {
+                    floatx4 tacc = zero4(), qacc = zero4();
+#pragma unroll
+                    for (int s = 0; s < FK::NS; ++s) {
+                        const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                        const typename FK::V pf = FK::ld(Pb + (16 * jb + li) * LDK + k0);
+                        tacc = FK::mma(tacc, kf[s], pf);
+                        qacc = FK::mma(qacc, qf[s], pf);
                     }
+                    if (ib > jb) {
+                        MT* lo = Lo + (ib * (ib - 1) / 2 + jb) * 16 * LDE;
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            const int row = 4 * lg + rr;
+                            lo[row * LDE + li] = from_f32<MT>(tacc[rr]);
+                            Aq[(16 * ib + row) * LDC + 16 * jb + li] = from_f32<MT>(qacc[rr]);
+                        }
+                    } else {
+                        float* ld = Ld + ib * 16 * LDD;
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) {
+                            const int row = 4 * lg + rr;
+                            const float cdiag = DIAG ? s_rm[16 * ib + row] + tacc[rr] : 1.f;
+                            ld[row * LDD + li] = row > li ? tacc[rr] : (row == li ? cdiag : 0.f);
+                            Aq[(16 * ib + row) * LDC + 16 * jb + li] =
+                                from_f32<MT>(row >= li ? qacc[rr] : 0.f);
+                        }
+                    }
+                };
+                // with four row blocks, wave 0 also takes the first two pairs of row block 3,
+                // so no wave has more than three
+                constexpr bool SHIFT = NB == 4 && NMW == 4;
+                if (SHIFT && mw == 0) {
+                    typename FK::V kf[FK::NS], qf[FK::NS];
+#pragma unroll
+                    for (int s = 0; s < FK::NS; ++s) {
+                        const int k0 = FK::KF * s + (FK::KF / 4) * lg;
+                        kf[s] = FK::ld(Kb + (16 * 3 + li) * LDK + k0);
+                        qf[s] = FK::ld(Qb + (16 * 3 + li) * LDK + k0);
+                    }
+                    lq_unit(3, 0, kf, qf);
+                    lq_unit(3, 1, kf, qf);
                 }
 #pragma unroll
                 for (int rw = 0; rw < CF::RPW; ++rw) {
@@ -788,49 +828,8 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                             kf[s] = FK::ld(Kb + (16 * ib + li) * LDK + k0);
                             qf[s] = FK::ld(Qb + (16 * ib + li) * LDK + k0);
                         }
-                        for (int jb = 0; jb <= ib; ++jb) {
-                            floatx4 tacc = zero4(), qacc = zero4();
-#pragma unroll
-                            for (int s = 0; s < FK::NS; ++s) {
-                                const int k0 = FK::KF * s + (FK::KF / 4) * lg;
-                                const typename FK::V pf = FK::ld(Pb + (16 * jb + li) * LDK + k0);
-                                tacc = FK::mma(tacc, kf[s], pf);
-                                qacc = FK::mma(qacc, qf[s], pf);
-                            }
-                            if (ib > jb) {
-                                MT* lo = Lo + (ib * (ib - 1) / 2 + jb) * 16 * LDE;
-#pragma unroll
-                                for (int rr = 0; rr < 4; ++rr) {
-                                    const int row = 4 * lg + rr;
-                                    lo[row * LDE + li] = from_f32<MT>(tacc[rr]);
-                                    Aq[(16 * ib + row) * LDC + 16 * jb + li] =
-                                        from_f32<MT>(qacc[rr]);
-                                }
-                            } else {
-                                float* ld = Ld + ib * 16 * LDD;
-#pragma unroll
-                                for (int rr = 0; rr < 4; ++rr) {
-                                    const int row = 4 * lg + rr;
-                                    const float cdiag =
-                                        DIAG ? s_rm[16 * ib + row] + tacc[rr] : 1.f;
-                                    ld[row * LDD + li] =
-                                        row > li ? tacc[rr] : (row == li ? cdiag : 0.f);
-                                    Aq[(16 * ib + row) * LDC + 16 * jb + li] =
-                                        from_f32<MT>(row >= li ? qacc[rr] : 0.f);
-                                }
-                            }
-                        }
-                        // the blocks of A_qk right of the diagonal are zero (16-byte stores)
-                        {
-                            constexpr int VPB = 16 * (int)sizeof(MT) / 16;
-                            for (int idx = lane; idx < (NB - 1 - ib) * 16 * VPB; idx += 64) {
-                                const int jb = ib + 1 + idx / (16 * VPB);
-                                const int row16 = (idx / VPB) % 16, vec = idx % VPB;
-                                *reinterpret_cast<uint4*>(Aq + (16 * ib + row16) * LDC + 16 * jb +
-                                                          vec * (16 / (int)sizeof(MT))) =
-                                    make_uint4(0, 0, 0, 0);
-                            }
-                        }
+                        for (int jb = SHIFT && ib == 3 ? 2 : 0; jb <= ib; ++jb)
+                            lq_unit(ib, jb, kf, qf);
 #pragma unroll
                         for (int nt = 0; nt < CF::NNT; ++nt) {
                             const int j = rw * CF::NNT + nt;
@@ -858,7 +857,18 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             }
             __syncthreads();
 
-            // ---- phase B: the diagonal blocks of L^-1 -----------------------------------------
+            // ---- phase B: the diagonal blocks of L^-1 (wave 0); the previous chunk's O rows
+            // (the other matrix waves) ------------------------------------------------------
+            if (mwork && mw >= 1 && m >= 1) {  // a full chunk: only the last one can be partial
+                constexpr int VE = 16 / (int)sizeof(TI), VPR = BV / VE;
+                const int c0p = c0m - C;
+#pragma unroll 1
+                for (int idx = mtid - 64; idx < C * VPR; idx += 64 * (NMW - 1)) {
+                    const int t = idx / VPR, e = (idx % VPR) * VE;
+                    *reinterpret_cast<uint4*>(go + ((size_t)(c0p + t) * H + h) * DV + col0 + e) =
+                        *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
+                }
+            }
             // Row i of A_bb = L_bb^-1 solves a^T L_bb = e_i^T: a_i = 1 / L_ii, and going down
             // the rows m = i, i-1, ..., 0 every finished a_m adds a_m L_m,k to the sums of the
             // k < m (right-looking backward substitution; the next row of L is read while the
