@@ -4,11 +4,11 @@
         --trace DIR --fetch DIR --write DIR --copy-fetch DIR --copy-write DIR \\
         --copy-bytes N --algorithmic-bytes N --commands FILE
 
-One forward is several kernels (chunk summaries, carry scan, prep passes, state passes; the
-state passes run on a second stream). The kernel trace is cut into forwards at every dispatch
-whose name contains SUBSTR (the forward's first kernel); a forward's span runs from its first
-dispatch's start to the last end before the next forward. The per-kernel duration statistics
-come from the same trace.
+One forward is the walk kernel, preceded for a packed batch by the kernel that orders its
+sequences and, for an in-place variance update, by a copy of the initial variances. The kernel
+trace is cut into forwards at every dispatch whose name contains SUBSTR (the forward's first
+kernel); a forward's span runs from its first dispatch's start to the last end before the next
+forward. The per-kernel duration statistics come from the same trace.
 
 The per-dispatch FETCH_SIZE and WRITE_SIZE counters (KiB) of every kernel of the forward are
 summed per forward, and the same two counters of a plain device copy of N bytes give each
@@ -30,8 +30,7 @@ import os
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_07816_amd", "csrc")
-FORWARD_KERNELS = ("summary_", "carry_scan", "chunk_table", "seg_table", "prep_kernel",
-                   "state_kernel")
+FORWARD_KERNELS = ("walk_kernel", "order_kernel", "copy_floats_kernel")
 
 
 def source_hash() -> str:
@@ -111,7 +110,7 @@ def copy_kib(dirname: str, kernel: str):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--name", required=True)
-    ap.add_argument("--first-kernel", default="summary_")
+    ap.add_argument("--first-kernel", default="walk_kernel")
     ap.add_argument("--trace", required=True)
     ap.add_argument("--fetch", required=True)
     ap.add_argument("--write", required=True)
@@ -136,7 +135,7 @@ def main():
     w_scale = args.copy_bytes / (cwk * 1024.0)
     read_b = fk * 1024.0 * f_scale
     write_b = wk * 1024.0 * w_scale
-    rec = dict(unit="one forward call (all kernels, both streams)",
+    rec = dict(unit="one forward call (every kernel of the call)",
                kernel_source_sha256=source_hash(), forwards=len(steady),
                forward_span_ns=span_ns, kernels=stats,
                fetch_kib_per_forward=fk, write_kib_per_forward=wk, counter_forwards=[nf, nw],
@@ -155,7 +154,7 @@ def main():
         f"{v['max_ns'] / 1e3:.1f} us |" for k, v in order)
     md = f"""# {args.name}
 
-Unit: one forward call (every kernel of the path, both streams).
+Unit: one forward call (every kernel of the call; here the walk kernel alone).
 Kernel source sha256 (all of csrc/): `{rec['kernel_source_sha256']}`
 
 ## Forward span (rocprofv3 --kernel-trace --stats)
@@ -167,9 +166,6 @@ forward of the run excluded): **{span_ns / 1e3:.1f} us**.
 |---|---|---|---|---|
 {krows}
 
-The state passes run on a second stream, overlapped with the next segment's prep pass, so the
-kernel durations add up to more than the span.
-
 ## HBM bytes per forward (rocprofv3 --pmc, one counter per run)
 
 | counter | forward (KiB) | plain copy of {args.copy_bytes / 2**30:.2f} GiB (KiB) | scale (bytes moved / counter bytes) | forward bytes |
@@ -178,9 +174,10 @@ kernel durations add up to more than the span.
 | WRITE_SIZE | {wk:.0f} | {cwk:.0f} | {w_scale:.4f} | {write_b / gb:.4f} GB |
 
 Traffic per forward: {(read_b + write_b) / gb:.4f} GB; algorithmic bytes per forward:
-{args.algorithmic_bytes / gb:.4f} GB (ratio {(read_b + write_b) / args.algorithmic_bytes:.3f}). The excess
-is the chunk summaries' second read of k, alpha and omega and the per-(chunk, head) WY factors
-that the prep passes write and the state passes read.
+{args.algorithmic_bytes / gb:.4f} GB (ratio {(read_b + write_b) / args.algorithmic_bytes:.3f}). Every
+workgroup of a head (one per block of value columns) reads the head's q, k, alpha and omega;
+the blocks of one head run on one XCD, so all but the first read should hit its L2, and
+traffic above the algorithmic bytes counts the reads that did not.
 Achieved on algorithmic bytes at the traced span: {args.algorithmic_bytes / (span_ns * 1e-9) / gb:.1f} GB/s.
 
 ## Commands (run from the repository root on the GPU host, TMPDIR=/tmp)

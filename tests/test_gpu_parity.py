@@ -81,19 +81,18 @@ def test_forward_packed_ragged(variant, dtype):
 
 
 @pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
-def test_forward_segmented_f32(variant, apc):
-    # 69 chunks of 16 per sequence: every sequence is cut into 4 segments, the state pass of a
-    # segment runs on a second stream behind the prep pass, and S crosses segments through the
-    # workspace (initial states given)
+def test_forward_long_f32(variant, apc):
+    # 69 chunks of 16 per sequence (the last one partial): the state and the variance chain are
+    # carried through many chunk steps of the walk, from given initial states
     x = W.draw_inputs(variant, "f32", 2, 1100, 2, 32, 32, seed=47, alpha_per_channel=apc,
                       random_state=True)
     compare_forward(x, 16)
 
 
 @pytest.mark.parametrize("variant", ["diag", "iso"])
-def test_forward_segmented_packed_f32(variant):
-    # packed sequences of 44, 1, 65, 0 and 21 chunks, each cut into 4 segments of its own
-    # (several of them empty)
+def test_forward_long_packed_f32(variant):
+    # packed sequences of 44, 1, 65, 0 and 21 chunks (one empty, two with a partial last
+    # chunk), walked longest first
     lens = [700, 3, 1040, 0, 333]
     x = W.draw_inputs(variant, "f32", 1, sum(lens), 2, 32, 32, seed=48, lengths=lens,
                       random_state=True)
