@@ -50,6 +50,47 @@ def algorithmic_flops(B, T, H, dk, dv, C=64):
     return B * T * H * (6 * d * dv + 10 * C * d + C * C / 3.0)
 
 
+def decode_bytes(R, H, dk, dv, in_bytes):
+    """Minimum HBM traffic of one Diagonal decode step: the state slot read and written
+    (S and P in float32), the token's inputs read and o written."""
+    per_row_head = 2 * (dk * dv * 4 + dk * 4) + (2 * dk + dv + 2 * dk) * in_bytes + in_bytes \
+        + dv * in_bytes
+    return R * H * per_row_head
+
+
+def decode_measure(kdn, W, torch, steps=64):
+    """Diagonal decode steps at the serving shape (R = 256 rows, H = 16, d = 128, bf16 inputs,
+    a float32 state pool of 256 slots updated in place): per-step HIP-event durations on the
+    caller's stream, against the HBM roofline. Reported beside the forward line."""
+    import numpy as np
+    R, H, d = 256, 16, 128
+    x = W.draw_inputs("diag", "bf16", R, 1, H, d, d, seed=1004, random_state=True)
+    dev = {n: torch.from_numpy(x.stored[n].view(np.int16)).view(torch.bfloat16).cuda()[:, 0]
+           for n in ("q", "k", "v", "alpha", "omega", "r")}
+    S = torch.from_numpy(x.S0.astype(np.float32)).cuda()
+    P = torch.from_numpy(x.P0.astype(np.float32)).cuda()
+    stream = torch.cuda.current_stream()
+    args = [dev[n] for n in ("q", "k", "v", "alpha", "omega", "r")]
+    for _ in range(5):
+        kdn.decode_step("diag", *args, S, P, mu=x.mu, scale=x.scale)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        kdn.decode_step("diag", *args, S, P, mu=x.mu, scale=x.scale)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    nbytes = decode_bytes(R, H, d, d, 2)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"workload": "diag-decode-R256-H16-d128 (state pool of 256 slots, bf16 inputs)",
+            "kernel": "decode_kernel: one workgroup per (row, head)", "steps": steps,
+            "ms_per_step_median": round(ms, 4), "tokens_per_s": round(R / (ms * 1e-3), 1),
+            "algorithmic_bytes_per_step": nbytes, "achieved": round(gbs, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 PROFILE = os.path.join(ROOT, "profiles", "kdn_forward_diag_B4_T4096_H16_d128.json")
 
 
@@ -197,6 +238,7 @@ def main():
                      "mfma_frac": round(aflops / (kmean * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
                                         4)},
     }
+    rec["decode"] = decode_measure(kdn, W, torch)
     if not args.no_cpu_baseline:
         nthreads = min(16, os.cpu_count() or 1)
         rec["cpu_baseline"] = cpu_baseline(x, nthreads)
