@@ -17,14 +17,14 @@
 //      follow from the chunk carry (eq. chunk-gain-local-prefix), and each wave replays its
 //      tokens (eq. chunk-gain-emission) to get p_hat_t (diagonal) or b_hat_t and
 //      beta_t = b_hat_t / (r_t + b_hat_t ||k_t||^2) (isotropic);
-//   2. operands: K_bar = Gamma (.) K, Q_bar = scale Gamma (.) Q, P_bar = G (.) K (/) Gamma with
+//   2. operands: K_bar = Gamma (.) K, Q_bar = Gamma (.) Q, P_bar = G (.) K (/) Gamma with
 //      G = p_hat (diagonal) or beta (isotropic);
 //   3. L = diag(c) + tril(K_bar P_bar^T, -1) with c_t = r_t + (K_bar P_bar^T)_tt
 //      = r_t + sum_i p_hat_ti k_ti^2 (diagonal, the innovation variance of eq. kla-box-gain) or
 //      c_t = 1 (isotropic); A = L^-1; A_qk = tril(Q_bar P_bar^T) (diagonal included: the read
 //      follows the write);
 //   4. R = A (V - K_bar S)   (row t: token t's innovation divided by c_t),
-//      O = Q_bar S + A_qk R,  S <- gamma_C (.) (S + P_bar^T R).
+//      O = scale (Q_bar S + A_qk R),  S <- gamma_C (.) (S + P_bar^T R).
 // This is Sec. "Chunkwise Memory Scan" (R = U - W S with W = A K_bar and U = A V, K_tail =
 // (gamma_C / gamma) (.) kappa) with the gain's normalisation kappa_t = p_hat_t (.) k_t / c_t
 // moved into the triangular solve: the unit-lower I + T of the section becomes L, and W, U are
@@ -661,7 +661,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     }
                     if (vact) {
                         st2<MT>(Kb + t * LDK + ch, g0 * K.x, g1 * K.y);
-                        st2<MT>(Qb + t * LDK + ch, a.scale * g0 * Q.x, a.scale * g1 * Q.y);
+                        st2<MT>(Qb + t * LDK + ch, g0 * Q.x, g1 * Q.y);  // scale: applied to O
                         st2<MT>(Pb + t * LDK + ch, pb0[j], pb1[j]);
                     }
                 }
@@ -961,7 +961,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
 #pragma unroll
                         for (int rr = 0; rr < 4; ++rr)
                             Ost[(16 * ib + 4 * lg + rr) * LDO + 16 * nt + li] =
-                                from_f32<TI>(Oacc[j][rr]);
+                                from_f32<TI>(a.scale * Oacc[j][rr]);
                     }
                 }
 #pragma unroll
