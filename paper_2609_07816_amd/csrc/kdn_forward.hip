@@ -775,13 +775,18 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                 // fragments
                 auto lq_unit = [&](int ib, int jb, const typename FK::V* kf,
                                    const typename FK::V* qf) {
+                    // all fragments are read before the products (fixed by a scheduling barrier),
+                    // so their LDS latency overlaps instead of being paid step by step
+                    typename FK::V pf[FK::NS];
+#pragma unroll
+                    for (int s = 0; s < FK::NS; ++s)
+                        pf[s] = FK::ld(Pb + (16 * jb + li) * LDK + FK::KF * s + (FK::KF / 4) * lg);
+                    __builtin_amdgcn_sched_barrier(0);
                     floatx4 tacc = zero4(), qacc = zero4();
 #pragma unroll
                     for (int s = 0; s < FK::NS; ++s) {
-                        const int k0 = FK::KF * s + (FK::KF / 4) * lg;
-                        const typename FK::V pf = FK::ld(Pb + (16 * jb + li) * LDK + k0);
-                        tacc = FK::mma(tacc, kf[s], pf);
-                        qacc = FK::mma(qacc, qf[s], pf);
+                        tacc = FK::mma(tacc, kf[s], pf[s]);
+                        qacc = FK::mma(qacc, qf[s], pf[s]);
                     }
                     if (ib > jb) {
                         MT* lo = Lo + (ib * (ib - 1) / 2 + jb) * 16 * LDE;
@@ -830,6 +835,15 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                         }
                         for (int jb = SHIFT && ib == 3 ? 2 : 0; jb <= ib; ++jb)
                             lq_unit(ib, jb, kf, qf);
+                        // the S fragments of every column tile are read before the products
+                        typename FK::V sf[CF::NNT][FK::NS];
+#pragma unroll
+                        for (int nt = 0; nt < CF::NNT; ++nt)
+#pragma unroll
+                            for (int s = 0; s < FK::NS; ++s)
+                                sf[nt][s] = FK::ld(SmT + (16 * nt + li) * LDK + FK::KF * s +
+                                                   (FK::KF / 4) * lg);
+                        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                         for (int nt = 0; nt < CF::NNT; ++nt) {
                             const int j = rw * CF::NNT + nt;
@@ -837,10 +851,8 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                             Oacc[j] = zero4();
 #pragma unroll
                             for (int s = 0; s < FK::NS; ++s) {
-                                const int k0 = FK::KF * s + (FK::KF / 4) * lg;
-                                const typename FK::V b = FK::ld(SmT + (16 * nt + li) * LDK + k0);
-                                xacc = FK::mma(xacc, kf[s], b);
-                                Oacc[j] = FK::mma(Oacc[j], qf[s], b);
+                                xacc = FK::mma(xacc, kf[s], sf[nt][s]);
+                                Oacc[j] = FK::mma(Oacc[j], qf[s], sf[nt][s]);
                             }
                             float xv[4];
 #pragma unroll

@@ -398,21 +398,6 @@ hipError_t launch_gain_dk(int dk, int variant, const void* k, const void* alpha,
 
 }  // namespace
 
-hipError_t launch_chunk_table(const int32_t* cu, int N, int cg, int32_t* choff, hipStream_t st)
-{
-    hipLaunchKernelGGL(chunk_table_kernel, dim3(1), dim3(1), 0, st, cu, N, cg, choff);
-    return hipGetLastError();
-}
-
-hipError_t launch_carry_scan(const float4* summ, const float* P0, const SeqArgs& sa, int nchan,
-                             int cg, const int32_t* choff, float2* carry, float* P_T,
-                             hipStream_t st)
-{
-    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H, (nchan + 3) / 4), dim3(256), 0, st,
-                       summ, P0, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, cg, carry, P_T);
-    return hipGetLastError();
-}
-
 size_t gain_workspace_bytes(int variant, int N, int B, int T, int H, int dk)
 {
     // chunks: fixed length has N * ceil(T / CG) <= B*T/CG + N; a packed batch (B = 1) has at

@@ -83,15 +83,7 @@ hipError_t launch_gain(int variant, const void* k, const void* alpha, const void
                        float* P_T, const SeqArgs& sa, int dk, kdn_dtype_t dtype,
                        int alpha_per_channel, float mu, void* workspace, hipStream_t stream);
 
-// Chunk machinery of the variance scan (kdn_gain.hip), shared with the chunked forward.
-// choff[n] = first global chunk of sequence n for chunks of cg tokens (packed batches only).
-hipError_t launch_chunk_table(const int32_t* cu, int N, int cg, int32_t* choff, hipStream_t st);
-// Exclusive carries z_in (float2 per chunk, head and channel) from chunk summaries, and P_T.
-hipError_t launch_carry_scan(const float4* summ, const float* P0, const SeqArgs& sa, int nchan,
-                             int cg, const int32_t* choff, float2* carry, float* P_T,
-                             hipStream_t st);
-
-// Chunked forward (kdn_chunked.hip).
+// Chunked forward: the walk kernel (kdn_forward.hip).
 struct FwdCall {
     int variant, apc;  // 0 = diagonal, 1 = isotropic; per-channel gate (isotropic)
     const void *q, *k, *v, *alpha, *omega, *r;
