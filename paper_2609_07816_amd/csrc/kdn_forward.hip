@@ -958,18 +958,38 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             // ---- phase D: O = Q_bar S + A_qk R (staged for the next iteration's stores) and
             // S <- gamma_C (.) (S + P_bar^T R) ------------------------------------------------
             if (mwork) {
+                // every fragment of the phase is read before the products (fixed by a
+                // scheduling barrier); the blocks of A_qk right of the diagonal are zero, so the
+                // O tiles run the whole contraction
+                typename FC::V rf[CF::NNT][FC::NS], af[CF::XPW][FC::NS], pf[CF::SPW][FC::NS];
+#pragma unroll
+                for (int nt = 0; nt < CF::NNT; ++nt)
+#pragma unroll
+                    for (int s = 0; s < FC::NS; ++s)
+                        rf[nt][s] = FC::ld(RT + (16 * nt + li) * LDC + FC::KF * s + (FC::KF / 4) * lg);
+#pragma unroll
+                for (int j = 0; j < CF::XPW; ++j) {
+                    const int ib = min(mw + NMW * (j / CF::NNT), NB - 1);
+#pragma unroll
+                    for (int s = 0; s < FC::NS; ++s)
+                        af[j][s] = FC::ld(Aq + (16 * ib + li) * LDC + FC::KF * s + (FC::KF / 4) * lg);
+                }
+#pragma unroll
+                for (int j = 0; j < CF::SPW; ++j) {
+                    const int ik = min(mw + NMW * j, CF::NST - 1) % CF::NKT;
+#pragma unroll
+                    for (int s = 0; s < FC::NS; ++s)
+                        pf[j][s] =
+                            FC::ld(PbTm + (16 * ik + li) * LDC + FC::KF * s + (FC::KF / 4) * lg);
+                }
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int j = 0; j < CF::XPW; ++j) {
                     const int ib = mw + NMW * (j / CF::NNT), nt = j % CF::NNT;
                     if (ib < NB) {
 #pragma unroll
-                        for (int s = 0; s < FC::NS; ++s) {
-                            if (FC::KF * s < 16 * (ib + 1)) {
-                                const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-                                Oacc[j] = FC::mma(Oacc[j], FC::ld(Aq + (16 * ib + li) * LDC + k0),
-                                                  FC::ld(RT + (16 * nt + li) * LDC + k0));
-                            }
-                        }
+                        for (int s = 0; s < FC::NS; ++s)
+                            Oacc[j] = FC::mma(Oacc[j], af[j][s], rf[nt][s]);
 #pragma unroll
                         for (int rr = 0; rr < 4; ++rr)
                             Ost[(16 * ib + 4 * lg + rr) * LDO + 16 * nt + li] =
@@ -981,12 +1001,13 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     const int x = mw + NMW * j;
                     if (x < CF::NST) {
                         const int ik = x % CF::NKT, nt = x / CF::NKT;
+                        // with NKT a multiple of NMW the column tile depends on j alone
+                        constexpr bool NTS = CF::NKT % NMW == 0;
+                        const int ntr = NTS ? NMW * j / CF::NKT : nt;
 #pragma unroll
-                        for (int s = 0; s < FC::NS; ++s) {
-                            const int k0 = FC::KF * s + (FC::KF / 4) * lg;
-                            Sacc[j] = FC::mma(Sacc[j], FC::ld(PbTm + (16 * ik + li) * LDC + k0),
-                                              FC::ld(RT + (16 * nt + li) * LDC + k0));
-                        }
+                        for (int s = 0; s < FC::NS; ++s)
+                            Sacc[j] = FC::mma(Sacc[j], pf[j][s],
+                                              ntr == 0 ? rf[0][s] : rf[CF::NNT - 1][s]);
                         const float4 gc =
                             *reinterpret_cast<const float4*>(gC + pm * DK + 16 * ik + 4 * lg);
                         Sacc[j][0] *= gc.x;
