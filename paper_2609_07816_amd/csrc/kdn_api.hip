@@ -79,9 +79,9 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
     if (!(mu > 0.f) || !(scale > 0.f))
         return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
                     scale);
-    if (chunk != 0 && !kdn::chunked_supported(dtype, dk, dv, chunk))
-        return fail(KDN_ERR_UNSUPPORTED, "chunk=%d does not fit one workgroup's LDS for this "
-                    "dtype, dk=%d and dv=%d (use 0 for the largest that fits)", chunk, dk, dv);
+    if (!kdn::chunked_supported(chunk))
+        return fail(KDN_ERR_UNSUPPORTED, "chunk=%d: the forward runs chunks of 64 tokens (pass 0 "
+                    "or 64)", chunk);
     const size_t ntok = (size_t)B * T * H, es = esize(dtype);
     const size_t nk = ntok * dk * es, nv = ntok * dv * es;
     if (nk >= ((size_t)1 << 31) || nv >= ((size_t)1 << 31))
@@ -103,8 +103,7 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
         return fail(KDN_ERR_INVALID_ARG, "P_T partially overlaps P0");
     if (overlaps(o, nv, S_T, ns) || overlaps(o, nv, P_T, np))
         return fail(KDN_ERR_INVALID_ARG, "o overlaps the state outputs");
-    const size_t need =
-        kdn::chunked_workspace_bytes(variant, cu != nullptr, N, B, T, H, dk, dv, dtype, chunk);
+    const size_t need = kdn::chunked_workspace_bytes(variant, cu != nullptr, N, B, T, H, dk, dtype);
     if (need > 0 && (!ws || ws_bytes < need))
         return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                     ws ? ws_bytes : (size_t)0);
@@ -115,14 +114,14 @@ kdn::FwdCall fwd_call(int variant, int apc, const void* q, const void* k, const 
                       const void* alpha, const void* omega, const void* r, const float* S0,
                       const float* P0, void* o, float* S_T, float* P_T, const int32_t* cu,
                       int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
-                      kdn_dtype_t dtype, float mu, float scale, int32_t chunk, void* ws)
+                      kdn_dtype_t dtype, float mu, float scale, void* ws)
 {
     kdn::FwdCall c;
     c.variant = variant; c.apc = apc;
     c.q = q; c.k = k; c.v = v; c.alpha = alpha; c.omega = omega; c.r = r;
     c.S0 = S0; c.P0 = P0; c.o = o; c.S_T = S_T; c.P_T = P_T;
     c.sa = {cu, N, B, T, H};
-    c.dk = dk; c.dv = dv; c.dtype = dtype; c.mu = mu; c.scale = scale; c.chunk = chunk;
+    c.dk = dk; c.dv = dv; c.dtype = dtype; c.mu = mu; c.scale = scale;
     c.workspace = ws;
     return c;
 }
@@ -153,8 +152,10 @@ size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_
 {
     if (N <= 0 || B <= 0 || T <= 0 || H <= 0 || !head_ok(dk) || !head_ok(dv)) return 0;
     if (dtype != KDN_F32 && dtype != KDN_BF16) return 0;
-    if (chunk != 0 && !kdn::chunked_supported(dtype, dk, dv, chunk)) return 0;
-    return kdn::chunked_workspace_bytes(variant, packed != 0, N, B, T, H, dk, dv, dtype, chunk);
+    if (variant != 0 && variant != 1) return 0;
+    if (!kdn::chunked_supported(chunk)) return 0;
+    (void)dv;
+    return kdn::chunked_workspace_bytes(variant, packed != 0, N, B, T, H, dk, dtype);
 }
 
 size_t kdn_gain_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
@@ -177,7 +178,7 @@ kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const
     if (st != KDN_OK) return st;
     return hip_status(kdn::launch_chunked(fwd_call(0, 1, q, k, v, alpha, omega, r, S0, P0, o, S_T,
                                                    P_T, cu_seqlens, N, B, T, H, dk, dv, dtype,
-                                                   mu, scale, chunk, workspace),
+                                                   mu, scale, workspace),
                                           (hipStream_t)stream),
                       "kdn_forward_diag launch");
 }
@@ -197,7 +198,7 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
     if (st != KDN_OK) return st;
     return hip_status(kdn::launch_chunked(fwd_call(1, apc, q, k, v, alpha, omega, r, S0, P0, o,
                                                    S_T, P_T, cu_seqlens, N, B, T, H, dk, dv,
-                                                   dtype, mu, scale, chunk, workspace),
+                                                   dtype, mu, scale, workspace),
                                           (hipStream_t)stream),
                       "kdn_forward_iso launch");
 }
@@ -229,8 +230,11 @@ kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, cons
     const size_t ns = (size_t)num_slots * H * dk * dv * 4;
     const size_t np = (size_t)num_slots * H * (variant == 0 ? dk : 1) * 4;
     const void* ins[6] = {q, k, v, alpha, omega, r};
+    const size_t insz[6] = {rows * dk * es, rows * dk * es, rows * dv * es,
+                            rows * ((variant == 0 || alpha_per_channel) ? dk : 1) * es,
+                            rows * (variant == 0 ? dk : 1) * es, rows * es};
     for (int i = 0; i < 6; ++i)
-        if (overlaps(o, rows * dv * es, ins[i], rows * es))
+        if (overlaps(o, rows * dv * es, ins[i], insz[i]))
             return fail(KDN_ERR_INVALID_ARG, "output o overlaps input %d", i);
     if (overlaps(o, rows * dv * es, S, ns) || overlaps(o, rows * dv * es, P, np) ||
         overlaps(S, ns, P, np))

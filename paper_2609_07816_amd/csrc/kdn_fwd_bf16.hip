@@ -1,0 +1,8 @@
+// bf16 instantiation of the chunked forward (kernels in kdn_fwd.h).
+#include "kdn_fwd.h"
+
+namespace kdn {
+namespace fwd {
+template hipError_t run_forward<bf16>(const FwdCall& fc, hipStream_t st);
+}  // namespace fwd
+}  // namespace kdn

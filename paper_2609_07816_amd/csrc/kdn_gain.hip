@@ -15,7 +15,7 @@
 // Every product is rescaled by an exact power of two, which leaves n / d unchanged.
 // The diagonal chain gives every channel its own thread (channels are independent); the
 // isotropic chain gives every token a lane and scans inside the wavefront.
-#include "kdn_internal.h"
+#include "kdn_device.h"
 
 namespace kdn {
 namespace {
@@ -53,63 +53,6 @@ __device__ __forceinline__ Mat2 shfl_up_mat(const Mat2& x, int off)
     return y;
 }
 
-// Token range [t0, t1) (flat token index over B*T) of sequence n.
-__device__ __forceinline__ void seq_bounds(const int32_t* cu, int n, int T, int& t0, int& t1)
-{
-    if (cu) {
-        t0 = cu[n];
-        t1 = cu[n + 1];
-        if (t1 < t0) t1 = t0;
-    } else {
-        t0 = n * T;
-        t1 = t0 + T;
-    }
-}
-
-// Locate global chunk g: sequence n, chunk start token t (flat), chunk end, last-of-sequence.
-// Chunk offsets: fixed length -> n * ceil(T / CG); packed -> the table built on the device.
-__device__ __forceinline__ bool locate_chunk(const int32_t* cu, const int32_t* choff, int N,
-                                             int T, int g, int& n, int& c0, int& c1,
-                                             int& mloc, bool& last, int cg = CG)
-{
-    if (!cu) {
-        const int ncs = (T + cg - 1) / cg;
-        n = g / ncs;
-        if (n >= N) return false;
-        mloc = g - n * ncs;
-    } else {
-        if (g >= choff[N]) return false;
-        int lo = 0, hi = N - 1;  // largest n with choff[n] <= g
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (choff[mid] <= g) lo = mid; else hi = mid - 1;
-        }
-        n = lo;
-        mloc = g - choff[n];
-    }
-    int t0, t1;
-    seq_bounds(cu, n, T, t0, t1);
-    c0 = t0 + mloc * cg;
-    c1 = min(c0 + cg, t1);
-    last = (c1 == t1);
-    return c0 < c1;
-}
-
-// Chunk-offset table for packed batches: choff[n] = sum_{m < n} ceil(len_m / cg).
-__global__ void chunk_table_kernel(const int32_t* __restrict__ cu, int N, int cg,
-                                   int32_t* __restrict__ choff)
-{
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
-    int acc = 0;
-    for (int n = 0; n < N; ++n) {
-        choff[n] = acc;
-        int len = cu[n + 1] - cu[n];
-        if (len < 0) len = 0;
-        acc += (len + cg - 1) / cg;
-    }
-    choff[N] = acc;
-}
-
 // ------------------------------------------------------------------------------------------
 // Diagonal chain
 // ------------------------------------------------------------------------------------------
@@ -118,13 +61,12 @@ __global__ void chunk_table_kernel(const int32_t* __restrict__ cu, int N, int cg
 template <class E, int DK>
 __global__ __launch_bounds__(DK) void diag_summary_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, const int32_t* __restrict__ cu, const int32_t* __restrict__ choff,
-    int N, int T, int H, float mu, float4* __restrict__ summ)
+    const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
 {
     const int g = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
-    int n, c0, c1, m;
+    int n, c0, c1;
     bool last;
-    if (!locate_chunk(cu, choff, N, T, g, n, c0, c1, m, last)) return;
+    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
     Mat2 acc = {1.f, 0.f, 0.f, 1.f};
     for (int t = c0; t < c1; ++t) {
         const size_t row = (size_t)t * H + h;
@@ -135,72 +77,20 @@ __global__ __launch_bounds__(DK) void diag_summary_kernel(
     summ[((size_t)g * H + h) * DK + c] = make_float4(acc.a, acc.b, acc.c, acc.d);
 }
 
-// Pass 2: per (sequence, head, channel) exclusive scan of the summaries over chunks of cg
-// tokens. Grid (sequence x head, channel groups of 4); one wavefront per channel, lanes are
-// chunks, blocks of 64 chunks carry into the next.
-__global__ __launch_bounds__(256) void carry_scan_kernel(
-    const float4* __restrict__ summ, const float* __restrict__ P0,
-    const int32_t* __restrict__ cu, const int32_t* __restrict__ choff, int N, int T, int H,
-    int nchan, int cg, float2* __restrict__ carry, float* __restrict__ P_T)
-{
-    const int n = blockIdx.x / H, h = blockIdx.x % H;
-    if (n >= N) return;
-    int t0, t1;
-    seq_bounds(cu, n, T, t0, t1);
-    const int nch = (t1 - t0 + cg - 1) / cg;
-    const int g0 = cu ? choff[n] : n * ((T + cg - 1) / cg);
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int c = 4 * blockIdx.y + w;  // one channel per wavefront
-    if (c >= nchan) return;
-    if (nch == 0) {  // an empty sequence keeps its initial variances
-        if (P_T && lane == 0) {
-            const size_t pidx = ((size_t)n * H + h) * nchan + c;
-            P_T[pidx] = P0 ? P0[pidx] : 1.f;
-        }
-        return;
-    }
-    {
-        const size_t pidx = ((size_t)n * H + h) * nchan + c;
-        float cn = P0 ? P0[pidx] : 1.f, cd = 1.f;  // z_0 = [p_0; 1]
-        for (int b0 = 0; b0 < nch; b0 += 64) {
-            const int m = b0 + lane;
-            Mat2 x = {1.f, 0.f, 0.f, 1.f};
-            if (m < nch) {
-                const float4 s = summ[((size_t)(g0 + m) * H + h) * nchan + c];
-                x = {s.x, s.y, s.z, s.w};
-            }
-#pragma unroll
-            for (int off = 1; off < 64; off <<= 1) {  // inclusive Kogge-Stone, later on the left
-                const Mat2 y = shfl_up_mat(x, off);
-                if (lane >= off) x = mul(x, y);
-            }
-            float zn = x.a * cn + x.b * cd, zd = x.c * cn + x.d * cd;  // state after chunk m
-            renorm2(zn, zd);
-            float en = __shfl_up(zn, 1, 64), ed = __shfl_up(zd, 1, 64);
-            if (lane == 0) { en = cn; ed = cd; }
-            if (m < nch) carry[((size_t)(g0 + m) * H + h) * nchan + c] = make_float2(en, ed);
-            const int lastl = min(63, nch - 1 - b0);
-            cn = __shfl(zn, lastl, 64);
-            cd = __shfl(zd, lastl, 64);
-        }
-    }
-}
-
 // Pass 3: replay each chunk from its carry; p_hat_t = a_t n/d + w_t before M_t is applied;
 // kappa_t = p_hat_t k_t / (r_t + sum_i p_hat_ti k_ti^2) (eq. chunk-gain-emission).
 template <class E, int DK>
 __global__ __launch_bounds__(DK) void diag_emit_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, const float2* __restrict__ carry, const int32_t* __restrict__ cu,
-    const int32_t* __restrict__ choff, int N, int T, int H, float mu,
+    const E* __restrict__ r, const float2* __restrict__ carry, ChunkMap cm, int H, float mu,
     float* __restrict__ kappa_out, float* __restrict__ phat_out, float* __restrict__ P_T)
 {
     __shared__ float s_part[CG][DK + 1];
     __shared__ float s_rden[CG];
     const int g = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
-    int n, c0, c1, m;
+    int n, c0, c1;
     bool last;
-    if (!locate_chunk(cu, choff, N, T, g, n, c0, c1, m, last)) return;
+    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
     const float2 z = carry[((size_t)g * H + h) * DK + c];
     float zn = z.x, zd = z.y;
     float pk[CG];
@@ -271,13 +161,12 @@ __device__ __forceinline__ void iso_coeffs(const E* k, const E* alpha, const E* 
 template <class E, int DK, bool APC>
 __global__ __launch_bounds__(64) void iso_summary_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, const int32_t* __restrict__ cu, const int32_t* __restrict__ choff,
-    int N, int T, int H, float mu, float4* __restrict__ summ)
+    const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
 {
     const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-    int n, c0, c1, m;
+    int n, c0, c1;
     bool last;
-    if (!locate_chunk(cu, choff, N, T, g, n, c0, c1, m, last)) return;
+    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
     Mat2 x = {1.f, 0.f, 0.f, 1.f};
     if (c0 + lane < c1) {
         float a, w, u, nk;
@@ -299,14 +188,13 @@ __global__ __launch_bounds__(64) void iso_summary_kernel(
 template <class E, int DK, bool APC>
 __global__ __launch_bounds__(64) void iso_emit_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, const float2* __restrict__ carry, const int32_t* __restrict__ cu,
-    const int32_t* __restrict__ choff, int N, int T, int H, float mu,
+    const E* __restrict__ r, const float2* __restrict__ carry, ChunkMap cm, int H, float mu,
     float* __restrict__ beta_out, float* __restrict__ bhat_out, float* __restrict__ P_T)
 {
     const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
-    int n, c0, c1, m;
+    int n, c0, c1;
     bool last;
-    if (!locate_chunk(cu, choff, N, T, g, n, c0, c1, m, last)) return;
+    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
     const bool valid = c0 + lane < c1;
     const size_t row = (size_t)(c0 + lane) * H + h;
     float a = 1.f, w = 0.f, u = 0.f, nk = 0.f;
@@ -345,34 +233,40 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
     off += (size_t)maxch * sa.H * nchan * sizeof(float4);
     float2* carry = (float2*)(ws + off);
     if (maxch == 0) return hipSuccess;
-    if (sa.cu_seqlens)
-        hipLaunchKernelGGL(chunk_table_kernel, dim3(1), dim3(1), 0, st, sa.cu_seqlens, sa.N,
-                           CG, choff);
+    ChunkMap cm;
+    cm.cu = sa.cu_seqlens;
+    cm.choff = sa.cu_seqlens ? choff : nullptr;
+    cm.N = sa.N;
+    cm.T = sa.T;
+    cm.ntok = sa.B * sa.T;
+    cm.maxch = maxch;
+    hipError_t e;
+    if (sa.cu_seqlens &&
+        (e = launch_chunk_table(sa.cu_seqlens, sa.N, cm.ntok, CG, maxch, choff, st)) != hipSuccess)
+        return e;
     const dim3 grid(maxch, sa.H);
     if (variant == 0) {
         hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
-                           sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, summ);
+                           cm, sa.H, mu, summ);
     } else if (apc) {
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,
-                           r_, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, summ);
+                           r_, cm, sa.H, mu, summ);
     } else {
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, false>), grid, dim3(64), 0, st, k_, a_,
-                           w_, r_, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, summ);
+                           w_, r_, cm, sa.H, mu, summ);
     }
-    hipLaunchKernelGGL(carry_scan_kernel, dim3(sa.N * sa.H, (nchan + 3) / 4), dim3(256), 0, st,
-                       summ, P0, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, nchan, CG, carry, P_T);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_carry_scan(summ, P0, cm, CG, sa.H, nchan, carry, P_T, st)) != hipSuccess)
+        return e;
     if (variant == 0) {
         hipLaunchKernelGGL((diag_emit_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
-                           carry, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, gain_out,
-                           phat_out, P_T);
+                           carry, cm, sa.H, mu, gain_out, phat_out, P_T);
     } else if (apc) {
         hipLaunchKernelGGL((iso_emit_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,
-                           r_, carry, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, gain_out,
-                           phat_out, P_T);
+                           r_, carry, cm, sa.H, mu, gain_out, phat_out, P_T);
     } else {
         hipLaunchKernelGGL((iso_emit_kernel<E, DK, false>), grid, dim3(64), 0, st, k_, a_, w_,
-                           r_, carry, sa.cu_seqlens, choff, sa.N, sa.T, sa.H, mu, gain_out,
-                           phat_out, P_T);
+                           r_, carry, cm, sa.H, mu, gain_out, phat_out, P_T);
     }
     return hipGetLastError();
 }

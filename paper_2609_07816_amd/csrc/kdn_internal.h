@@ -83,7 +83,8 @@ hipError_t launch_gain(int variant, const void* k, const void* alpha, const void
                        float* P_T, const SeqArgs& sa, int dk, kdn_dtype_t dtype,
                        int alpha_per_channel, float mu, void* workspace, hipStream_t stream);
 
-// Chunked forward: the walk kernel (kdn_forward.hip).
+// Chunked forward (kdn_fwd.hip): chunk summaries, the log-depth carry scan, the per-chunk prep
+// and the walk over the chunks.
 struct FwdCall {
     int variant, apc;  // 0 = diagonal, 1 = isotropic; per-channel gate (isotropic)
     const void *q, *k, *v, *alpha, *omega, *r;
@@ -94,13 +95,11 @@ struct FwdCall {
     int dk, dv;
     kdn_dtype_t dtype;
     float mu, scale;
-    int chunk;        // 16, 32, 64 or 0 (largest that fits)
     void* workspace;  // chunked_workspace_bytes(...) bytes
 };
-bool chunked_supported(kdn_dtype_t dtype, int dk, int dv, int chunk);
-int chunked_default_chunk(kdn_dtype_t dtype, int dk, int dv);
+bool chunked_supported(int chunk);
 size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
-                               int dv, kdn_dtype_t dtype, int chunk);
+                               kdn_dtype_t dtype);
 hipError_t launch_chunked(const FwdCall& fc, hipStream_t stream);
 
 }  // namespace kdn

@@ -56,8 +56,8 @@ def test_forward_argument_errors(L, variant):
     assert fwd(L, variant, dk=48) == kdn.KDN_ERR_UNSUPPORTED
     assert fwd(L, variant, dv=256) == kdn.KDN_ERR_UNSUPPORTED
     assert fwd(L, variant, chunk=24) == kdn.KDN_ERR_UNSUPPORTED
-    assert fwd(L, variant, dtype=0, dk=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
-    assert fwd(L, variant, dtype=0, dk=128, dv=128, chunk=64) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, chunk=16) == kdn.KDN_ERR_UNSUPPORTED
+    assert fwd(L, variant, chunk=32) == kdn.KDN_ERR_UNSUPPORTED
     # output aliasing an input
     p = [P(i) for i in range(7)]
     p[6] = p[2]
@@ -106,18 +106,42 @@ def test_forward_workspace(L):
         == kdn.KDN_ERR_WORKSPACE
 
 
+def rec_bytes(dk, es):
+    """Bytes of one (chunk, head) record of the prep: K_bar, Q_bar, P_tail^T (64 x dk each),
+    L^-1 and A_qk (64 x 64 each) in the operand precision, and gamma_C (dk float32), rounded up
+    to 256."""
+    raw = 3 * 64 * dk * es + 2 * 64 * 64 * es + 4 * dk
+    return (raw + 255) // 256 * 256
+
+
+def al256(x):
+    return (x + 255) // 256 * 256
+
+
 def test_workspace_queries(L):
-    # fixed length: a staging copy of P0 (one float per (sequence, head, channel)), rounded up
-    # to 256 bytes; a packed batch adds the walk order (one int32 per sequence)
-    full = L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 1, 0, 0)
-    assert full == 4 * 16 * 128 * 4
-    assert L.kdn_forward_workspace_bytes(1, 4, 4, 4096, 16, 128, 128, 1, 0, 0) == 256
-    assert L.kdn_forward_workspace_bytes(0, 32, 1, 135000, 16, 128, 128, 1, 1, 0) \
-        == 256 + 32 * 16 * 128 * 4
+    # fixed length: maxch = N * ceil(T / 64) chunks; per chunk and head a float4 summary and a
+    # float2 carry per variance channel, and one prep record
+    N, T, H, dk = 4, 4096, 16, 128
+    maxch = N * 64
+    want = al256(maxch * H * dk * 16) + al256(maxch * H * dk * 8) + maxch * H * rec_bytes(dk, 2)
+    assert L.kdn_forward_workspace_bytes(0, N, N, T, H, dk, 128, 1, 0, 0) == want
+    assert L.kdn_forward_workspace_bytes(0, N, N, T, H, dk, 128, 1, 0, 64) == want
+    want_iso = al256(maxch * H * 16) + al256(maxch * H * 8) + maxch * H * rec_bytes(dk, 2)
+    assert L.kdn_forward_workspace_bytes(1, N, N, T, H, dk, 128, 1, 0, 0) == want_iso
+    want_f32 = al256(maxch * H * dk * 16) + al256(maxch * H * dk * 8) + \
+        maxch * H * rec_bytes(dk, 4)
+    assert L.kdn_forward_workspace_bytes(0, N, N, T, H, dk, 128, 0, 0, 0) == want_f32
+    # packed: maxch = T / 64 + N, plus the chunk-offset table and the walk order
+    Np, Tp = 32, 135000
+    maxp = Tp // 64 + Np
+    want_p = al256((Np + 1) * 4) + al256(Np * 4) + al256(maxp * H * dk * 16) + \
+        al256(maxp * H * dk * 8) + maxp * H * rec_bytes(dk, 2)
+    assert L.kdn_forward_workspace_bytes(0, Np, 1, Tp, H, dk, 128, 1, 1, 0) == want_p
     # rejected arguments give 0
-    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 0, 0, 64) == 0
+    assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 128, 128, 1, 0, 32) == 0
     assert L.kdn_forward_workspace_bytes(0, 4, 4, 4096, 16, 48, 128, 1, 0, 0) == 0
     assert L.kdn_forward_workspace_bytes(0, 0, 4, 4096, 16, 128, 128, 1, 0, 0) == 0
+    assert L.kdn_forward_workspace_bytes(2, 4, 4, 4096, 16, 128, 128, 1, 0, 0) == 0
     small = L.kdn_gain_workspace_bytes(0, 1, 1, 64, 1, 128)
     big = L.kdn_gain_workspace_bytes(0, 4, 4, 4096, 16, 128)
     assert big > small > 0

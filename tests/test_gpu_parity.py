@@ -44,24 +44,24 @@ def compare_forward(x, chunk=0, tol=None):
 # ---------------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
-@pytest.mark.parametrize("chunk", [16, 0])
+@pytest.mark.parametrize("chunk", [64, 0])
 def test_forward_tiny_f32(variant, apc, chunk):
     compare_forward(W.draw_workload(0, variant, apc), chunk)
 
 
 @pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
-@pytest.mark.parametrize("chunk", [16, 32, 64])
-def test_forward_f32_multichunk_ragged(variant, apc, chunk):
-    x = W.draw_inputs(variant, "f32", 2, 150, 3, 32, 32, seed=41, alpha_per_channel=apc,
+@pytest.mark.parametrize("T", [150, 64, 17])
+def test_forward_f32_multichunk_ragged(variant, apc, T):
+    x = W.draw_inputs(variant, "f32", 2, T, 3, 32, 32, seed=41, alpha_per_channel=apc,
                       random_state=True)
-    compare_forward(x, chunk)
+    compare_forward(x)
 
 
-@pytest.mark.parametrize("dk,dv,chunk", [(128, 64, 32), (64, 128, 32), (16, 128, 16),
-                                         (32, 16, 64)])
-def test_forward_f32_head_sizes(dk, dv, chunk):
+@pytest.mark.parametrize("dk,dv", [(128, 128), (128, 64), (64, 128), (16, 128), (32, 16),
+                                   (16, 16)])
+def test_forward_f32_head_sizes(dk, dv):
     x = W.draw_inputs("diag", "f32", 1, 100, 2, dk, dv, seed=42, random_state=True)
-    compare_forward(x, chunk)
+    compare_forward(x)
 
 
 @pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
@@ -82,38 +82,56 @@ def test_forward_packed_ragged(variant, dtype):
 
 @pytest.mark.parametrize("variant,apc", [("diag", True), ("iso", True), ("iso", False)])
 def test_forward_long_f32(variant, apc):
-    # 69 chunks of 16 per sequence (the last one partial): the state and the variance chain are
-    # carried through many chunk steps of the walk, from given initial states
-    x = W.draw_inputs(variant, "f32", 2, 1100, 2, 32, 32, seed=47, alpha_per_channel=apc,
+    # 71 chunks of 64 per sequence (the last one partial): the variance carry crosses a block of
+    # 64 chunks of the log-depth scan, and the walk carries S through every chunk, from given
+    # initial states
+    x = W.draw_inputs(variant, "f32", 2, 4500, 2, 32, 32, seed=47, alpha_per_channel=apc,
                       random_state=True)
-    compare_forward(x, 16)
+    compare_forward(x)
 
 
 @pytest.mark.parametrize("variant", ["diag", "iso"])
 def test_forward_long_packed_f32(variant):
-    # packed sequences of 44, 1, 65, 0 and 21 chunks (one empty, two with a partial last
-    # chunk), walked longest first
-    lens = [700, 3, 1040, 0, 333]
+    # packed sequences of 11, 1, 66, 0, 17 and 6 chunks (one empty, several with a partial last
+    # chunk; one crosses a 64-chunk block of the carry scan), walked longest first
+    lens = [700, 3, 4200, 0, 1040, 333]
     x = W.draw_inputs(variant, "f32", 1, sum(lens), 2, 32, 32, seed=48, lengths=lens,
                       random_state=True)
-    compare_forward(x, 16)
+    compare_forward(x)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_chunk_size_independence(dtype):
+@pytest.mark.parametrize("variant", ["diag", "iso"])
+def test_forward_composition(variant, dtype):
+    """Two chained calls carrying (S, P) equal one call over the whole sequence (composition,
+    with the split inside a chunk)."""
+    from paper_2609_07816_amd import kdn
     d = 64
-    x = W.draw_inputs("diag", dtype, 1, 256, 2, d, d, seed=45, random_state=True)
-    chunks = (16, 32, 64) if dtype == "bf16" else (16, 32)  # float32 d=64 fits up to 32
-    outs = [run_gpu_forward(x, c) for c in chunks]
-    for o, S, P in outs[1:]:
-        check("o vs chunk 16", o, outs[0][0], TOL[dtype])
-        check("S vs chunk 16", S, outs[0][1], TOL[dtype])
+    x = W.draw_inputs(variant, dtype, 2, 300, 2, d, d, seed=45, random_state=True)
+    dd = to_device(x)
+    f = kdn.forward_diag if variant == "diag" else kdn.forward_iso
+    o, S, P = f(*[dd[n] for n in NAMES], S0=dd["S0"], P0=dd["P0"], mu=x.mu, scale=x.scale)
+    cut = 157
+    part = [dd[n][:, :cut].contiguous() for n in NAMES]
+    rest = [dd[n][:, cut:].contiguous() for n in NAMES]
+    o1, S1, P1 = f(*part, S0=dd["S0"], P0=dd["P0"], mu=x.mu, scale=x.scale)
+    o2, S2, P2 = f(*rest, S0=S1, P0=P1, mu=x.mu, scale=x.scale)
+    torch.cuda.synchronize()
+    check("o (two calls vs one)", host_f64(torch.cat([o1, o2], dim=1)), host_f64(o), TOL[dtype])
+    check("S_T (two calls vs one)", host_f64(S2), host_f64(S), TOL[dtype])
+    check("P_T (two calls vs one)", host_f64(P2), host_f64(P), TOL[dtype])
 
 
-def test_determinism_bitwise():
-    x = W.draw_inputs("diag", "bf16", 2, 300, 2, 128, 128, seed=46)
+@pytest.mark.parametrize("packed", [False, True])
+def test_determinism_bitwise(packed):
+    if packed:
+        lens = [300, 0, 1000, 64, 5, 700]
+        x = W.draw_inputs("diag", "bf16", 1, sum(lens), 2, 128, 128, seed=46, lengths=lens,
+                          random_state=True)
+    else:
+        x = W.draw_inputs("diag", "bf16", 2, 300, 2, 128, 128, seed=46)
     a = run_gpu_forward(x)
-    for _ in range(3):
+    for _ in range(10):
         b = run_gpu_forward(x)
         for u, w in zip(a, b):
             assert np.array_equal(u, w)
