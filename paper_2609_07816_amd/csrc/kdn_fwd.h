@@ -51,6 +51,8 @@ constexpr int NTH = 64 * NW;
 //   Kb [C][DK]   K_bar = gamma (.) k            Qb [C][DK]  Q_bar = gamma (.) q
 //   Pt [DK][C]   P_tail^T                       Li [C][C]   L^-1 (zeros above the diagonal)
 //   Aq [C][C]    A_qk (zeros above)             gC [DK]     gamma_C (float32)
+// The five matrices are stored in MFMA-fragment order (frag_off), so that the walk reads
+// every operand fragment as one contiguous block.
 template <class MT, int DK>
 struct OpRec {
     static constexpr size_t OFF_KB = 0;
@@ -61,6 +63,56 @@ struct OpRec {
     static constexpr size_t OFF_GC = OFF_AQ + (size_t)C * C * sizeof(MT);
     static constexpr size_t BYTES = al256(OFF_GC + (size_t)DK * 4);
 };
+
+// Fragment order of an R x K matrix (R and K multiples of 16) used as an MFMA A operand with
+// contraction over K: fragment (rb, s) holds rows 16 rb .. 16 rb + 15 and k in [KF s, KF s + KF)
+// as 64 consecutive pieces of E = KF / 4 elements, piece 16 g + i = row 16 rb + i,
+// k = KF s + E g .. + E - 1. Lane 16 g + i of a wave then loads piece 16 g + i: one fragment is
+// one contiguous read of 64 E elements.
+template <class MT, int K>
+__device__ __forceinline__ size_t frag_off(int row, int k)
+{
+    using F = Frag<MT, K>;
+    constexpr int E = F::KF / 4;
+    const int rb = row >> 4, i = row & 15, sk = k / F::KF, g = (k % F::KF) / E, e = k % E;
+    return ((size_t)(rb * F::NS + sk) * 64 + 16 * g + i) * E + e;
+}
+
+// Lane `lane`'s piece of fragment (rb, s).
+template <class MT, int K>
+__device__ __forceinline__ const MT* frag_piece(const MT* base, int rb, int sk, int lane)
+{
+    using F = Frag<MT, K>;
+    return base + ((size_t)(rb * F::NS + sk) * 64 + lane) * (F::KF / 4);
+}
+
+// Copy an R x K row-major LDS tile (leading dimension ld) to global memory in fragment order,
+// one piece of E elements per thread and step.
+template <class MT, int R, int K, int NTHR>
+__device__ __forceinline__ void copy_frag_order(MT* dst, const MT* src, int ld, int tid)
+{
+    using F = Frag<MT, K>;
+    constexpr int E = F::KF / 4, NPC = R * K / E;
+    static_assert(E * sizeof(MT) == 16 || E * sizeof(MT) == 8, "pieces of 8 or 16 bytes");
+    for (int p = tid; p < NPC; p += NTHR) {
+        const int lane = p & 63, fr = p >> 6;
+        const int rb = fr / F::NS, sk = fr % F::NS;
+        const int row = 16 * rb + (lane & 15), k = F::KF * sk + E * (lane >> 4);
+        if constexpr (E * sizeof(MT) == 16)
+            *reinterpret_cast<uint4*>(dst + (size_t)p * E) =
+                *reinterpret_cast<const uint4*>(src + row * ld + k);
+        else
+            *reinterpret_cast<uint2*>(dst + (size_t)p * E) =
+                *reinterpret_cast<const uint2*>(src + row * ld + k);
+    }
+}
+
+template <class MT, int N>
+__device__ __forceinline__ void storeN(MT* dst, const float* x)
+{
+    if constexpr (N == 8) store8<MT>(dst, x);
+    else store4<MT>(dst, x[0], x[1], x[2], x[3]);
+}
 
 // ------------------------------------------------------------------------------------------
 // variance side (summary and prep): wave w takes block w of the chunk; lane l the key-channel
@@ -422,13 +474,10 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
     float2 pk[SL];  // G_t k_t per channel of the pair: p_hat k (diagonal) or beta k (isotropic)
     auto replay = [&](auto mk_c) {
         constexpr bool MK = decltype(mk_c)::value;
-        float2 P = Gs;  // decay since the chunk start
 #pragma unroll
         for (int j = 0; j < SL; ++j) {
             const int t = SL * w + j;
             const TokIn x = tok_in<MK>(in, j, Lw);
-            P.x *= x.A.x;
-            P.y *= x.A.y;
             if constexpr (DIAG) {
                 const float mr = s_mr[t];
                 const float nn0 = fmaf(x.A.x * x.A.x, n0, x.W.x * d0);  // p_hat d
@@ -450,10 +499,6 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
                 d0 = fmaf(kn[j] * s_mr[t] * (1.f / (float)DK), nn, d0);
                 n0 = nn;
                 if ((j & 3) == 3) rescale2(n0, d0);
-            }
-            if (vact) {
-                st2<MT>(gKb + t * DK + ch, P.x * x.K.x, P.y * x.K.y);
-                st2<MT>(gQb + t * DK + ch, P.x * x.Q.x, P.y * x.Q.y);
             }
         }
     };
@@ -487,12 +532,11 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
             Q.y *= A.y;
         }
         if (vact) {
-            MT* r0 = gPt + (size_t)ch * C + SL * w;
-            MT* r1 = gPt + (size_t)(ch + 1) * C + SL * w;
+            constexpr int E = Frag<MT, C>::KF / 4;
 #pragma unroll
-            for (int e = 0; e < SL; e += 8) {
-                store8<MT>(r0 + e, px + e);
-                store8<MT>(r1 + e, py + e);
+            for (int e = 0; e < SL; e += E) {
+                storeN<MT, E>(gPt + frag_off<MT, C>(ch, SL * w + e), px + e);
+                storeN<MT, E>(gPt + frag_off<MT, C>(ch + 1, SL * w + e), py + e);
             }
             if (w == 0) {
                 float2 gc = make_float2(1.f, 1.f);
@@ -687,16 +731,28 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         }
     }
     __syncthreads();
+    copy_frag_order<MT, C, C, NTH>(gAq, Aqs, LDC, tid);
+    copy_frag_order<MT, C, C, NTH>(gLi, Lis, LDC, tid);
+    __syncthreads();
+
+    // ---- K_bar = gamma (.) k and Q_bar = gamma (.) q (decay since the chunk start) ---------
     {
-        constexpr int VE = 16 / (int)sizeof(MT), VPR = C / VE;
-        for (int idx = tid; idx < C * VPR; idx += NTH) {
-            const int row = idx / VPR, e = (idx % VPR) * VE;
-            *reinterpret_cast<uint4*>(gAq + row * C + e) =
-                *reinterpret_cast<const uint4*>(Aqs + row * LDC + e);
-            *reinterpret_cast<uint4*>(gLi + row * C + e) =
-                *reinterpret_cast<const uint4*>(Lis + row * LDC + e);
+        float2 P = Gs;
+#pragma unroll
+        for (int j = 0; j < SL; ++j) {
+            const TokIn x = mk ? tok_in<true>(in, j, Lw) : tok_in<false>(in, j, Lw);
+            P.x *= x.A.x;
+            P.y *= x.A.y;
+            if (vact) {
+                const int t = SL * w + j;
+                st2<MT>(Ka + t * LDK + ch, P.x * x.K.x, P.y * x.K.y);
+                st2<MT>(Qa + t * LDK + ch, P.x * x.Q.x, P.y * x.Q.y);
+            }
         }
     }
+    __syncthreads();
+    copy_frag_order<MT, C, DK, NTH>(gKb, Ka, LDK, tid);
+    copy_frag_order<MT, C, DK, NTH>(gQb, Qa, LDK, tid);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -720,7 +776,11 @@ struct WalkCfg {
     static constexpr size_t OFF_XT = al16((size_t)BV * LDK * sizeof(MT));      // X^T [BV][LDC]
     static constexpr size_t OFF_RT = OFF_XT + al16((size_t)BV * LDC * sizeof(MT));  // R^T
     static constexpr size_t OFF_O = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));   // O [C][LDO]
-    static constexpr size_t TOTAL = al16(OFF_O + (size_t)C * LDO * sizeof(TI));
+    static constexpr size_t OFF_V = OFF_O + al16((size_t)C * LDO * sizeof(TI));     // V [C][LDO]
+    static constexpr size_t TOTAL = al16(OFF_V + (size_t)C * LDO * sizeof(TI));
+    // V tile of a chunk in 16-byte pieces: VPC per row, NVP in all, VPT per thread
+    static constexpr int VPC = BV * (int)sizeof(TI) / 16, NVP = C * VPC;
+    static constexpr int VPT = (NVP + NTH - 1) / NTH;
 };
 
 struct WalkArgs {
@@ -751,6 +811,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     MT* XT = (MT*)(smem + CF::OFF_XT);
     MT* RT = (MT*)(smem + CF::OFF_RT);
     TI* Ost = (TI*)(smem + CF::OFF_O);
+    TI* Vt = (TI*)(smem + CF::OFF_V);
 
     // block -> (sequence-head slot, value tile): the NV tiles of one head get block indices
     // congruent modulo 8, so round-robin dispatch puts them on one XCD, where they share the L2
@@ -793,7 +854,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     const rsrc_t rv = make_rsrc(a.v, a.bytes_v);
     constexpr uint32_t es = sizeof(TI);
     const uint32_t rowv = (uint32_t)H * DV * es;
-    const uint32_t colv = ((uint32_t)h * DV + col0 + li) * es;
+    const uint32_t colv = ((uint32_t)h * DV + col0) * es;
     auto recp = [&](int m) -> const char* {
         const int mm = min(m, max(nch - 1, 0));
         return a.ops + ((size_t)(g0 + mm) * H + h) * Rec::BYTES;
@@ -801,50 +862,64 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     auto key_tile = [&](int p) { return min(CF::SHARE ? SPW * w / NNT + p : (SPW * w + p) / NNT,
                                             CF::NKT - 1); };
 
-    // operands of the next chunk, loaded one step ahead of their use
+    // operands of the next chunk, loaded one step ahead of their use (fragment order: one
+    // contiguous piece per lane)
     typename FK::V kf[NSK], qf[NSK];
     typename FC::V lf[NSC], af[NSC], pf[PPW][NSC];
     float4 gc[PPW];
-    typename Raw1<TI>::type vv[NNT][4];
+    uint4 vraw[CF::VPT];  // the chunk's V tile, 16 bytes per thread and piece
     auto load1 = [&](int m) {
         const char* rec = recp(m);
-        const MT* Kb = (const MT*)(rec + Rec::OFF_KB) + (16 * w + li) * DK;
-        const MT* Qb = (const MT*)(rec + Rec::OFF_QB) + (16 * w + li) * DK;
+        const MT* Kb = (const MT*)(rec + Rec::OFF_KB);
+        const MT* Qb = (const MT*)(rec + Rec::OFF_QB);
 #pragma unroll
         for (int s = 0; s < NSK; ++s) {
-            kf[s] = FK::ld(Kb + FK::KF * s + (FK::KF / 4) * lg);
-            qf[s] = FK::ld(Qb + FK::KF * s + (FK::KF / 4) * lg);
+            kf[s] = FK::ld(frag_piece<MT, DK>(Kb, w, s, lane));
+            qf[s] = FK::ld(frag_piece<MT, DK>(Qb, w, s, lane));
         }
         const uint32_t c0 = (uint32_t)(t0 + min(m, max(nch - 1, 0)) * C);
 #pragma unroll
-        for (int nt = 0; nt < NNT; ++nt)
+        for (int u = 0; u < CF::VPT; ++u) {
+            const int p = tid + NTH * u;
+            const uint32_t r = (uint32_t)(min(p, CF::NVP - 1) / CF::VPC);
+            const uint32_t cb = (uint32_t)(p % CF::VPC) * 16;
+            vraw[u] = __builtin_bit_cast(
+                uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)((c0 + r) * rowv + colv + cb),
+                                                             0, 0));
+        }
+    };
+    auto store_v = [&]() {  // the V tile to LDS
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                vv[nt][rr] = Raw1<TI>::load(
-                    rv, (c0 + (uint32_t)(16 * w + 4 * lg + rr)) * rowv + colv + 16 * nt * es);
+        for (int u = 0; u < CF::VPT; ++u) {
+            const int p = tid + NTH * u;
+            if (p < CF::NVP)
+                *reinterpret_cast<uint4*>(Vt + (p / CF::VPC) * LDO + (p % CF::VPC) * (16 / es)) =
+                    vraw[u];
+        }
     };
     auto load2 = [&](int m) {
-        const MT* Li = (const MT*)(recp(m) + Rec::OFF_LI) + (16 * w + li) * C;
+        const MT* Li = (const MT*)(recp(m) + Rec::OFF_LI);
 #pragma unroll
-        for (int s = 0; s < NSC; ++s) lf[s] = FC::ld(Li + FC::KF * s + (FC::KF / 4) * lg);
+        for (int s = 0; s < NSC; ++s) lf[s] = FC::ld(frag_piece<MT, C>(Li, w, s, lane));
     };
     auto load3 = [&](int m) {
         const char* rec = recp(m);
-        const MT* Aq = (const MT*)(rec + Rec::OFF_AQ) + (16 * w + li) * C;
+        const MT* Aq = (const MT*)(rec + Rec::OFF_AQ);
 #pragma unroll
-        for (int s = 0; s < NSC; ++s) af[s] = FC::ld(Aq + FC::KF * s + (FC::KF / 4) * lg);
+        for (int s = 0; s < NSC; ++s) af[s] = FC::ld(frag_piece<MT, C>(Aq, w, s, lane));
 #pragma unroll
         for (int p = 0; p < PPW; ++p) {
             const int ik = key_tile(p);
-            const MT* Pt = (const MT*)(rec + Rec::OFF_PT) + (16 * ik + li) * C;
+            const MT* Pt = (const MT*)(rec + Rec::OFF_PT);
 #pragma unroll
-            for (int s = 0; s < NSC; ++s) pf[p][s] = FC::ld(Pt + FC::KF * s + (FC::KF / 4) * lg);
+            for (int s = 0; s < NSC; ++s) pf[p][s] = FC::ld(frag_piece<MT, C>(Pt, ik, s, lane));
             gc[p] = *reinterpret_cast<const float4*>((const float*)(rec + Rec::OFF_GC) +
                                                      16 * ik + 4 * lg);
         }
     };
     if (nch > 0) {
         load1(0);
+        store_v();
         load2(0);
         load3(0);
     }
@@ -884,7 +959,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
 #pragma unroll
                 for (int rr = 0; rr < 4; ++rr) {
                     const int t = 16 * w + 4 * lg + rr;
-                    xv[rr] = (t < L ? Raw1<TI>::f32(vv[nt][rr]) : 0.f) - xacc[rr];
+                    xv[rr] = (t < L ? to_f32(Vt[t * LDO + 16 * nt + li]) : 0.f) - xacc[rr];
                 }
                 store4<MT>(XT + (16 * nt + li) * LDC + 16 * w + 4 * lg, xv[0], xv[1], xv[2],
                            xv[3]);
@@ -911,6 +986,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
         }
         load2(m + 1);
         __syncthreads();
+        store_v();  // V of the next chunk: this chunk's V was last read before the last barrier
         // ---- O = scale (Q_bar S + A_qk R); S <- gamma_C (.) S + P_tail^T R --------------------
         {
             typename FC::V rf[NNT][NSC];
@@ -932,13 +1008,17 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
             for (int j = 0; j < SPW; ++j) {
                 const int x = SPW * w + j;
                 if (x < NST) {
-                    const int ik = x / NNT, nt = x % NNT, p = CF::SHARE ? j / NNT : j;
+                    // with SHARE, x % NNT = j % NNT is known at compile time
+                    const int ik = x / NNT, nt = CF::SHARE ? j % NNT : x % NNT;
+                    const int p = CF::SHARE ? j / NNT : j;
                     Sacc[j][0] *= gc[p].x;
                     Sacc[j][1] *= gc[p].y;
                     Sacc[j][2] *= gc[p].z;
                     Sacc[j][3] *= gc[p].w;
+                    static_assert(NNT <= 2, "value tiles of at most 32 columns");
 #pragma unroll
-                    for (int s = 0; s < NSC; ++s) Sacc[j] = FC::mma(Sacc[j], pf[p][s], rf[nt][s]);
+                    for (int s = 0; s < NSC; ++s)
+                        Sacc[j] = FC::mma(Sacc[j], pf[p][s], nt == 0 ? rf[0][s] : rf[NNT - 1][s]);
                     store4<MT>(SmT + (16 * nt + li) * LDK + 16 * ik + 4 * lg, Sacc[j][0],
                                Sacc[j][1], Sacc[j][2], Sacc[j][3]);
                 }
