@@ -778,9 +778,10 @@ struct WalkCfg {
     static constexpr size_t OFF_O = OFF_RT + al16((size_t)BV * LDC * sizeof(MT));   // O [C][LDO]
     static constexpr size_t OFF_V = OFF_O + al16((size_t)C * LDO * sizeof(TI));     // V [C][LDO]
     static constexpr size_t TOTAL = al16(OFF_V + (size_t)C * LDO * sizeof(TI));
-    // V tile of a chunk in 16-byte pieces: VPC per row, NVP in all, VPT per thread
-    static constexpr int VPC = BV * (int)sizeof(TI) / 16, NVP = C * VPC;
-    static constexpr int VPT = (NVP + NTH - 1) / NTH;
+    // V tile of a chunk in 16-byte pieces: VPC per row; wave w moves the 16 rows of its own row
+    // block (16 VPC pieces), VPW per lane
+    static constexpr int VPC = BV * (int)sizeof(TI) / 16;
+    static constexpr int VPW = (16 * VPC + 63) / 64;
 };
 
 struct WalkArgs {
@@ -867,7 +868,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     typename FK::V kf[NSK], qf[NSK];
     typename FC::V lf[NSC], af[NSC], pf[PPW][NSC];
     float4 gc[PPW];
-    uint4 vraw[CF::VPT];  // the chunk's V tile, 16 bytes per thread and piece
+    uint4 vraw[CF::VPW];  // the wave's rows of the chunk's V tile, 16 bytes per piece
     auto load1 = [&](int m) {
         const char* rec = recp(m);
         const MT* Kb = (const MT*)(rec + Rec::OFF_KB);
@@ -879,22 +880,24 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
         }
         const uint32_t c0 = (uint32_t)(t0 + min(m, max(nch - 1, 0)) * C);
 #pragma unroll
-        for (int u = 0; u < CF::VPT; ++u) {
-            const int p = tid + NTH * u;
-            const uint32_t r = (uint32_t)(min(p, CF::NVP - 1) / CF::VPC);
-            const uint32_t cb = (uint32_t)(p % CF::VPC) * 16;
+        for (int u = 0; u < CF::VPW; ++u) {
+            const int q = min(lane + 64 * u, 16 * CF::VPC - 1);
+            const uint32_t r = (uint32_t)(16 * w + q / CF::VPC);
+            const uint32_t cb = (uint32_t)(q % CF::VPC) * 16;
             vraw[u] = __builtin_bit_cast(
                 uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, (int)((c0 + r) * rowv + colv + cb),
                                                              0, 0));
         }
     };
-    auto store_v = [&]() {  // the V tile to LDS
+    // the wave's V rows to LDS: every wave reads only the rows it writes, and LDS operations of
+    // one wave run in order, so no barrier is needed between this and their use
+    auto store_v = [&]() {
 #pragma unroll
-        for (int u = 0; u < CF::VPT; ++u) {
-            const int p = tid + NTH * u;
-            if (p < CF::NVP)
-                *reinterpret_cast<uint4*>(Vt + (p / CF::VPC) * LDO + (p % CF::VPC) * (16 / es)) =
-                    vraw[u];
+        for (int u = 0; u < CF::VPW; ++u) {
+            const int q = lane + 64 * u;
+            if (q < 16 * CF::VPC)
+                *reinterpret_cast<uint4*>(Vt + (16 * w + q / CF::VPC) * LDO +
+                                          (q % CF::VPC) * (16 / es)) = vraw[u];
         }
     };
     auto load2 = [&](int m) {
@@ -919,7 +922,6 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
     };
     if (nch > 0) {
         load1(0);
-        store_v();
         load2(0);
         load3(0);
     }
@@ -937,6 +939,7 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     *reinterpret_cast<const uint4*>(Ost + t * LDO + e);
             }
         }
+        store_v();
         // ---- X = V - K_bar S (to LDS, transposed); Q_bar S kept for the output --------------
         floatx4 Oacc[NNT];
         {
@@ -955,12 +958,15 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     xacc = FK::mma(xacc, kf[s], sf[nt][s]);
                     Oacc[nt] = FK::mma(Oacc[nt], qf[s], sf[nt][s]);
                 }
-                float xv[4];
+                // rows past the end of the sequence hold another sequence's V or stale data:
+                // every row is read (no divergent reads), then masked
+                float vr[4], xv[4];
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int t = 16 * w + 4 * lg + rr;
-                    xv[rr] = (t < L ? to_f32(Vt[t * LDO + 16 * nt + li]) : 0.f) - xacc[rr];
-                }
+                for (int rr = 0; rr < 4; ++rr)
+                    vr[rr] = to_f32(Vt[(16 * w + 4 * lg + rr) * LDO + 16 * nt + li]);
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    xv[rr] = (16 * w + 4 * lg + rr < L ? vr[rr] : 0.f) - xacc[rr];
                 store4<MT>(XT + (16 * nt + li) * LDC + 16 * w + 4 * lg, xv[0], xv[1], xv[2],
                            xv[3]);
             }
@@ -986,7 +992,6 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
         }
         load2(m + 1);
         __syncthreads();
-        store_v();  // V of the next chunk: this chunk's V was last read before the last barrier
         // ---- O = scale (Q_bar S + A_qk R); S <- gamma_C (.) S + P_tail^T R --------------------
         {
             typename FC::V rf[NNT][NSC];
