@@ -416,19 +416,50 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         s_r[tid] = ok ? rv : 1.f;
         s_mr[tid] = ok ? a.in.mu / rv : 0.f;
     }
-    SegIn<TI, CF, true> in;
-    load_seg(in, sr, (uint32_t)(c0 + SL * w));
+    const int Lw = c1 - (c0 + SL * w);  // tokens of this block in the sequence (may be <= 0)
+    // the block's tokens in float32, unpacked once
+    float2 Kf[SL], Qf[SL], Af[SL], Wf[SL];
+    {
+        SegIn<TI, CF, true> in;
+        load_seg(in, sr, (uint32_t)(c0 + SL * w));
+#pragma unroll
+        for (int j = 0; j < SL; ++j) {
+            const TokIn x = tok_in<true>(in, j, Lw);
+            Kf[j] = x.K;
+            Qf[j] = x.Q;
+            Af[j] = x.A;
+            Wf[j] = x.W;
+        }
+    }
     __syncthreads();
 
-    // ---- the block's Moebius and decay products ---------------------------------------------
-    const int Lw = c1 - (c0 + SL * w);  // tokens of this block in the sequence (may be <= 0)
-    const bool mk = Lw < SL;
-    float kn[DIAG ? 1 : SL], ka[DIAG ? 1 : SL];
+    // ---- the block's Moebius and decay products (eq. chunk-gain-summary) ----------------------
+    float kn[DIAG ? 1 : SL], ka[DIAG ? 1 : SL];  // isotropic: ||k||^2 and mean alpha^2
     {
-        float m0[4], m1[4];
-        float2 gs;
-        if (mk) block_summary<true>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka);
-        else block_summary<false>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka);
+        float m0[4] = {1.f, 0.f, 0.f, 1.f}, m1[4] = {1.f, 0.f, 0.f, 1.f};
+        float2 gs = make_float2(1.f, 1.f);
+#pragma unroll
+        for (int j = 0; j < SL; ++j) {
+            const float mr = s_mr[SL * w + j];
+            if constexpr (DIAG) {
+                mob_left(m0, Af[j].x * Af[j].x, Wf[j].x, Kf[j].x * Kf[j].x * mr);
+                mob_left(m1, Af[j].y * Af[j].y, Wf[j].y, Kf[j].y * Kf[j].y * mr);
+            } else {
+                kn[j] = wave_sum(vact ? fmaf(Kf[j].x, Kf[j].x, Kf[j].y * Kf[j].y) : 0.f);
+                if constexpr (CF::APC)
+                    ka[j] = wave_sum(vact ? fmaf(Af[j].x, Af[j].x, Af[j].y * Af[j].y) : 0.f) *
+                            (1.f / (float)DK);
+                else
+                    ka[j] = Af[j].x * Af[j].x;
+                mob_left(m0, ka[j], Wf[j].x, kn[j] * mr * (1.f / (float)DK));
+            }
+            gs.x *= Af[j].x;
+            gs.y *= Af[j].y;
+            if ((j & 3) == 3) {
+                rescale4(m0);
+                if constexpr (DIAG) rescale4(m1);
+            }
+        }
         if (vact) {
             if constexpr (DIAG) {
                 segA[w * DK + ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
@@ -470,40 +501,35 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         }
     }
 
-    // ---- replay: p_hat (or beta) per token; K_bar, Q_bar to the record ----------------------
-    float2 pk[SL];  // G_t k_t per channel of the pair: p_hat k (diagonal) or beta k (isotropic)
-    auto replay = [&](auto mk_c) {
-        constexpr bool MK = decltype(mk_c)::value;
+    // ---- replay (eqs. chunk-gain-local-prefix, chunk-gain-emission): G_t k_t per channel of the
+    // pair, G = p_hat (diagonal) or beta (isotropic) ------------------------------------------
+    float2 pk[SL];
 #pragma unroll
-        for (int j = 0; j < SL; ++j) {
-            const int t = SL * w + j;
-            const TokIn x = tok_in<MK>(in, j, Lw);
-            if constexpr (DIAG) {
-                const float mr = s_mr[t];
-                const float nn0 = fmaf(x.A.x * x.A.x, n0, x.W.x * d0);  // p_hat d
-                const float nn1 = fmaf(x.A.y * x.A.y, n1, x.W.y * d1);
-                pk[j] = make_float2(nn0 * x.K.x * __builtin_amdgcn_rcpf(d0),
-                                    nn1 * x.K.y * __builtin_amdgcn_rcpf(d1));
-                d0 = fmaf(x.K.x * x.K.x * mr, nn0, d0);
-                d1 = fmaf(x.K.y * x.K.y * mr, nn1, d1);
-                n0 = nn0;
-                n1 = nn1;
-                if ((j & 3) == 3) {
-                    rescale2(n0, d0);
-                    rescale2(n1, d1);
-                }
-            } else {
-                const float nn = fmaf(ka[j], n0, x.W.x * d0);  // b_hat d
-                const float beta = nn / fmaf(d0, s_r[t], nn * kn[j]);
-                pk[j] = make_float2(beta * x.K.x, beta * x.K.y);
-                d0 = fmaf(kn[j] * s_mr[t] * (1.f / (float)DK), nn, d0);
-                n0 = nn;
-                if ((j & 3) == 3) rescale2(n0, d0);
+    for (int j = 0; j < SL; ++j) {
+        const int t = SL * w + j;
+        if constexpr (DIAG) {
+            const float mr = s_mr[t];
+            const float nn0 = fmaf(Af[j].x * Af[j].x, n0, Wf[j].x * d0);  // p_hat d
+            const float nn1 = fmaf(Af[j].y * Af[j].y, n1, Wf[j].y * d1);
+            pk[j] = make_float2(nn0 * Kf[j].x * __builtin_amdgcn_rcpf(d0),
+                                nn1 * Kf[j].y * __builtin_amdgcn_rcpf(d1));
+            d0 = fmaf(Kf[j].x * Kf[j].x * mr, nn0, d0);
+            d1 = fmaf(Kf[j].y * Kf[j].y * mr, nn1, d1);
+            n0 = nn0;
+            n1 = nn1;
+            if ((j & 3) == 3) {
+                rescale2(n0, d0);
+                rescale2(n1, d1);
             }
+        } else {
+            const float nn = fmaf(ka[j], n0, Wf[j].x * d0);  // b_hat d
+            const float beta = nn / fmaf(d0, s_r[t], nn * kn[j]);
+            pk[j] = make_float2(beta * Kf[j].x, beta * Kf[j].y);
+            d0 = fmaf(kn[j] * s_mr[t] * (1.f / (float)DK), nn, d0);
+            n0 = nn;
+            if ((j & 3) == 3) rescale2(n0, d0);
         }
-    };
-    if (mk) replay(std::true_type());
-    else replay(std::false_type());
+    }
     if (w == NW - 1 && last && a.P_T) {  // the final variances n / d
         if constexpr (DIAG) {
             if (vact)
@@ -514,12 +540,7 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         }
     }
 
-    // decay factor of token j (1 past the end of the sequence)
-    auto alpha_of = [&](int j) -> float2 {
-        return mk ? tok_in<true>(in, j, Lw).A : tok_in<false>(in, j, Lw).A;
-    };
-
-    // ---- P_tail^T = (gamma_C / gamma_s) G_s k_s; gamma_C ------------------------------------
+    // ---- P_tail^T = (gamma_C / gamma_s) G_s k_s (record, fragment order); gamma_C -----------
     {
         float px[SL], py[SL];
         float2 Q = Gt;
@@ -527,9 +548,8 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         for (int j = SL - 1; j >= 0; --j) {
             px[j] = pk[j].x * Q.x;
             py[j] = pk[j].y * Q.y;
-            const float2 A = alpha_of(j);
-            Q.x *= A.x;
-            Q.y *= A.y;
+            Q.x *= Af[j].x;
+            Q.y *= Af[j].y;
         }
         if (vact) {
             constexpr int E = Frag<MT, C>::KF / 4;
@@ -554,33 +574,27 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
     // ---- diagonal blocks: operands referenced to the block midpoint ---------------------------
     // F_t = prod_{8 <= j <= t} alpha_j (t >= 8), 1 / prod_{t < j <= 7} alpha_j (t < 8);
     // K_t F_t and G_s k_s / F_s give F_t / F_s = prod_{s < j <= t} alpha_j.
-    {
+    if (vact) {
         float2 b = make_float2(1.f, 1.f);
 #pragma unroll
         for (int j = SL / 2 - 1; j >= 0; --j) {
-            const TokIn x = mk ? tok_in<true>(in, j, Lw) : tok_in<false>(in, j, Lw);
+            const int t = SL * w + j;
             const float fx = sat_rcp(b.x), fy = sat_rcp(b.y);
-            if (vact) {
-                const int t = SL * w + j;
-                st2<MT>(Ka + t * LDK + ch, x.K.x * fx, x.K.y * fy);
-                st2<MT>(Qa + t * LDK + ch, x.Q.x * fx, x.Q.y * fy);
-                st2<MT>(Pa + t * LDK + ch, pk[j].x * b.x, pk[j].y * b.y);
-            }
-            b.x *= x.A.x;
-            b.y *= x.A.y;
+            st2<MT>(Ka + t * LDK + ch, Kf[j].x * fx, Kf[j].y * fy);
+            st2<MT>(Qa + t * LDK + ch, Qf[j].x * fx, Qf[j].y * fy);
+            st2<MT>(Pa + t * LDK + ch, pk[j].x * b.x, pk[j].y * b.y);
+            b.x *= Af[j].x;
+            b.y *= Af[j].y;
         }
         float2 f = make_float2(1.f, 1.f);
 #pragma unroll
         for (int j = SL / 2; j < SL; ++j) {
-            const TokIn x = mk ? tok_in<true>(in, j, Lw) : tok_in<false>(in, j, Lw);
-            f.x *= x.A.x;
-            f.y *= x.A.y;
-            if (vact) {
-                const int t = SL * w + j;
-                st2<MT>(Ka + t * LDK + ch, x.K.x * f.x, x.K.y * f.y);
-                st2<MT>(Qa + t * LDK + ch, x.Q.x * f.x, x.Q.y * f.y);
-                st2<MT>(Pa + t * LDK + ch, pk[j].x * sat_rcp(f.x), pk[j].y * sat_rcp(f.y));
-            }
+            const int t = SL * w + j;
+            f.x *= Af[j].x;
+            f.y *= Af[j].y;
+            st2<MT>(Ka + t * LDK + ch, Kf[j].x * f.x, Kf[j].y * f.y);
+            st2<MT>(Qa + t * LDK + ch, Qf[j].x * f.x, Qf[j].y * f.y);
+            st2<MT>(Pa + t * LDK + ch, pk[j].x * sat_rcp(f.x), pk[j].y * sat_rcp(f.y));
         }
     }
     __syncthreads();
@@ -605,28 +619,24 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
 
     // ---- blocks off the diagonal: rows referenced to their block's start, columns to their
     // block's end, the decay of the blocks between applied to the column side -----------------
-    {
+    if (vact) {
         float2 P = make_float2(1.f, 1.f);
 #pragma unroll
         for (int j = 0; j < SL; ++j) {
-            const TokIn x = mk ? tok_in<true>(in, j, Lw) : tok_in<false>(in, j, Lw);
-            P.x *= x.A.x;
-            P.y *= x.A.y;
-            if (vact) {
-                const int t = SL * w + j;
-                st2<MT>(Ka + t * LDK + ch, x.K.x * P.x, x.K.y * P.y);
-                st2<MT>(Qa + t * LDK + ch, x.Q.x * P.x, x.Q.y * P.y);
-            }
+            const int t = SL * w + j;
+            P.x *= Af[j].x;
+            P.y *= Af[j].y;
+            st2<MT>(Ka + t * LDK + ch, Kf[j].x * P.x, Kf[j].y * P.y);
+            st2<MT>(Qa + t * LDK + ch, Qf[j].x * P.x, Qf[j].y * P.y);
         }
         float2 Q = make_float2(1.f, 1.f);
 #pragma unroll
         for (int j = SL - 1; j >= 0; --j) {
-            if (vact) st2<MT>(Pa + (SL * w + j) * LDK + ch, pk[j].x * Q.x, pk[j].y * Q.y);
-            const float2 A = alpha_of(j);
-            Q.x *= A.x;
-            Q.y *= A.y;
+            st2<MT>(Pa + (SL * w + j) * LDK + ch, pk[j].x * Q.x, pk[j].y * Q.y);
+            Q.x *= Af[j].x;
+            Q.y *= Af[j].y;
         }
-        if (NB == 4 && w == 0 && vact)  // decay of blocks 1 and 2 (pair (3, 0))
+        if (NB == 4 && w == 0)  // decay of blocks 1 and 2 (pair (3, 0))
             *reinterpret_cast<float2*>(rho + ch) =
                 make_float2(segG[DK + ch] * segG[2 * DK + ch],
                             segG[DK + ch + 1] * segG[2 * DK + ch + 1]);
@@ -687,7 +697,7 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
 
     // ---- L^-1 by columns of blocks (float32 MFMA): wave c takes block column c,
     // Li_bc = -A_bb sum_{c <= j < b} L_bj Li_jc, Li_cc = A_cc. A_qk and L^-1 are staged in the
-    // operand area (now free) and written out as whole rows --------------------------------
+    // operand area (now free) and written out in fragment order -------------------------------
     MT* Aqs = Ka;  // [C][LDC]
     MT* Lis = Qa;  // [C][LDC]
     {
@@ -735,19 +745,17 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
     copy_frag_order<MT, C, C, NTH>(gLi, Lis, LDC, tid);
     __syncthreads();
 
-    // ---- K_bar = gamma (.) k and Q_bar = gamma (.) q (decay since the chunk start) ---------
-    {
+    // ---- K_bar = gamma (.) k and Q_bar = gamma (.) q (decay since the chunk start), staged in
+    // the operand area and written out in fragment order --------------------------------------
+    if (vact) {
         float2 P = Gs;
 #pragma unroll
         for (int j = 0; j < SL; ++j) {
-            const TokIn x = mk ? tok_in<true>(in, j, Lw) : tok_in<false>(in, j, Lw);
-            P.x *= x.A.x;
-            P.y *= x.A.y;
-            if (vact) {
-                const int t = SL * w + j;
-                st2<MT>(Ka + t * LDK + ch, P.x * x.K.x, P.y * x.K.y);
-                st2<MT>(Qa + t * LDK + ch, P.x * x.Q.x, P.y * x.Q.y);
-            }
+            const int t = SL * w + j;
+            P.x *= Af[j].x;
+            P.y *= Af[j].y;
+            st2<MT>(Ka + t * LDK + ch, Kf[j].x * P.x, Kf[j].y * P.y);
+            st2<MT>(Qa + t * LDK + ch, Qf[j].x * P.x, Qf[j].y * P.y);
         }
     }
     __syncthreads();
