@@ -25,7 +25,16 @@
  *   than 2 GiB each (KDN_ERR_UNSUPPORTED otherwise).
  * - Device-side contract (not checked on the host, which never reads device data):
  *   cu_seqlens non-decreasing with cu_seqlens[0] == 0 and cu_seqlens[N] == T; 0 < alpha <= 1;
- *   omega >= 0; r > 0. Kernels never write outside the caller's buffers even when it is broken.
+ *   omega >= 0; r > 0. Kernels never write outside the caller's buffers even when it is broken:
+ *   every sequence span is clamped to [0, B*T] on the device and the number of chunks to the
+ *   workspace the query sized (results for such a batch are unspecified, the writes in bounds).
+ * - Gates: the forward is exact (to rounding) for every 0 < alpha <= 1 whose product over any 8
+ *   consecutive tokens of an aligned 16-token block stays above 2^-126 per channel (every
+ *   alpha >= 2^-15 ~ 3.1e-5 suffices): decay ratios inside a chunk are referenced to block
+ *   starts, ends and midpoints, never to a factor above one elsewhere. Below that floor the
+ *   midpoint factors saturate at 2^126: outputs, states and variances stay finite, and the
+ *   intra-block products of the affected channels lose accuracy. Decode and the gain scan have
+ *   no floor.
  * - Errors are returned, never printed or raised; kdn_last_error() gives detail for the calling
  *   thread's most recent non-OK status.
  */
@@ -63,10 +72,12 @@ typedef enum { KDN_F32 = 0, KDN_BF16 = 1 } kdn_dtype_t;
  *   q, k, alpha, omega: [B,T,H,dk]; v, o: [B,T,H,dv]; r: [B,T,H]   (dtype)
  *   S0, S_T: [N,H,dk,dv] float32;  P0, P_T: [N,H,dk] float32
  *   mu > 0 (the paper uses mu = dk); scale > 0 (the paper uses dk^-1/2).
- *   chunk: memory-chunk length (16, 32 or 64), or 0 for the library's choice. Results do not
- *   depend on it beyond rounding.
+ *   chunk: memory-chunk length, 64 or 0 (= 64); anything else is KDN_ERR_UNSUPPORTED.
  *   workspace: device scratch of at least kdn_forward_workspace_bytes(...) bytes
- *   (KDN_ERR_WORKSPACE when smaller or NULL).
+ *   (KDN_ERR_WORKSPACE when smaller or NULL). Four kernels run on `stream` in order: chunk
+ *   summaries of the variance chain, a log-depth carry scan across chunks (eq.
+ *   chunk-gain-carry), a per-chunk prep that writes each chunk's S-independent operands to the
+ *   workspace, and the walk that carries S through the chunks.
  */
 kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const void* alpha,
                               const void* omega, const void* r, const float* S0, const float* P0,
@@ -95,12 +106,16 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
 /*
  * Device scratch (bytes) that kdn_forward_diag (variant 0) / kdn_forward_iso (variant 1) need
  * for these sizes; packed != 0 for a packed batch (cu_seqlens given), chunk as passed to the
- * forward (0 = the library's choice). Returns 0 for arguments the forward rejects. The scratch
- * holds the order in which the sequences of a packed batch are walked (longest first) and, for
- * an in-place variance update (P_T == P0), a copy of P0 taken before the walk starts. It is
- * small (at most 4 (N + 1) + 4 N H dk bytes, rounded up to 256), needs no initialisation and
- * is dead once the forward's work on the stream has finished; two forwards in flight at once
- * need two.
+ * forward. Returns 0 for arguments the forward rejects. With M chunks at most
+ * (M = N ceil(T / 64) for a fixed-length batch, M = T / 64 + N for a packed one), a variance
+ * channel count c (dk diagonal, 1 isotropic) and e the input element size, it holds, each
+ * part rounded up to 256 bytes:
+ *   packed only: the chunk-offset table (4 (N + 1)) and the walk order (4 N);
+ *   the chunk summaries (16 M H c) and the carries into every chunk (8 M H c);
+ *   one record per (chunk, head) of M H records, each 3 64 dk e + 2 64 64 e + 4 dk bytes
+ *   rounded up to 256 (K_bar, Q_bar, P_tail^T, L^-1, A_qk, gamma_C),
+ * about 1 KB per token and head for bf16 at dk = 128. It needs no initialisation and is dead
+ * once the forward's work on the stream has finished; two forwards in flight at once need two.
  */
 size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
                                    int32_t dk, int32_t dv, kdn_dtype_t dtype, int32_t packed,

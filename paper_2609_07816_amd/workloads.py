@@ -125,15 +125,36 @@ class KdnInputs:
         return self.B * self.T
 
 
+def _law(rng: np.random.Generator, shape, law, default):
+    """Values of one tensor: ``default(rng, shape)`` unless ``law`` overrides it with
+    ("uniform", lo, hi), ("const", c) or ("spikes", base, low, frac): ``base`` everywhere except
+    a random fraction ``frac`` of the entries, which take the value ``low``."""
+    if law is None:
+        return default(rng, shape)
+    kind = law[0]
+    if kind == "uniform":
+        return rng.uniform(law[1], law[2], shape)
+    if kind == "const":
+        return np.full(shape, float(law[1]))
+    if kind == "spikes":
+        x = np.full(shape, float(law[1]))
+        x[rng.random(shape) < law[3]] = float(law[2])
+        return x
+    raise ValueError(f"unknown law {law!r}")
+
+
 def draw_inputs(variant: str, dtype: str, B: int, T: int, H: int, dk: int, dv: int, *,
                 seed: int, stream: int = 0, alpha_per_channel: bool = True,
                 lengths: Optional[Sequence[int]] = None, random_state: bool = False,
-                mu: Optional[float] = None, scale: Optional[float] = None) -> KdnInputs:
+                mu: Optional[float] = None, scale: Optional[float] = None,
+                alpha_law=None, omega_law=None, r_law=None) -> KdnInputs:
     """Draw one batch.
 
     ``variant`` is "diag" or "iso". With ``lengths`` the batch is packed (B must be 1 and T the
     total length). ``random_state`` draws S0 ~ N(0, 0.02^2) and P0 ~ U(0.1, 1) per sequence;
-    otherwise both are None (the method's defaults S0 = 0 and P0 = 1 apply).
+    otherwise both are None (the method's defaults S0 = 0 and P0 = 1 apply). ``alpha_law``,
+    ``omega_law`` and ``r_law`` replace the default laws of the gates and noise terms (see
+    ``_law``; used by the stress tests: small or unit gates, zero process noise, tiny r).
     """
     if variant not in ("diag", "iso"):
         raise ValueError(variant)
@@ -151,13 +172,13 @@ def draw_inputs(variant: str, dtype: str, B: int, T: int, H: int, dk: int, dv: i
     st["k"] = round_to(_unit_rows(_rng(seed, stream, SID_K).standard_normal((B, T, H, dk))), dtype)
     st["v"] = round_to(_rng(seed, stream, SID_V).standard_normal((B, T, H, dv)), dtype)
     ashape = (B, T, H, dk) if (variant == "diag" or alpha_per_channel) else (B, T, H)
-    st["alpha"] = round_to(_sigmoid(_rng(seed, stream, SID_ALPHA).standard_normal(ashape) + 2.0),
-                           dtype)
+    st["alpha"] = round_to(_law(_rng(seed, stream, SID_ALPHA), ashape, alpha_law,
+                                lambda g, sh: _sigmoid(g.standard_normal(sh) + 2.0)), dtype)
     oshape = (B, T, H, dk) if variant == "diag" else (B, T, H)
-    st["omega"] = round_to(_softplus(_rng(seed, stream, SID_OMEGA).standard_normal(oshape)) + 1e-3,
-                           dtype)
-    st["r"] = round_to(_softplus(_rng(seed, stream, SID_R).standard_normal((B, T, H))) + 1e-3,
-                       dtype)
+    st["omega"] = round_to(_law(_rng(seed, stream, SID_OMEGA), oshape, omega_law,
+                                lambda g, sh: _softplus(g.standard_normal(sh)) + 1e-3), dtype)
+    st["r"] = round_to(_law(_rng(seed, stream, SID_R), (B, T, H), r_law,
+                            lambda g, sh: _softplus(g.standard_normal(sh)) + 1e-3), dtype)
     S0 = P0 = None
     if random_state:
         S0 = (0.02 * _rng(seed, stream, SID_S0).standard_normal((N, H, dk, dv))).astype(np.float32)

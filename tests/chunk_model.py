@@ -71,3 +71,89 @@ def chunk_forward_lsolve(q, k, v, alpha, gainvec, diag, S0, C, scale):
         O[sl] = Qb @ S + np.tril(Qb @ Pb.T) @ R
         S = gamma[-1][:, None] * (S + Pb.T @ R)
     return O, S
+
+
+# ---------------------------------------------------------------------------------------------
+# float32 model of how the kernels form the intra-chunk products
+# ---------------------------------------------------------------------------------------------
+
+def intra_chunk_exact(k, q, alpha, G):
+    """Exact (float64, per pair) intra-chunk products of one chunk:
+    M_ts = sum_i k_ti (prod_{s < j <= t} alpha_ji) G_si k_si and M^q with q in place of k, for
+    s <= t (zero above the diagonal). k, q, alpha, G: [C, dk]."""
+    C = k.shape[0]
+    M, Mq = np.zeros((C, C)), np.zeros((C, C))
+    for t in range(C):
+        for s in range(t + 1):
+            ratio = np.prod(alpha[s + 1:t + 1], axis=0)  # empty product = 1
+            w = ratio * G[s] * k[s]
+            M[t, s] = np.dot(k[t], w)
+            Mq[t, s] = np.dot(q[t], w)
+    return M, Mq
+
+
+def intra_chunk_f32(k, q, alpha, G, scheme):
+    """The same products as the GPU forms them, every operand and product in float32.
+
+    scheme "chunk_start": gamma_t = prod_{j <= t} alpha_j from the chunk start, K_bar = gamma k and
+    P_bar = G k / gamma (one factorisation for the whole chunk).
+    scheme "blocks": 16-token blocks; inside a diagonal block both sides are referenced to its
+    midpoint, F_t = prod_{8 <= j <= t} alpha_j or 1 / prod_{t < j <= 7} alpha_j (reciprocals
+    saturated at 2^126); for a pair of distinct blocks (b > c) the rows are referenced to the
+    start of block b, the columns to the end of block c, and the decay of the blocks between
+    them scales the columns."""
+    f = np.float32
+    k, q, alpha, G = (np.asarray(x, dtype=f) for x in (k, q, alpha, G))
+    C, dk = k.shape
+    M, Mq = np.zeros((C, C), f), np.zeros((C, C), f)
+    with np.errstate(over="ignore", invalid="ignore", divide="ignore", under="ignore"):
+        if scheme == "chunk_start":
+            gam = np.cumprod(alpha, axis=0, dtype=f)
+            Kb, Qb, Pb = gam * k, gam * q, (G * k) / gam
+            M, Mq = np.tril(Kb @ Pb.T), np.tril(Qb @ Pb.T)
+            return M, Mq
+        assert scheme == "blocks" and C % 16 == 0
+        sat = lambda x: np.minimum(f(1) / np.maximum(x, f(2.0 ** -126)), f(2.0 ** 126))
+        nb = C // 16
+        blk = [slice(16 * b, 16 * b + 16) for b in range(nb)]
+        for b in range(nb):
+            a = alpha[blk[b]]
+            F = np.ones((16, dk), f)
+            acc = np.ones(dk, f)
+            for j in range(7, -1, -1):          # t < 8: 1 / prod_{t < j <= 7} alpha
+                F[j] = sat(acc)
+                acc = acc * a[j]
+            Pm = np.ones((16, dk), f)
+            acc = np.ones(dk, f)
+            for j in range(7, -1, -1):          # column side, t < 8: prod_{t < j <= 7} alpha
+                Pm[j] = acc
+                acc = acc * a[j]
+            acc = np.ones(dk, f)
+            for j in range(8, 16):              # t >= 8: prod_{8 <= j <= t} alpha
+                acc = acc * a[j]
+                F[j] = acc
+                Pm[j] = sat(acc)
+            Kt, Qt, Pt = k[blk[b]] * F, q[blk[b]] * F, (G * k)[blk[b]] * Pm
+            M[blk[b], blk[b]] = np.tril(Kt @ Pt.T)
+            Mq[blk[b], blk[b]] = np.tril(Qt @ Pt.T)
+        start = [np.cumprod(alpha[blk[b]], axis=0, dtype=f) for b in range(nb)]   # incl. t
+        end = []
+        for b in range(nb):                       # prod_{s < j <= end of block}
+            a = alpha[blk[b]]
+            e = np.ones((16, dk), f)
+            acc = np.ones(dk, f)
+            for j in range(15, -1, -1):
+                e[j] = acc
+                acc = acc * a[j]
+            end.append(e)
+        gblk = [np.prod(alpha[blk[b]], axis=0, dtype=f) for b in range(nb)]
+        for ib in range(nb):
+            for jb in range(ib):
+                rho = np.ones(dk, f)
+                for m in range(jb + 1, ib):
+                    rho = rho * gblk[m]
+                Kr, Qr = k[blk[ib]] * start[ib], q[blk[ib]] * start[ib]
+                Pc = (G * k)[blk[jb]] * end[jb] * rho
+                M[blk[ib], blk[jb]] = Kr @ Pc.T
+                Mq[blk[ib], blk[jb]] = Qr @ Pc.T
+    return M, Mq

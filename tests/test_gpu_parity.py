@@ -259,42 +259,3 @@ def test_full_workload_packed_sampled():
         check("o", o[:, t0:t1][:, :, heads], ref["o"], TOL[x.dtype])
         check("S_T", S[n:n + 1][:, heads], ref["S_T"], TOL[x.dtype])
         check("P_T", P[n:n + 1][:, heads], ref["P_T"], TOL[x.dtype])
-
-
-@pytest.mark.parametrize("variant", ["diag", "iso"])
-def test_decode_workload4_sampled(variant):
-    """The decode workload at full size: a slot pool of R = 256 rows (H16, d128), 64 decode
-    steps over all rows. Rows 0, 77 and 255 start from a T = 1024 prefill run on the GPU (the
-    other slots start from S = 0, P = 1); those rows are checked against the oracle."""
-    from paper_2609_07816_amd import kdn
-    R, H, d, steps = 256, 16, 128, 64
-    rows = [0, 77, 255]
-    pre = W.draw_inputs(variant, "bf16", len(rows), 1024, H, d, d, seed=1004, stream=0,
-                        alpha_per_channel=True)
-    dpre = to_device(pre)
-    f = kdn.forward_diag if variant == "diag" else kdn.forward_iso
-    _, S3, P3 = f(dpre["q"], dpre["k"], dpre["v"], dpre["alpha"], dpre["omega"], dpre["r"],
-                  mu=pre.mu, scale=pre.scale)
-    S_dev = torch.zeros((R, H, d, d), dtype=torch.float32, device="cuda")
-    P_dev = torch.ones((R, H, d) if variant == "diag" else (R, H), dtype=torch.float32,
-                       device="cuda")
-    S_dev[rows] = S3
-    P_dev[rows] = P3
-    ref = run_oracle_forward(pre)
-    S_ref, P_ref = ref["S_T"].copy(), ref["P_T"].copy()
-    torch.cuda.synchronize()
-    check("prefill S_T", host_f64(S3), S_ref, TOL["bf16"])
-    check("prefill P_T", host_f64(P3), P_ref, TOL["bf16"])
-    for s in range(steps):
-        x = W.draw_decode_step(variant, s)
-        dd = to_device(x)
-        o = kdn.decode_step(variant, *[dd[n][:, 0].contiguous() for n in NAMES], S_dev, P_dev,
-                            mu=x.mu, scale=x.scale)
-        o_ref = oracle.decode_step(variant, *[x.f64(n)[rows, 0] for n in NAMES], S_ref, P_ref,
-                                   mu=x.mu, scale=x.scale)
-        if s % 16 == 15:
-            torch.cuda.synchronize()
-            check(f"o step {s} (sampled rows)", host_f64(o)[rows], o_ref, TOL["bf16"])
-    torch.cuda.synchronize()
-    check("S after decode", host_f64(S_dev)[rows], S_ref, TOL["bf16"])
-    check("P after decode", host_f64(P_dev)[rows], P_ref, TOL["bf16"])
