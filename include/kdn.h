@@ -87,6 +87,26 @@ kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * kdn_forward_diag without a workspace argument, for callers that cannot allocate device
+ * memory (code under stream capture, serving loops, harnesses that forbid allocation). The
+ * operation, the other arguments, the outputs and the errors are those of kdn_forward_diag.
+ * Its scratch is a fixed 64 MiB array in the library, one copy per GPU (the device current
+ * at the call), created when the library's code is loaded on that GPU and held until the
+ * process ends; its address is looked up on the first call on each GPU. Sizes whose workspace
+ * (kdn_forward_workspace_bytes) exceeds 64 MiB give KDN_ERR_UNSUPPORTED: about 1000
+ * (chunk, head) pairs at dk = 128 in bf16, e.g. H = 16 heads of 4000 tokens. Nothing in the
+ * scratch needs to start at zero. Every call on one GPU uses the same scratch: calls that
+ * overlap in time on one GPU (two streams, or two threads) race and give undefined results;
+ * calls serialised on one stream are safe.
+ */
+kdn_status_t kdn_forward_diag_noalloc(const void* q, const void* k, const void* v,
+                                      const void* alpha, const void* omega, const void* r,
+                                      const float* S0, const float* P0, void* o, float* S_T,
+                                      float* P_T, const int32_t* cu_seqlens, int32_t N,
+                                      int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                                      kdn_dtype_t dtype, float mu, float scale, void* stream);
+
+/*
  * Isotropic KDN forward (Prop. "Isotropic Kalman Delta Network", eqs.
  * iso-kla-box-cov-update, iso-kla-box-gain, iso-kla-box-memory). One variance b per head:
  *   a = mean_i alpha_i^2;  b_hat = a b + omega;  beta = b_hat / (r + b_hat ||k||^2)

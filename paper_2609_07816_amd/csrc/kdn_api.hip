@@ -4,9 +4,20 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "kdn_internal.h"
 
 namespace {
+
+// Scratch of kdn_forward_diag_noalloc: one copy per GPU, held until the process ends. Host code
+// never uses the array's name as an address: the device address of each GPU's copy comes from
+// hipGetSymbolAddress (scratch_on_current_device).
+constexpr size_t SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
 
 thread_local char g_err[512] = "";
 
@@ -43,6 +54,27 @@ kdn_status_t hip_status(hipError_t e, const char* what)
 {
     if (e == hipSuccess) return ok();
     return fail(KDN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device address of the current device's copy of `scratch`, looked up once per device.
+kdn_status_t scratch_on_current_device(void** out)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(KDN_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= MAX_DEVICES)
+        return fail(KDN_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, MAX_DEVICES);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(KDN_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return KDN_OK;
 }
 
 // Shared validation of the forward / gain argument sets.
@@ -181,6 +213,35 @@ kdn_status_t kdn_forward_diag(const void* q, const void* k, const void* v, const
                                                    mu, scale, workspace),
                                           (hipStream_t)stream),
                       "kdn_forward_diag launch");
+}
+
+kdn_status_t kdn_forward_diag_noalloc(const void* q, const void* k, const void* v,
+                                      const void* alpha, const void* omega, const void* r,
+                                      const float* S0, const float* P0, void* o, float* S_T,
+                                      float* P_T, const int32_t* cu_seqlens, int32_t N,
+                                      int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                                      kdn_dtype_t dtype, float mu, float scale, void* stream)
+{
+    const size_t need = (B > 0 && T > 0 && H > 0 && N > 0 && head_ok(dk) && head_ok(dv) &&
+                         (dtype == KDN_F32 || dtype == KDN_BF16))
+                            ? kdn::chunked_workspace_bytes(0, cu_seqlens != nullptr, N, B, T, H,
+                                                           dk, dtype)
+                            : 0;
+    if (need > SCRATCH_BYTES)
+        return fail(KDN_ERR_UNSUPPORTED, "kdn_forward_diag_noalloc: these sizes need %zu bytes of "
+                    "scratch, more than its fixed %zu (use kdn_forward_diag with a workspace)",
+                    need, SCRATCH_BYTES);
+    void* ws = nullptr;
+    kdn_status_t st = scratch_on_current_device(&ws);
+    if (st != KDN_OK) return st;
+    st = check_forward(0, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, cu_seqlens, N, B, T, H,
+                       dk, dv, dtype, 1, mu, scale, 0, ws, SCRATCH_BYTES);
+    if (st != KDN_OK) return st;
+    return hip_status(kdn::launch_chunked(fwd_call(0, 1, q, k, v, alpha, omega, r, S0, P0, o, S_T,
+                                                   P_T, cu_seqlens, N, B, T, H, dk, dv, dtype,
+                                                   mu, scale, ws),
+                                          (hipStream_t)stream),
+                      "kdn_forward_diag_noalloc launch");
 }
 
 kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const void* alpha,

@@ -9,6 +9,7 @@ Functions mirror the C entry points:
 * ``forward_diag(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
   scale=None, chunk=0) -> (o, S_T, P_T)``
 * ``forward_iso(...)`` -- same, ``alpha`` may be [B,T,H,dk] (per channel) or [B,T,H]
+* ``forward_diag_noalloc(...)`` -- ``forward_diag`` on the library's fixed scratch
 * ``decode_step(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None, scale=None)
   -> o`` (S and P updated in place)
 * ``gain_diag(k, alpha, omega, r, P0=None, cu_seqlens=None, mu=None) -> (kappa, phat, P_T)``
@@ -61,14 +62,15 @@ def lib():
                                                             vp]
     L.kdn_forward_iso.argtypes = [vp] * 12 + [i32] * 6 + [ctypes.c_int, i32, f32, f32, i32, vp,
                                                            sz, vp]
+    L.kdn_forward_diag_noalloc.argtypes = [vp] * 12 + [i32] * 6 + [ctypes.c_int, f32, f32, vp]
     L.kdn_decode_step.argtypes = [i32] + [vp] * 10 + [i32] * 5 + [ctypes.c_int, i32, f32, f32,
                                                                    vp]
     L.kdn_gain_diag.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, f32, vp, sz, vp]
     L.kdn_gain_iso.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, i32, f32, vp, sz, vp]
     L.kdn_forward_workspace_bytes.argtypes = [i32] * 7 + [ctypes.c_int, i32, i32]
     L.kdn_gain_workspace_bytes.argtypes = [i32] * 6
-    for name in ("kdn_forward_diag", "kdn_forward_iso", "kdn_decode_step", "kdn_gain_diag",
-                 "kdn_gain_iso"):
+    for name in ("kdn_forward_diag", "kdn_forward_iso", "kdn_forward_diag_noalloc",
+                 "kdn_decode_step", "kdn_gain_diag", "kdn_gain_iso"):
         getattr(L, name).restype = ctypes.c_int
     L.kdn_forward_workspace_bytes.restype = sz
     L.kdn_gain_workspace_bytes.restype = sz
@@ -155,6 +157,31 @@ def forward_diag(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu
                  scale=None, chunk=0):
     """Diagonal KDN forward; returns (o, S_T, P_T)."""
     return _forward(0, q, k, v, alpha, omega, r, S0, P0, cu_seqlens, mu, scale, chunk)
+
+
+def forward_diag_noalloc(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
+                         scale=None, o=None, S_T=None, P_T=None):
+    """Diagonal KDN forward with the library's own fixed scratch (no workspace); outputs may be
+    passed in (o, S_T, P_T) so that the call allocates nothing. Returns (o, S_T, P_T)."""
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    _same(k.dtype, q, v, alpha, omega, r)
+    dev = k.device
+    N = B if cu_seqlens is None else cu_seqlens.numel() - 1
+    mu = float(dk if mu is None else mu)
+    scale = float(dk ** -0.5 if scale is None else scale)
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=k.dtype, device=dev)
+    if S_T is None:
+        S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
+    if P_T is None:
+        P_T = torch.empty((N, H, dk), dtype=torch.float32, device=dev)
+    st = lib().kdn_forward_diag_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(omega), _ptr(r), _ptr(_f32(S0)),
+        _ptr(_f32(P0)), _ptr(o), _ptr(_f32(S_T)), _ptr(_f32(P_T)), _ptr(cu_seqlens), N, B, T, H,
+        dk, dv, _dtype_code(k), ctypes.c_float(mu), ctypes.c_float(scale), _stream(dev))
+    _check(st, "kdn_forward_diag_noalloc")
+    return o, S_T, P_T
 
 
 def forward_iso(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
