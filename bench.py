@@ -1,17 +1,21 @@
 """Benchmark of the KDN forward hot path on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--only WHAT]
 
-Workload: Diagonal KDN forward, B=4, H=16, T=4096, dk=dv=128, bf16 q/k/v/gates/noise, float32
-state (the mixer shape of the paper's 750M model: 16 heads x 128 at d_model 2048, 4K context,
-batch 4 as in its throughput probe). Inputs are seeded synthetic tensors resident in HBM before
-timing starts. One step = one full forward over the batch (every stage of the path: the
-variance chain and gains, the chunk operands, the chunkwise triangular solve, the state update,
-the outputs and the final states; all in one walk kernel).
+Headline workload: Diagonal KDN forward, B=4, H=16, T=4096, dk=dv=128, bf16 q/k/v/gates/noise,
+float32 state (the mixer shape of the paper's 750M model: 16 heads x 128 at d_model 2048, 4K
+context, batch 4 as in its throughput probe). Inputs are seeded synthetic tensors resident in HBM
+before timing starts. One step = one full forward over the batch: every stage of the path (the
+chunk summaries of the variance chain, the log-depth carry scan, the per-chunk prep of the gains
+and the chunk operands, and the walk that carries the memory through the chunks).
 
-Prints one JSON line with tokens/s, the roofline position of one forward call (algorithmic bytes
-per call / the HIP-event duration of the call on the caller's stream, against the 8 TB/s HBM
-peak) and the CPU oracle timed on a bounded sample of the same workload.
+Prints one JSON line: tokens/s of the headline forward, the roofline position of one forward call
+(algorithmic bytes per call / the HIP-event duration of the call on the caller's stream, against
+the 8 TB/s HBM peak), the CPU oracle timed on a bounded sample of the same workload, and one
+object per other workload of the path (the isotropic forward, the packed variable-length batch,
+the decode workload's prefill and decode steps, the gain scan alone), each timed the same way.
+The larger workloads draw their inputs on the GPU with the same laws (timing only; their parity
+is checked by the tests on host-drawn inputs).
 """
 
 from __future__ import annotations
@@ -19,6 +23,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import platform
 import sys
 import time
 
@@ -28,67 +33,232 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "KDN forward tokens/s (H=16,d=128,T=4096) + % of MFMA/HBM roofline"
-HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+FORWARD_KERNELS = "forward call: 4 kernels (chunk summaries, log-depth carry scan, per-chunk " \
+                  "prep, walk over the chunks)"
 
 
-def algorithmic_bytes(B, T, H, dk, dv, in_bytes, variant="diag"):
-    """Minimum HBM traffic of one forward: every input read once, o written once, final states
-    written once (no initial state is read here: S0 = 0, P0 = 1)."""
-    per_tok_head = (2 * dk + dv) * in_bytes + dv * in_bytes  # q, k, v in; o out
+# ---------------------------------------------------------------------------------------------
+# algorithmic work
+# ---------------------------------------------------------------------------------------------
+
+def forward_bytes(tokens, N, H, dk, dv, es, variant, apc=True, with_init=False):
+    """Minimum HBM traffic of one forward: every input read once, o written once, the final
+    states written once (and the initial states read once when given)."""
     if variant == "diag":
-        per_tok_head += 2 * dk * in_bytes + in_bytes          # alpha, omega per channel; r
+        per = (2 * dk + dv) * es + 2 * dk * es + es            # q, k, v; alpha, omega; r
     else:
-        per_tok_head += 3 * in_bytes                          # scalar alpha, omega, r
-    states = H * B * (dk * dv * 4 + (dk if variant == "diag" else 1) * 4)
-    return B * T * H * per_tok_head + states
+        per = (2 * dk + dv) * es + (dk if apc else 1) * es + 2 * es  # q, k, v; alpha; omega, r
+    per += dv * es                                              # o
+    nst = dk if variant == "diag" else 1
+    states = N * H * (dk * dv * 4 + nst * 4)
+    return tokens * H * per + states * (2 if with_init else 1)
 
 
-def algorithmic_flops(B, T, H, dk, dv, C=64):
+def forward_flops(tokens, H, dk, dv, C=64):
     """Dense flop count of the chunked WY form per token-head: 6 dk dv + 10 C d + C^2 / 3."""
-    d = dk
-    return B * T * H * (6 * d * dv + 10 * C * d + C * C / 3.0)
+    return tokens * H * (6 * dk * dv + 10 * C * dk + C * C / 3.0)
 
 
-def decode_bytes(R, H, dk, dv, in_bytes):
-    """Minimum HBM traffic of one Diagonal decode step: the state slot read and written
-    (S and P in float32), the token's inputs read and o written."""
-    per_row_head = 2 * (dk * dv * 4 + dk * 4) + (2 * dk + dv + 2 * dk) * in_bytes + in_bytes \
-        + dv * in_bytes
-    return R * H * per_row_head
+def decode_bytes(R, H, dk, dv, es, variant):
+    """Minimum HBM traffic of one decode step: the state slot read and written (S and P in
+    float32), the token's inputs read and o written."""
+    nst = dk if variant == "diag" else 1
+    per = 2 * (dk * dv * 4 + nst * 4) + (2 * dk + dv) * es + dk * es \
+        + (dk if variant == "diag" else 1) * es + es + dv * es
+    return R * H * per
 
 
-def decode_measure(kdn, W, torch, steps=64):
-    """Diagonal decode steps at the serving shape (R = 256 rows, H = 16, d = 128, bf16 inputs,
-    a float32 state pool of 256 slots updated in place): per-step HIP-event durations on the
-    caller's stream, against the HBM roofline. Reported beside the forward line."""
-    import numpy as np
-    R, H, d = 256, 16, 128
-    x = W.draw_inputs("diag", "bf16", R, 1, H, d, d, seed=1004, random_state=True)
-    dev = {n: torch.from_numpy(x.stored[n].view(np.int16)).view(torch.bfloat16).cuda()[:, 0]
-           for n in ("q", "k", "v", "alpha", "omega", "r")}
-    S = torch.from_numpy(x.S0.astype(np.float32)).cuda()
-    P = torch.from_numpy(x.P0.astype(np.float32)).cuda()
+def gain_bytes(tokens, H, dk, es):
+    """Minimum traffic of the gain scan alone (diagonal): k, alpha, omega and r read once, the
+    gains written once in float32."""
+    return tokens * H * (3 * dk * es + es + 4 * dk)
+
+
+# ---------------------------------------------------------------------------------------------
+# inputs drawn on the GPU (same laws as paper_2609_07816_amd/workloads.py)
+# ---------------------------------------------------------------------------------------------
+
+def gpu_inputs(torch, variant, B, T, H, dk, dv, seed, apc=True, random_state=False, N=None):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    f32, bf = torch.float32, torch.bfloat16
+
+    def normal(shape):
+        return torch.randn(shape, generator=g, device="cuda", dtype=f32)
+
+    def unit(x):
+        return (x / x.norm(dim=-1, keepdim=True)).to(bf)
+
+    sp = torch.nn.functional.softplus
+    d = {"q": unit(normal((B, T, H, dk))), "k": unit(normal((B, T, H, dk))),
+         "v": normal((B, T, H, dv)).to(bf)}
+    ashape = (B, T, H, dk) if (variant == "diag" or apc) else (B, T, H)
+    d["alpha"] = torch.sigmoid(normal(ashape) + 2.0).to(bf)
+    oshape = (B, T, H, dk) if variant == "diag" else (B, T, H)
+    d["omega"] = (sp(normal(oshape)) + 1e-3).to(bf)
+    d["r"] = (sp(normal((B, T, H))) + 1e-3).to(bf)
+    if random_state:
+        n = B if N is None else N
+        d["S0"] = 0.02 * normal((n, H, dk, dv))
+        pshape = (n, H, dk) if variant == "diag" else (n, H)
+        d["P0"] = torch.rand(pshape, generator=g, device="cuda") * 0.9 + 0.1
+    return d
+
+
+NAMES = ("q", "k", "v", "alpha", "omega", "r")
+
+
+def time_calls(torch, fn, steps, warmup):
+    """HIP events around every call on torch's current stream (the stream the binding passes to
+    the library; every kernel of a call runs on it). Returns per-call milliseconds."""
     stream = torch.cuda.current_stream()
-    args = [dev[n] for n in ("q", "k", "v", "alpha", "omega", "r")]
-    for _ in range(5):
-        kdn.decode_step("diag", *args, S, P, mu=x.mu, scale=x.scale)
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
     torch.cuda.synchronize()
-    for i in range(steps):
-        ev[i][0].record(stream)
-        kdn.decode_step("diag", *args, S, P, mu=x.mu, scale=x.scale)
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
-    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-    nbytes = decode_bytes(R, H, d, d, 2)
-    gbs = nbytes / (ms * 1e-3) / 1e9
-    return {"workload": "diag-decode-R256-H16-d128 (state pool of 256 slots, bf16 inputs)",
-            "kernel": "decode_kernel: one workgroup per (row, head)", "steps": steps,
-            "ms_per_step_median": round(ms, 4), "tokens_per_s": round(R / (ms * 1e-3), 1),
-            "algorithmic_bytes_per_step": nbytes, "achieved": round(gbs, 1),
-            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def summary(ms, nbytes, tokens, extra=None):
+    med, mean = float(np.median(ms)), float(np.mean(ms))
+    gbs = nbytes / (mean * 1e-3) / 1e9
+    rec = {"ms_median": round(med, 4), "ms_mean": round(mean, 4),
+           "tokens_per_s": round(tokens / (med * 1e-3), 1), "algorithmic_bytes": int(nbytes),
+           "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    if extra:
+        rec.update(extra)
+    return rec
+
+
+# ---------------------------------------------------------------------------------------------
+# the other workloads of the path
+# ---------------------------------------------------------------------------------------------
+
+def bench_iso(torch, kdn, steps):
+    """Workload 1: isotropic forward, B4 H16 T2048 d128, scalar gates, bf16."""
+    B, T, H, d = 4, 2048, 16, 128
+    x = gpu_inputs(torch, "iso", B, T, H, d, d, seed=1001, apc=False)
+    ms = time_calls(torch, lambda: kdn.forward_iso(*[x[n] for n in NAMES], mu=float(d),
+                                                   scale=d ** -0.5), steps, 3)
+    return summary(ms, forward_bytes(B * T, B, H, d, d, 2, "iso", apc=False), B * T,
+                   {"workload": "iso-fwd-B4-H16-T2048-d128 (scalar gates)",
+                    "kernels": FORWARD_KERNELS})
+
+
+def bench_varlen(torch, kdn, W, steps):
+    """Workload 3: diagonal forward over 32 packed sequences of U[256, 8192] tokens, random
+    initial states, bf16."""
+    H, d = 16, 128
+    lens = W.draw_lengths(32, 256, 8192, seed=1003)
+    T = int(lens.sum())
+    x = gpu_inputs(torch, "diag", 1, T, H, d, d, seed=1003, random_state=True, N=len(lens))
+    cu = torch.zeros(len(lens) + 1, dtype=torch.int32, device="cuda")
+    cu[1:] = torch.from_numpy(np.cumsum(lens).astype(np.int32)).cuda()
+    ms = time_calls(torch, lambda: kdn.forward_diag(*[x[n] for n in NAMES], S0=x["S0"],
+                                                    P0=x["P0"], cu_seqlens=cu, mu=float(d),
+                                                    scale=d ** -0.5), steps, 3)
+    return summary(ms, forward_bytes(T, len(lens), H, d, d, 2, "diag", with_init=True), T,
+                   {"workload": f"diag-varlen-32seq-U256-8192-H16-d128 ({T} tokens)",
+                    "kernels": FORWARD_KERNELS})
+
+
+def bench_decode_workload(torch, kdn, steps):
+    """Workload 4: B256 T1024 prefill of every row (diagonal, bf16), then decode steps of both
+    variants on 256 rows; also the diagonal step on a pool of 1024 slots (4x the state the
+    Infinity Cache can hold), rows mapped to every fourth slot."""
+    R, H, d, T = 256, 16, 128, 1024
+    out = {}
+    x = gpu_inputs(torch, "diag", R, T, H, d, d, seed=1004)
+    ms = time_calls(torch, lambda: kdn.forward_diag(*[x[n] for n in NAMES], mu=float(d),
+                                                    scale=d ** -0.5), max(3, steps // 4), 1)
+    out["prefill"] = summary(ms, forward_bytes(R * T, R, H, d, d, 2, "diag"), R * T,
+                             {"workload": "diag-fwd-B256-H16-T1024-d128 (the decode prefill)",
+                              "kernels": FORWARD_KERNELS})
+    del x
+    torch.cuda.empty_cache()
+    for variant in ("diag", "iso"):
+        st = gpu_inputs(torch, variant, R, 1, H, d, d, seed=1104, apc=True, random_state=True)
+        args = [st[n][:, 0].contiguous() for n in NAMES]
+        S, P = st["S0"], st["P0"]
+        ms = time_calls(torch, lambda: kdn.decode_step(variant, *args, S, P, mu=float(d),
+                                                       scale=d ** -0.5), 64, 5)
+        out[f"decode_{variant}"] = summary(
+            ms, decode_bytes(R, H, d, d, 2, variant), R,
+            {"workload": f"{variant}-decode-R256-H16-d128 (state pool of 256 slots, 256 MiB)",
+             "kernel": "decode_kernel: one workgroup per (row, head)"})
+    st = gpu_inputs(torch, "diag", R, 1, H, d, d, seed=1105, random_state=True, N=4 * R)
+    args = [st[n][:, 0].contiguous() for n in NAMES]
+    slots = torch.arange(0, 4 * R, 4, dtype=torch.int32, device="cuda")
+    ms = time_calls(torch, lambda: kdn.decode_step("diag", *args, st["S0"], st["P0"],
+                                                   slot_idx=slots, mu=float(d),
+                                                   scale=d ** -0.5), 64, 5)
+    out["decode_diag_pool1024"] = summary(
+        ms, decode_bytes(R, H, d, d, 2, "diag"), R,
+        {"workload": "diag-decode-R256-H16-d128, rows on every fourth slot of a 1024-slot pool "
+                     "(1 GiB of state)", "kernel": "decode_kernel"})
+    return out
+
+
+def bench_gain(torch, kdn, x, steps):
+    """The gain scan alone (kdn_gain_diag) at the headline shape: chunk summaries, carry scan
+    and emission of the float32 gains."""
+    B, T, H, d = x["k"].shape
+    ms = time_calls(torch, lambda: kdn.gain_diag(x["k"], x["alpha"], x["omega"], x["r"],
+                                                 mu=float(d), want_phat=False), steps, 3)
+    return summary(ms, gain_bytes(B * T, H, d, 2), B * T,
+                   {"workload": "diag-gain-scan-B4-H16-T4096-d128 (kappa out, float32)",
+                    "kernels": "gain scan: chunk summaries, carry scan, emission"})
+
+
+# ---------------------------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the headline workload
+# ---------------------------------------------------------------------------------------------
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(x, nthreads):
+    """The oracle, unchanged, on the workload's independent (batch row, head) chains at full
+    length: all 64 chains in one OpenMP call on nthreads threads, and one chain alone on one
+    thread. Returns the rate in workload tokens/s."""
+    import oracle
+    arrs = {n: x.f64(n) for n in NAMES}
+    chains = [(b, h) for b in range(x.B) for h in range(x.H)]
+    a1 = [np.ascontiguousarray(arrs[n][0:1, :, 0:1]) for n in NAMES]
+    t0 = time.perf_counter()
+    oracle.forward_diag(*a1, mu=x.mu, scale=x.scale, nthreads=1)
+    t_one = time.perf_counter() - t0
+    a = [np.ascontiguousarray(np.stack([arrs[n][b, :, h] for b, h in chains])[:, :, None])
+         for n in NAMES]
+    t0 = time.perf_counter()
+    oracle.forward_diag(*a, mu=x.mu, scale=x.scale, nthreads=nthreads)
+    t_par = time.perf_counter() - t0
+    token_heads = len(chains) * x.T
+    return {"value": round(token_heads / x.H / t_par, 1), "unit": "tokens/s",
+            "cores": nthreads, "kind": "oracle", "nproc": os.cpu_count(),
+            "cpu_model": cpu_model(),
+            "sample": f"all {len(chains)} (batch row, head) chains of the headline workload at "
+                      f"full length T={x.T} ({token_heads} token-heads, one workload token = "
+                      f"{x.H} token-heads); float64 sequential recurrence, OpenMP over chains on "
+                      f"{nthreads} threads: {t_par:.2f} s; one chain on one thread: "
+                      f"{t_one:.2f} s"}
 
 
 PROFILE = os.path.join(ROOT, "profiles", "kdn_forward_diag_B4_T4096_H16_d128.json")
@@ -109,38 +279,6 @@ def measured_traffic():
         return None
 
 
-def cpu_baseline(x, nthreads):
-    """The oracle, unchanged, on the workload's independent (batch row, head) chains at full
-    length (a bounded run: about ten seconds on one core). Returns the rate in workload
-    tokens/s."""
-    import oracle
-    names = ("q", "k", "v", "alpha", "omega", "r")
-    chains = [(b, h) for b in range(x.B) for h in range(x.H)]  # every chain: ~10 s on one core
-    arrs = {n: x.f64(n) for n in names}
-    t_total = 0.0
-    for b, h in chains:
-        a = [np.ascontiguousarray(arrs[n][b:b + 1, :, h:h + 1]) for n in names]
-        t0 = time.perf_counter()
-        oracle.forward_diag(*a, mu=x.mu, scale=x.scale, nthreads=1)
-        t_total += time.perf_counter() - t0
-    # chains are independent and the oracle parallelises over chains with OpenMP; the sample is
-    # timed chain by chain on one thread and scaled by the thread count actually available
-    # (measured directly below with all chains in one OpenMP call)
-    a = [np.ascontiguousarray(np.stack([arrs[n][b, :, h] for b, h in chains])[:, :, None])
-         for n in names]
-    t0 = time.perf_counter()
-    oracle.forward_diag(*a, mu=x.mu, scale=x.scale, nthreads=nthreads)
-    t_par = time.perf_counter() - t0
-    token_heads = len(chains) * x.T
-    tokens_equiv = token_heads / x.H  # one workload token carries H head-chains
-    return {"value": tokens_equiv / t_par, "unit": "tokens/s", "cores": nthreads,
-            "kind": "oracle",
-            "sample": f"{len(chains)} of {x.B * x.H} (batch row, head) chains of the workload at "
-                      f"full length T={x.T} ({token_heads} token-heads); float64 sequential "
-                      f"recurrence, OpenMP over chains; single-thread time "
-                      f"{t_total:.2f} s, {nthreads}-thread time {t_par:.2f} s"}
-
-
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -148,6 +286,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--only", default="all",
+                    choices=["all", "headline", "iso", "varlen", "decode", "gain"],
+                    help="run only the headline forward or one other workload (profiling runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (used to "
                          "calibrate the HBM byte counters of rocprofv3)")
@@ -173,15 +314,23 @@ def main():
                           "launches": 5}))
         return
     kdn.lib()
+    if args.only in ("iso", "varlen", "decode"):
+        fn = {"iso": lambda: bench_iso(torch, kdn, args.steps),
+              "varlen": lambda: bench_varlen(torch, kdn, W, args.steps),
+              "decode": lambda: bench_decode_workload(torch, kdn, args.steps)}[args.only]
+        print(json.dumps({args.only: fn()}), flush=True)
+        return
+
     x = W.draw_workload(2)
     B, T, H, dk, dv = x.B, x.T, x.H, x.dk, x.dv
-    names = ("q", "k", "v", "alpha", "omega", "r")
     dev = {n: torch.from_numpy(x.stored[n].view(np.int16)).view(torch.bfloat16).cuda()
-           for n in names}
-    stream = torch.cuda.current_stream()
+           for n in NAMES}
+    if args.only == "gain":
+        print(json.dumps({"gain": bench_gain(torch, kdn, dev, args.steps)}), flush=True)
+        return
 
     def step():
-        return kdn.forward_diag(*[dev[n] for n in names], mu=x.mu, scale=x.scale,
+        return kdn.forward_diag(*[dev[n] for n in NAMES], mu=x.mu, scale=x.scale,
                                 chunk=args.chunk)
 
     for _ in range(args.warmup):
@@ -191,6 +340,7 @@ def main():
     # timed region: K steps between two synchronisations; HIP events around every forward
     # call on torch's current stream, which the binding passes to the library (every kernel of
     # the call runs on that stream)
+    stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -208,8 +358,8 @@ def main():
     value = tokens / (ms_per_step / 1e3)
     kmean = float(np.mean(kern_ms))
     kmed = float(np.median(kern_ms))
-    abytes = algorithmic_bytes(B, T, H, dk, dv, 2)
-    aflops = algorithmic_flops(B, T, H, dk, dv)
+    abytes = forward_bytes(B * T, B, H, dk, dv, 2, "diag")
+    aflops = forward_flops(B * T, H, dk, dv)
     achieved = abytes / (kmean * 1e-3) / 1e9
     rec = {
         "metric": METRIC,
@@ -226,22 +376,24 @@ def main():
         "data": "synthetic",
         "config": {"workload": "diag-fwd-B4-H16-T4096-d128", "variant": "diagonal", "B": B,
                    "T": T, "H": H, "dk": dk, "dv": dv, "inputs": "bf16", "state": "f32",
-                   "mfma": "bf16 in, f32 accumulate", "chunk": args.chunk or 64,
+                   "mfma": "bf16 in, f32 accumulate", "chunk": 64,
                    "mu": x.mu, "scale": x.scale},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(),
-                     "kernel": "walk_kernel: one workgroup per (sequence, head, 32 value "
-                               "columns) walks the chunks (bf16, dk=dv=128, chunk 64)",
+                     "kernel": FORWARD_KERNELS + "; bf16, dk=dv=128, chunk 64",
                      "algorithmic_bytes_per_launch": abytes,
                      "kernel_ms_mean": round(kmean, 4), "kernel_ms_median": round(kmed, 4),
                      "mfma_frac": round(aflops / (kmean * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
                                         4)},
     }
-    rec["decode"] = decode_measure(kdn, W, torch)
+    if args.only == "all":
+        rec["workloads"] = {"iso_forward": bench_iso(torch, kdn, args.steps),
+                            "varlen_forward": bench_varlen(torch, kdn, W, args.steps),
+                            "gain_scan": bench_gain(torch, kdn, dev, args.steps)}
+        rec["workloads"].update(bench_decode_workload(torch, kdn, args.steps))
     if not args.no_cpu_baseline:
-        nthreads = min(16, os.cpu_count() or 1)
-        rec["cpu_baseline"] = cpu_baseline(x, nthreads)
+        rec["cpu_baseline"] = cpu_baseline(x, min(16, os.cpu_count() or 1))
     print(json.dumps(rec), flush=True)
 
 
