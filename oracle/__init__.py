@@ -46,9 +46,10 @@ def _load():
     d = ctypes.POINTER(ctypes.c_double)
     i32p = ctypes.POINTER(ctypes.c_int32)
     ci, cd = ctypes.c_int, ctypes.c_double
-    lib.oracle_kdn_forward_diag.argtypes = [d] * 14 + [i32p] + [ci] * 6 + [cd, cd, ci]
-    lib.oracle_kdn_forward_iso.argtypes = [d] * 14 + [i32p] + [ci] * 7 + [cd, cd, ci]
-    lib.oracle_kdn_decode_step.argtypes = ([ci] + [d] * 8 + [i32p, d] + [ci] * 6 + [cd, cd, ci])
+    lib.oracle_kdn_forward_diag.argtypes = [d] * 14 + [i32p] + [ci] * 6 + [cd, cd, ci, d, d]
+    lib.oracle_kdn_forward_iso.argtypes = [d] * 14 + [i32p] + [ci] * 7 + [cd, cd, ci, d, d]
+    lib.oracle_kdn_decode_step.argtypes = ([ci] + [d] * 8 + [i32p, d] + [ci] * 6 +
+                                           [cd, cd, ci, d, d])
     for name in ("oracle_mobius_fold", "oracle_mobius_tree"):
         getattr(lib, name).argtypes = [d, d, d, cd, ctypes.c_int64, ci, d, d]
     lib.oracle_mobius_chunked.argtypes = [d, d, d, cd, ctypes.c_int64, ctypes.c_int64, ci, d, d]
@@ -78,9 +79,10 @@ def _f64(a):
 
 
 def forward_diag(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
-                 scale=None, traces=False, nthreads=0):
-    """Diagonal KDN forward. Returns dict with o, S_T, P_T (and phat, kappa, p when traces)."""
-    q, k, v, alpha, omega, r, S0, P0 = map(_f64, (q, k, v, alpha, omega, r, S0, P0))
+                 scale=None, traces=False, nthreads=0, mu_t=None, beta_eff=False):
+    """Diagonal KDN forward. Returns dict with o, S_T, P_T (and phat, kappa, p when traces;
+    beta_eff = k^T kappa per token when beta_eff). mu_t [B,T,H] replaces mu per token."""
+    q, k, v, alpha, omega, r, S0, P0, mu_t = map(_f64, (q, k, v, alpha, omega, r, S0, P0, mu_t))
     B, T, H, dk = k.shape
     dv = v.shape[-1]
     cu = None if cu_seqlens is None else np.ascontiguousarray(cu_seqlens, dtype=np.int32)
@@ -91,19 +93,23 @@ def forward_diag(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu
     if traces:
         for name in ("phat", "kappa", "p"):
             out[name] = np.zeros((B, T, H, dk))
+    if beta_eff:
+        out["beta_eff"] = np.zeros((B, T, H))
     rc = _load().oracle_kdn_forward_diag(
         _p(q), _p(k), _p(v), _p(alpha), _p(omega), _p(r), _p(S0), _p(P0), _p(out["o"]),
         _p(out["S_T"]), _p(out["P_T"]), _p(out.get("phat")), _p(out.get("kappa")),
-        _p(out.get("p")), _pi(cu), N, B, T, H, dk, dv, mu, scale, nthreads)
+        _p(out.get("p")), _pi(cu), N, B, T, H, dk, dv, mu, scale, nthreads, _p(mu_t),
+        _p(out.get("beta_eff")))
     if rc != 0:
         raise ValueError("oracle_kdn_forward_diag rejected its arguments")
     return out
 
 
 def forward_iso(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
-                scale=None, traces=False, nthreads=0):
-    """Isotropic KDN forward; alpha [B,T,H,dk] (per channel) or [B,T,H] (per head)."""
-    q, k, v, alpha, omega, r, S0, P0 = map(_f64, (q, k, v, alpha, omega, r, S0, P0))
+                scale=None, traces=False, nthreads=0, mu_t=None, beta_eff=False):
+    """Isotropic KDN forward; alpha [B,T,H,dk] (per channel) or [B,T,H] (per head).
+    mu_t [B,T,H] replaces mu per token; beta_eff adds beta ||k||^2 per token."""
+    q, k, v, alpha, omega, r, S0, P0, mu_t = map(_f64, (q, k, v, alpha, omega, r, S0, P0, mu_t))
     B, T, H, dk = k.shape
     dv = v.shape[-1]
     per_channel = int(alpha.ndim == 4)
@@ -115,19 +121,23 @@ def forward_iso(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=
     if traces:
         for name in ("bhat", "beta", "b"):
             out[name] = np.zeros((B, T, H))
+    if beta_eff:
+        out["beta_eff"] = np.zeros((B, T, H))
     rc = _load().oracle_kdn_forward_iso(
         _p(q), _p(k), _p(v), _p(alpha), _p(omega), _p(r), _p(S0), _p(P0), _p(out["o"]),
         _p(out["S_T"]), _p(out["P_T"]), _p(out.get("bhat")), _p(out.get("beta")),
-        _p(out.get("b")), _pi(cu), N, B, T, H, dk, dv, per_channel, mu, scale, nthreads)
+        _p(out.get("b")), _pi(cu), N, B, T, H, dk, dv, per_channel, mu, scale, nthreads,
+        _p(mu_t), _p(out.get("beta_eff")))
     if rc != 0:
         raise ValueError("oracle_kdn_forward_iso rejected its arguments")
     return out
 
 
 def decode_step(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None, scale=None,
-                nthreads=0):
-    """One decode step; S and P (float64 arrays) are updated in place. Returns o [R,H,dv]."""
-    q, k, v, alpha, omega, r = map(_f64, (q, k, v, alpha, omega, r))
+                nthreads=0, mu_t=None, beta_eff=None):
+    """One decode step; S and P (float64 arrays) are updated in place. Returns o [R,H,dv].
+    mu_t [R,H] replaces mu per row; beta_eff (a float64 [R,H] array) receives k^T kappa."""
+    q, k, v, alpha, omega, r, mu_t = map(_f64, (q, k, v, alpha, omega, r, mu_t))
     assert S.dtype == np.float64 and S.flags["C_CONTIGUOUS"]
     assert P.dtype == np.float64 and P.flags["C_CONTIGUOUS"]
     R, H, dk = k.shape
@@ -141,7 +151,7 @@ def decode_step(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None,
     scale = float(dk ** -0.5 if scale is None else scale)
     rc = _load().oracle_kdn_decode_step(
         vid, _p(q), _p(k), _p(v), _p(alpha), _p(omega), _p(r), _p(S), _p(P), _pi(si), _p(o),
-        R, num_slots, H, dk, dv, per_channel, mu, scale, nthreads)
+        R, num_slots, H, dk, dv, per_channel, mu, scale, nthreads, _p(mu_t), _p(beta_eff))
     if rc != 0:
         raise ValueError("oracle_kdn_decode_step rejected its arguments")
     return o
@@ -171,3 +181,37 @@ def mobius_tree(a, w, u, p0=1.0, renorm=True):
 def mobius_chunked(a, w, u, p0=1.0, Cg=256, renorm=True):
     """Three-pass chunked Moebius scan with chunk length Cg; returns (phat, p) per token."""
     return _mobius("oracle_mobius_chunked", a, w, u, p0, renorm, int(Cg))
+
+
+# ---------------------------------------------------------------------------------------------
+# The mixer layer's input maps (Prop. "Diagonal Kalman Delta Network", eq.
+# kla-box-parameterization; Prop. "Isotropic Kalman Delta Network", eq.
+# iso-kla-box-parameterization): the gates and noise terms come from pre-activations through
+# alpha = sigmoid(.), omega = softplus(.), r = r_min + softplus(.); the layer's queries and keys
+# are L2-normalised per token and head (Sec. "Experiments", the KDA-style layer).
+# ---------------------------------------------------------------------------------------------
+
+def sigmoid(x):
+    """1 / (1 + exp(-x)) in float64, evaluated without overflow for either sign."""
+    x = np.asarray(x, dtype=np.float64)
+    e = np.exp(-np.abs(x))
+    return np.where(x >= 0, 1.0 / (1.0 + e), e / (1.0 + e))
+
+
+def softplus(x):
+    """log(1 + exp(x)) in float64, as max(x, 0) + log1p(exp(-|x|))."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.maximum(x, 0.0) + np.log1p(np.exp(-np.abs(x)))
+
+
+def l2_normalize(x):
+    """x / ||x|| over the last axis (zero rows stay zero)."""
+    x = np.asarray(x, dtype=np.float64)
+    n = np.sqrt(np.sum(x * x, axis=-1, keepdims=True))
+    return np.where(n > 0, x / np.where(n > 0, n, 1.0), 0.0)
+
+
+def layer_inputs(q, k, a_pre, w_pre, r_pre, r_min, qk_norm=True):
+    """The recurrence's inputs from the layer's: (q, k, alpha, omega, r) in float64."""
+    qq, kk = (l2_normalize(q), l2_normalize(k)) if qk_norm else (_f64(q), _f64(k))
+    return qq, kk, sigmoid(a_pre), softplus(w_pre), float(r_min) + softplus(r_pre)

@@ -78,7 +78,7 @@ static void set_threads(int nthreads)
 static void diag_step(int dk, int dv, double* S, double* p, const double* q, const double* k,
                       const double* v, const double* alpha, const double* omega, double r,
                       double mu, double scale, double* o, double* phat_out, double* kappa_out,
-                      double* p_out, double* ph, double* kappa, double* delta)
+                      double* p_out, double* beff_out, double* ph, double* kappa, double* delta)
 {
     double den = r;
     for (int i = 0; i < dk; ++i) {
@@ -86,6 +86,12 @@ static void diag_step(int dk, int dv, double* S, double* p, const double* q, con
         den += ph[i] * k[i] * k[i];
     }
     for (int i = 0; i < dk; ++i) kappa[i] = ph[i] * k[i] / den;
+    if (beff_out) { /* effective write strength k^T kappa (App. "Overwrite and Protection-Write
+                       Decoupling") */
+        double b = 0.0;
+        for (int i = 0; i < dk; ++i) b += k[i] * kappa[i];
+        *beff_out = b;
+    }
     /* predicted memory S_hat = diag(alpha) S, stored in place */
     for (int i = 0; i < dk; ++i)
         for (int j = 0; j < dv; ++j) S[(int64_t)i * dv + j] *= alpha[i];
@@ -125,7 +131,7 @@ static void diag_step(int dk, int dv, double* S, double* p, const double* q, con
 static void iso_step(int dk, int dv, double* S, double* b, const double* q, const double* k,
                      const double* v, const double* alpha, int per_channel, double omega,
                      double r, double mu, double scale, double* o, double* bhat_out,
-                     double* beta_out, double* b_out, double* delta)
+                     double* beta_out, double* b_out, double* beff_out, double* delta)
 {
     double a = 0.0;
     if (per_channel) {
@@ -138,6 +144,7 @@ static void iso_step(int dk, int dv, double* S, double* b, const double* q, cons
     for (int i = 0; i < dk; ++i) nk += k[i] * k[i];
     double bh = a * (*b) + omega;
     double beta = bh / (r + bh * nk);
+    if (beff_out) *beff_out = beta * nk; /* k^T (beta k) */
     for (int i = 0; i < dk; ++i) {
         double ai = per_channel ? alpha[i] : alpha[0];
         for (int j = 0; j < dv; ++j) S[(int64_t)i * dv + j] *= ai;
@@ -172,12 +179,15 @@ static int check_dims(int N, int B, int T, int H, int dk, int dv, const int32_t*
 }
 
 /* Forward pass of Diagonal KDN over every (sequence, head); optional per-token gain traces.   */
+/* mu_t (nullable, [B,T,H]): a per-token information scale in place of mu (App. "Overwrite
+   and Protection-Write Decoupling"); beff_out (nullable, [B,T,H]): k_t^T kappa_t per token.   */
 int oracle_kdn_forward_diag(const double* q, const double* k, const double* v,
                             const double* alpha, const double* omega, const double* r,
                             const double* S0, const double* P0, double* o, double* S_T,
                             double* P_T, double* phat_out, double* kappa_out, double* p_out,
                             const int32_t* cu_seqlens, int N, int B, int T, int H, int dk,
-                            int dv, double mu, double scale, int nthreads)
+                            int dv, double mu, double scale, int nthreads, const double* mu_t,
+                            double* beff_out)
 {
     if (check_dims(N, B, T, H, dk, dv, cu_seqlens)) return -1;
     set_threads(nthreads);
@@ -198,10 +208,10 @@ int oracle_kdn_forward_diag(const double* q, const double* k, const double* v,
         for (int64_t t = 0; t < sp.len; ++t) {
             const size_t row = ((size_t)sp.b * T + sp.t0 + t) * H + h; /* (b, t, h) */
             diag_step(dk, dv, S, p, q + row * dk, k + row * dk, v + row * dv,
-                      alpha + row * dk, omega + row * dk, r[row], mu, scale,
+                      alpha + row * dk, omega + row * dk, r[row], mu_t ? mu_t[row] : mu, scale,
                       o ? o + row * dv : NULL, phat_out ? phat_out + row * dk : NULL,
                       kappa_out ? kappa_out + row * dk : NULL, p_out ? p_out + row * dk : NULL,
-                      ph, kap, delta);
+                      beff_out ? beff_out + row : NULL, ph, kap, delta);
         }
         if (S_T) memcpy(S_T + soff, S, sizeof(double) * dk * dv);
         if (P_T) memcpy(P_T + poff, p, sizeof(double) * dk);
@@ -216,7 +226,8 @@ int oracle_kdn_forward_iso(const double* q, const double* k, const double* v,
                            const double* S0, const double* P0, double* o, double* S_T,
                            double* P_T, double* bhat_out, double* beta_out, double* b_out,
                            const int32_t* cu_seqlens, int N, int B, int T, int H, int dk, int dv,
-                           int alpha_per_channel, double mu, double scale, int nthreads)
+                           int alpha_per_channel, double mu, double scale, int nthreads,
+                           const double* mu_t, double* beff_out)
 {
     if (check_dims(N, B, T, H, dk, dv, cu_seqlens)) return -1;
     set_threads(nthreads);
@@ -235,9 +246,9 @@ int oracle_kdn_forward_iso(const double* q, const double* k, const double* v,
             const size_t row = ((size_t)sp.b * T + sp.t0 + t) * H + h;
             iso_step(dk, dv, S, &b, q + row * dk, k + row * dk, v + row * dv,
                      alpha + (alpha_per_channel ? row * dk : row), alpha_per_channel,
-                     omega[row], r[row], mu, scale, o ? o + row * dv : NULL,
+                     omega[row], r[row], mu_t ? mu_t[row] : mu, scale, o ? o + row * dv : NULL,
                      bhat_out ? bhat_out + row : NULL, beta_out ? beta_out + row : NULL,
-                     b_out ? b_out + row : NULL, delta);
+                     b_out ? b_out + row : NULL, beff_out ? beff_out + row : NULL, delta);
         }
         if (S_T) memcpy(S_T + soff, S, sizeof(double) * dk * dv);
         if (P_T) P_T[poff] = b;
@@ -257,7 +268,8 @@ int oracle_kdn_decode_step(int variant, const double* q, const double* k, const 
                            const double* alpha, const double* omega, const double* r,
                            double* S, double* P, const int32_t* slot_idx, double* o, int R,
                            int num_slots, int H, int dk, int dv, int alpha_per_channel,
-                           double mu, double scale, int nthreads)
+                           double mu, double scale, int nthreads, const double* mu_t,
+                           double* beff_out)
 {
     if (R < 0 || num_slots <= 0 || H <= 0 || dk <= 0 || dv <= 0) return -1;
     if (variant != 0 && variant != 1) return -1;
@@ -277,13 +289,14 @@ int oracle_kdn_decode_step(int variant, const double* q, const double* k, const 
         double* Sl = S + ((size_t)slot * H + h) * dk * dv;
         if (variant == 0) {
             diag_step(dk, dv, Sl, P + ((size_t)slot * H + h) * dk, q + row * dk, k + row * dk,
-                      v + row * dv, alpha + row * dk, omega + row * dk, r[row], mu, scale,
-                      o + row * dv, NULL, NULL, NULL, ph, kap, delta);
+                      v + row * dv, alpha + row * dk, omega + row * dk, r[row],
+                      mu_t ? mu_t[row] : mu, scale, o + row * dv, NULL, NULL, NULL,
+                      beff_out ? beff_out + row : NULL, ph, kap, delta);
         } else {
             iso_step(dk, dv, Sl, P + (size_t)slot * H + h, q + row * dk, k + row * dk,
                      v + row * dv, alpha + (alpha_per_channel ? row * dk : row),
-                     alpha_per_channel, omega[row], r[row], mu, scale, o + row * dv, NULL, NULL,
-                     NULL, delta);
+                     alpha_per_channel, omega[row], r[row], mu_t ? mu_t[row] : mu, scale,
+                     o + row * dv, NULL, NULL, NULL, beff_out ? beff_out + row : NULL, delta);
         }
         free(buf);
     }
