@@ -142,6 +142,53 @@ size_t kdn_forward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_
                                    int32_t chunk);
 
 /*
+ * Options of the layer calls (kdn_forward_layer, kdn_decode_step_layer): the steps of the
+ * mixer layer on either side of the recurrence, fused into its kernels. A NULL options pointer,
+ * or every field zero / NULL, gives exactly the plain call.
+ *   gates_preact != 0: alpha, omega and r hold pre-activations, mapped per element as
+ *     alpha = sigmoid(x), omega = softplus(x), r = r_min + softplus(x) (eqs.
+ *     kla-box-parameterization and iso-kla-box-parameterization); r_min > 0 is then required
+ *     (the paper's experiments use 0.01). Gate pre-activations below about -10 give gates under
+ *     the forward's gate floor (see "Gates" above); below about -88 the gate is 0.
+ *   qk_l2norm != 0: q and k are divided by their L2 norms over dk, per token and head (the
+ *     normalised keys of Sec. "Delta-rule models as fixed-gain Kalman filters"); an all-zero
+ *     row stays zero.
+ *   mu_t: per-token information scale [B,T,H] ([R,H] for decode) in the call's dtype, each
+ *     value > 0 (not checked on the host), used in place of mu (eq.
+ *     appendix-protection-scale-update); NULL = the scalar mu.
+ *   beta_eff: float32 [B,T,H] ([R,H] for decode) output, the effective write strength
+ *     k_t^T kappa_t of every token (eq. appendix-effective-write): z / (r + z) with
+ *     z = sum_i p_hat_i k_i^2 for the diagonal variant, beta ||k||^2 for the isotropic one;
+ *     NULL = not written. It must not overlap any other buffer of the call
+ *     (KDN_ERR_INVALID_ARG). Entries of skipped decode rows are left untouched.
+ * All pointers are device pointers owned by the caller; the struct itself is read on the host
+ * during the call only.
+ */
+typedef struct {
+    int32_t gates_preact;
+    float r_min;
+    int32_t qk_l2norm;
+    const void* mu_t;
+    float* beta_eff;
+} kdn_layer_opts;
+
+/*
+ * The forward of either variant (variant 0 = kdn_forward_diag, 1 = kdn_forward_iso, with
+ * alpha_per_channel read for variant 1 only; chunk 64) with the layer options applied in its
+ * kernels: the maps act on the values as loaded, in float32, before anything else uses them.
+ * Arguments, outputs, workspace (kdn_forward_workspace_bytes for the same sizes) and errors are
+ * those of the plain forward, plus the option errors listed above.
+ */
+kdn_status_t kdn_forward_layer(int32_t variant, const void* q, const void* k, const void* v,
+                               const void* alpha, const void* omega, const void* r,
+                               const float* S0, const float* P0, void* o, float* S_T, float* P_T,
+                               const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T,
+                               int32_t H, int32_t dk, int32_t dv, kdn_dtype_t dtype,
+                               int32_t alpha_per_channel, float mu, float scale,
+                               const kdn_layer_opts* opts, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
  * One recurrent decode step: exactly one token of the forward recurrence per row, with the
  * state resident in a slot pool and updated in place (the paper's constant-memory decoding;
  * Prop. "Diagonal Kalman Delta Network" / Prop. "Isotropic Kalman Delta Network" for T = 1).
@@ -159,6 +206,17 @@ kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, cons
                              int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
                              kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
                              void* stream);
+
+/*
+ * kdn_decode_step with the layer options (per-row arrays [R,H]); everything else as
+ * kdn_decode_step.
+ */
+kdn_status_t kdn_decode_step_layer(int32_t variant, const void* q, const void* k, const void* v,
+                                   const void* alpha, const void* omega, const void* r, float* S,
+                                   float* P, const int32_t* slot_idx, void* o, int32_t R,
+                                   int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                                   kdn_dtype_t dtype, int32_t alpha_per_channel, float mu,
+                                   float scale, const kdn_layer_opts* opts, void* stream);
 
 /*
  * Gain scan alone (App. "Hardware-Efficient Chunkwise Algorithm", Sec. "Chunkwise Gain

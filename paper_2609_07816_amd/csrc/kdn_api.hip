@@ -155,7 +155,34 @@ kdn::FwdCall fwd_call(int variant, int apc, const void* q, const void* k, const 
     c.sa = {cu, N, B, T, H};
     c.dk = dk; c.dv = dv; c.dtype = dtype; c.mu = mu; c.scale = scale;
     c.workspace = ws;
+    c.ly = kdn::LayerOpts{false, 0, 0, 0.f, nullptr, nullptr};
     return c;
+}
+
+// Layer options from the caller's struct (NULL: all off). Checks the values and that the
+// per-token arrays of `rows` entries neither alias nor overlap the call's other buffers.
+kdn_status_t layer_opts(const kdn_layer_opts* p, size_t rows, size_t es,
+                        const void* const* bufs, const size_t* sizes, int nbufs,
+                        kdn::LayerOpts* out)
+{
+    *out = kdn::LayerOpts{false, 0, 0, 0.f, nullptr, nullptr};
+    if (!p) return KDN_OK;
+    if (p->gates_preact && !(p->r_min > 0.f))
+        return fail(KDN_ERR_INVALID_ARG, "r_min must be positive with gates_preact (r_min=%g)",
+                    p->r_min);
+    for (int i = 0; i < nbufs; ++i) {
+        if (overlaps(p->beta_eff, rows * 4, bufs[i], sizes[i]))
+            return fail(KDN_ERR_INVALID_ARG, "beta_eff overlaps argument buffer %d", i);
+    }
+    if (overlaps(p->beta_eff, rows * 4, p->mu_t, rows * es))
+        return fail(KDN_ERR_INVALID_ARG, "beta_eff overlaps mu_t");
+    out->preact = p->gates_preact ? 1 : 0;
+    out->qknorm = p->qk_l2norm ? 1 : 0;
+    out->r_min = p->r_min;
+    out->mu_t = p->mu_t;
+    out->beta_eff = p->beta_eff;
+    out->on = out->preact || out->qknorm || out->mu_t || out->beta_eff;
+    return KDN_OK;
 }
 
 }  // namespace
@@ -264,12 +291,43 @@ kdn_status_t kdn_forward_iso(const void* q, const void* k, const void* v, const 
                       "kdn_forward_iso launch");
 }
 
-kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, const void* v,
-                             const void* alpha, const void* omega, const void* r, float* S,
-                             float* P, const int32_t* slot_idx, void* o, int32_t R,
-                             int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
-                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
-                             void* stream)
+kdn_status_t kdn_forward_layer(int32_t variant, const void* q, const void* k, const void* v,
+                               const void* alpha, const void* omega, const void* r,
+                               const float* S0, const float* P0, void* o, float* S_T, float* P_T,
+                               const int32_t* cu_seqlens, int32_t N, int32_t B, int32_t T,
+                               int32_t H, int32_t dk, int32_t dv, kdn_dtype_t dtype,
+                               int32_t alpha_per_channel, float mu, float scale,
+                               const kdn_layer_opts* opts, void* workspace,
+                               size_t workspace_bytes, void* stream)
+{
+    if (variant != 0 && variant != 1)
+        return fail(KDN_ERR_INVALID_ARG, "variant must be 0 (diagonal) or 1 (isotropic)");
+    const int apc = (variant == 0 || alpha_per_channel) ? 1 : 0;
+    kdn_status_t st = check_forward(variant, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T,
+                                    cu_seqlens, N, B, T, H, dk, dv, dtype, apc, mu, scale, 0,
+                                    workspace, workspace_bytes);
+    if (st != KDN_OK) return st;
+    const size_t rows = (size_t)B * T * H, es = esize(dtype);
+    const size_t nk = rows * dk * es, nv = rows * dv * es;
+    const void* bufs[10] = {q, k, v, alpha, omega, r, o, S_T, P_T, workspace};
+    const size_t bsz[10] = {nk, nk, nv, apc ? nk : rows * es, variant == 0 ? nk : rows * es,
+                            rows * es, nv, (size_t)N * H * dk * dv * 4,
+                            (size_t)N * H * (variant == 0 ? dk : 1) * 4, workspace_bytes};
+    kdn::LayerOpts ly;
+    st = layer_opts(opts, rows, es, bufs, bsz, 10, &ly);
+    if (st != KDN_OK) return st;
+    kdn::FwdCall fc = fwd_call(variant, apc, q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T,
+                               cu_seqlens, N, B, T, H, dk, dv, dtype, mu, scale, workspace);
+    fc.ly = ly;
+    return hip_status(kdn::launch_chunked(fc, (hipStream_t)stream), "kdn_forward_layer launch");
+}
+
+static kdn_status_t decode_common(int32_t variant, const void* q, const void* k, const void* v,
+                                  const void* alpha, const void* omega, const void* r, float* S,
+                                  float* P, const int32_t* slot_idx, void* o, int32_t R,
+                                  int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                                  kdn_dtype_t dtype, int32_t alpha_per_channel, float mu,
+                                  float scale, const kdn_layer_opts* opts, void* stream)
 {
     if (variant != 0 && variant != 1)
         return fail(KDN_ERR_INVALID_ARG, "variant must be 0 (diagonal) or 1 (isotropic)");
@@ -300,11 +358,39 @@ kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, cons
     if (overlaps(o, rows * dv * es, S, ns) || overlaps(o, rows * dv * es, P, np) ||
         overlaps(S, ns, P, np))
         return fail(KDN_ERR_INVALID_ARG, "o, S and P must not overlap");
+    const void* bufs[9] = {q, k, v, alpha, omega, r, o, S, P};
+    const size_t bsz[9] = {insz[0], insz[1], insz[2], insz[3], insz[4], insz[5],
+                           rows * dv * es, ns, np};
+    kdn::LayerOpts ly;
+    kdn_status_t st = layer_opts(opts, rows, es, bufs, bsz, 9, &ly);
+    if (st != KDN_OK) return st;
     return hip_status(kdn::launch_decode(variant, q, k, v, alpha, omega, r, S, P, slot_idx, o, R,
                                          num_slots, H, dk, dv, dtype,
-                                         alpha_per_channel ? 1 : 0, mu, scale,
+                                         alpha_per_channel ? 1 : 0, mu, scale, ly,
                                          (hipStream_t)stream),
                       "kdn_decode_step launch");
+}
+
+kdn_status_t kdn_decode_step(int32_t variant, const void* q, const void* k, const void* v,
+                             const void* alpha, const void* omega, const void* r, float* S,
+                             float* P, const int32_t* slot_idx, void* o, int32_t R,
+                             int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, int32_t alpha_per_channel, float mu, float scale,
+                             void* stream)
+{
+    return decode_common(variant, q, k, v, alpha, omega, r, S, P, slot_idx, o, R, num_slots, H,
+                         dk, dv, dtype, alpha_per_channel, mu, scale, nullptr, stream);
+}
+
+kdn_status_t kdn_decode_step_layer(int32_t variant, const void* q, const void* k, const void* v,
+                                   const void* alpha, const void* omega, const void* r, float* S,
+                                   float* P, const int32_t* slot_idx, void* o, int32_t R,
+                                   int32_t num_slots, int32_t H, int32_t dk, int32_t dv,
+                                   kdn_dtype_t dtype, int32_t alpha_per_channel, float mu,
+                                   float scale, const kdn_layer_opts* opts, void* stream)
+{
+    return decode_common(variant, q, k, v, alpha, omega, r, S, P, slot_idx, o, R, num_slots, H,
+                         dk, dv, dtype, alpha_per_channel, mu, scale, opts, stream);
 }
 
 static kdn_status_t gain_common(int variant, const void* k, const void* alpha, const void* omega,

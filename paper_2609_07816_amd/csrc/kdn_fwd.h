@@ -134,6 +134,11 @@ struct InArgs {
     uint32_t bytes_k, bytes_h;  // bytes of a channel tensor [.., H, DK], of a per-head [.., H]
     int H;
     float mu;
+    // read by the layer kernels only (LAYER = true)
+    const void* mu_t;  // per-token information scale [.., H], or nullptr (mu)
+    float* beta_eff;   // k^T kappa per token [.., H] float32, or nullptr
+    float r_min;
+    int preact, qknorm;
 };
 
 // Descriptors and byte strides of one workgroup's inputs.
@@ -220,20 +225,73 @@ __device__ __forceinline__ TokIn tok_in(const SegIn<TI, CF, WQ>& in, int j, int 
     return r;
 }
 
+// The layer's maps on one token held by a variance lane (layer kernels): gates and noise from
+// pre-activations, q and k divided by their L2 norms over the head (wave sums over the active
+// lanes; a zero row stays zero). Padding tokens keep their neutral values.
+template <class CF, bool WQ>
+__device__ __forceinline__ void layer_tok(TokIn& x, const InArgs& a, bool vact, bool pad)
+{
+    if (a.preact && !pad) {
+        if constexpr (CF::APC) {
+            x.A = make_float2(gate_sigmoid(x.A.x), gate_sigmoid(x.A.y));
+        } else {
+            const float g = gate_sigmoid(x.A.x);
+            x.A = make_float2(g, g);
+        }
+        if constexpr (CF::DIAG) {
+            x.W = make_float2(gate_softplus(x.W.x), gate_softplus(x.W.y));
+        } else {
+            const float g = gate_softplus(x.W.x);
+            x.W = make_float2(g, g);
+        }
+    }
+    if (a.qknorm) {
+        const float nk = wave_sum(vact ? fmaf(x.K.x, x.K.x, x.K.y * x.K.y) : 0.f);
+        const float ik = nk > 0.f ? __builtin_amdgcn_rsqf(nk) : 0.f;
+        x.K = make_float2(x.K.x * ik, x.K.y * ik);
+        if constexpr (WQ) {
+            const float nq = wave_sum(vact ? fmaf(x.Q.x, x.Q.x, x.Q.y * x.Q.y) : 0.f);
+            const float iq = nq > 0.f ? __builtin_amdgcn_rsqf(nq) : 0.f;
+            x.Q = make_float2(x.Q.x * iq, x.Q.y * iq);
+        }
+    }
+}
+
+// r and mu / r of the chunk's tokens (tid < C), with the layer's map of r and the per-token
+// information scale in the layer kernels. Tokens past the chunk read r = 1 and mu / r = 0.
+template <class TI, bool LAYER>
+__device__ __forceinline__ void load_r(const InArgs& a, const Src& sr, int c0, int c1, int tid,
+                                       float* s_r, float* s_mr)
+{
+    const int tok = c0 + tid;
+    const uint32_t off = (uint32_t)tok * sr.rowh + sr.lane_h;
+    float rv = Raw1<TI>::f32(Raw1<TI>::load(sr.r, off));
+    float mu = a.mu;
+    if constexpr (LAYER) {
+        if (a.preact) rv = a.r_min + gate_softplus(rv);
+        if (a.mu_t) mu = Raw1<TI>::f32(Raw1<TI>::load(make_rsrc(a.mu_t, a.bytes_h), off));
+    }
+    const bool ok = tok < c1;
+    if (s_r) s_r[tid] = ok ? rv : 1.f;
+    s_mr[tid] = ok ? mu / rv : 0.f;
+}
+
 // The block's Moebius product (later tokens on the left) and decay product. Diagonal: per
 // channel of the lane's pair (m0, m1). Isotropic: one chain per head, every lane alike, with
 // the per-token ||k||^2 and mean alpha^2 (wave reductions) returned in kn, ka.
-template <bool MK, class TI, class CF, bool WQ>
+template <bool MK, bool LAYER, class TI, class CF, bool WQ>
 __device__ __forceinline__ void block_summary(const SegIn<TI, CF, WQ>& in, int Lw,
                                               const float* s_mr, bool vact, float* m0, float* m1,
-                                              float2& gseg, float* kn, float* ka)
+                                              float2& gseg, float* kn, float* ka,
+                                              const InArgs& a)
 {
     m0[0] = 1.f; m0[1] = 0.f; m0[2] = 0.f; m0[3] = 1.f;
     m1[0] = 1.f; m1[1] = 0.f; m1[2] = 0.f; m1[3] = 1.f;
     float g0 = 1.f, g1 = 1.f;
 #pragma unroll
     for (int j = 0; j < SL; ++j) {
-        const TokIn x = tok_in<MK>(in, j, Lw);
+        TokIn x = tok_in<MK>(in, j, Lw);
+        if constexpr (LAYER) layer_tok<CF, WQ>(x, a, vact, MK && j >= Lw);
         const float mr = s_mr[j];
         if constexpr (CF::DIAG) {
             mob_left(m0, x.A.x * x.A.x, x.W.x, x.K.x * x.K.x * mr);
@@ -260,9 +318,9 @@ __device__ __forceinline__ void block_summary(const SegIn<TI, CF, WQ>& in, int L
 // ------------------------------------------------------------------------------------------
 // 1. chunk summaries
 // ------------------------------------------------------------------------------------------
-template <class TI, class CF>
-__global__ __launch_bounds__(NTH) void summary_kernel(InArgs a, ChunkMap cm,
-                                                      float4* __restrict__ summ)
+template <class TI, class CF, bool LAYER>
+__device__ __forceinline__ void summary_body(const InArgs& a, const ChunkMap& cm,
+                                             float4* __restrict__ summ)
 {
     constexpr int DK = CF::DK, NP = CF::NP;
     __shared__ float4 segA[NB][CF::NCHAN];
@@ -276,19 +334,15 @@ __global__ __launch_bounds__(NTH) void summary_kernel(InArgs a, ChunkMap cm,
     const int pc = min(lane, NP - 1), ch = 2 * pc;
     const bool vact = lane < NP;
     const Src sr = make_src<TI, CF>(a, h, ch);
-    if (tid < C) {
-        const int tok = c0 + tid;
-        const float rv = Raw1<TI>::f32(Raw1<TI>::load(sr.r, (uint32_t)tok * sr.rowh + sr.lane_h));
-        s_mr[tid] = tok < c1 ? a.mu / rv : 0.f;
-    }
+    if (tid < C) load_r<TI, LAYER>(a, sr, c0, c1, tid, nullptr, s_mr);
     SegIn<TI, CF, false> in;
     load_seg(in, sr, (uint32_t)(c0 + SL * w));
     __syncthreads();
     const int Lw = c1 - (c0 + SL * w);
     float m0[4], m1[4], kn[CF::DIAG ? 1 : SL], ka[CF::DIAG ? 1 : SL];
     float2 gs;
-    if (Lw < SL) block_summary<true>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka);
-    else block_summary<false>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka);
+    if (Lw < SL) block_summary<true, LAYER>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka, a);
+    else block_summary<false, LAYER>(in, Lw, s_mr + SL * w, vact, m0, m1, gs, kn, ka, a);
     if constexpr (CF::DIAG) {
         if (vact) {
             segA[w][ch] = make_float4(m0[0], m0[1], m0[2], m0[3]);
@@ -305,6 +359,22 @@ __global__ __launch_bounds__(NTH) void summary_kernel(InArgs a, ChunkMap cm,
         summ[((size_t)g * a.H + h) * CF::NCHAN + tid] = m;
     }
     (void)DK;
+}
+
+// The plain bf16 summary asks for six waves per SIMD: 16 workgroups per CU at the
+// 4 x 4096 x 16 shape then run in three rounds.
+template <class TI, class CF>
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(sizeof(TI) == 2 ? 6 : 4)))
+void summary_kernel(InArgs a, ChunkMap cm, float4* __restrict__ summ)
+{
+    summary_body<TI, CF, false>(a, cm, summ);
+}
+
+template <class TI, class CF>
+__global__ __launch_bounds__(NTH) void summary_layer_kernel(InArgs a, ChunkMap cm,
+                                                            float4* __restrict__ summ)
+{
+    summary_body<TI, CF, true>(a, cm, summ);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -370,8 +440,8 @@ __device__ __forceinline__ void pair_prod(const MT* Ka, const MT* Qa, const MT* 
     }
 }
 
-template <class TI, class CF>
-__global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
+template <class TI, class CF, bool LAYER>
+__device__ __forceinline__ void prep_body(const PrepArgs& a)
 {
     using MT = typename CF::MT;
     using Rec = OpRec<MT, CF::DK>;
@@ -409,13 +479,7 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
     float* gC = (float*)(rec + Rec::OFF_GC);
 
     const Src sr = make_src<TI, CF>(a.in, h, ch);
-    if (tid < C) {
-        const int tok = c0 + tid;
-        const float rv = Raw1<TI>::f32(Raw1<TI>::load(sr.r, (uint32_t)tok * sr.rowh + sr.lane_h));
-        const bool ok = tok < c1;
-        s_r[tid] = ok ? rv : 1.f;
-        s_mr[tid] = ok ? a.in.mu / rv : 0.f;
-    }
+    if (tid < C) load_r<TI, LAYER>(a.in, sr, c0, c1, tid, s_r, s_mr);
     const int Lw = c1 - (c0 + SL * w);  // tokens of this block in the sequence (may be <= 0)
     // the block's tokens in float32, unpacked once
     float2 Kf[SL], Qf[SL], Af[SL], Wf[SL];
@@ -424,7 +488,8 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
         load_seg(in, sr, (uint32_t)(c0 + SL * w));
 #pragma unroll
         for (int j = 0; j < SL; ++j) {
-            const TokIn x = tok_in<true>(in, j, Lw);
+            TokIn x = tok_in<true>(in, j, Lw);
+            if constexpr (LAYER) layer_tok<CF, true>(x, a.in, vact, j >= Lw);
             Kf[j] = x.K;
             Qf[j] = x.Q;
             Af[j] = x.A;
@@ -513,6 +578,14 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
             const float nn1 = fmaf(Af[j].y * Af[j].y, n1, Wf[j].y * d1);
             pk[j] = make_float2(nn0 * Kf[j].x * __builtin_amdgcn_rcpf(d0),
                                 nn1 * Kf[j].y * __builtin_amdgcn_rcpf(d1));
+            if constexpr (LAYER) {
+                if (a.in.beta_eff) {  // k^T kappa = z / (r + z), z = sum_i p_hat_i k_i^2
+                    const float z = wave_sum(vact ? fmaf(pk[j].x, Kf[j].x, pk[j].y * Kf[j].y)
+                                                  : 0.f);
+                    if (lane == 0 && j < Lw)
+                        a.in.beta_eff[(size_t)(c0 + t) * H + h] = z / (s_r[t] + z);
+                }
+            }
             d0 = fmaf(Kf[j].x * Kf[j].x * mr, nn0, d0);
             d1 = fmaf(Kf[j].y * Kf[j].y * mr, nn1, d1);
             n0 = nn0;
@@ -525,6 +598,10 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
             const float nn = fmaf(ka[j], n0, Wf[j].x * d0);  // b_hat d
             const float beta = nn / fmaf(d0, s_r[t], nn * kn[j]);
             pk[j] = make_float2(beta * Kf[j].x, beta * Kf[j].y);
+            if constexpr (LAYER) {
+                if (a.in.beta_eff && lane == 0 && j < Lw)  // k^T (beta k)
+                    a.in.beta_eff[(size_t)(c0 + t) * H + h] = beta * kn[j];
+            }
             d0 = fmaf(kn[j] * s_mr[t] * (1.f / (float)DK), nn, d0);
             n0 = nn;
             if ((j & 3) == 3) rescale2(n0, d0);
@@ -761,6 +838,21 @@ __global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
     __syncthreads();
     copy_frag_order<MT, C, DK, NTH>(gKb, Ka, LDK, tid);
     copy_frag_order<MT, C, DK, NTH>(gQb, Qa, LDK, tid);
+}
+
+template <class TI, class CF>
+__global__ __launch_bounds__(NTH) void prep_kernel(PrepArgs a)
+{
+    prep_body<TI, CF, false>(a);
+}
+
+// bf16: two workgroups per CU, as the plain prep (the LDS allows two; the layer maps must not
+// push the registers past that)
+template <class TI, class CF>
+__global__ __launch_bounds__(NTH) __attribute__((amdgpu_waves_per_eu(sizeof(TI) == 2 ? 2 : 1)))
+void prep_layer_kernel(PrepArgs a)
+{
+    prep_body<TI, CF, true>(a);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -1106,7 +1198,7 @@ hipError_t set_lds(K* kernel, size_t bytes)
                                (int)bytes);
 }
 
-template <class TI, int DK, int DV, int VARIANT, bool APC>
+template <class TI, bool LAYER, int DK, int DV, int VARIANT, bool APC>
 hipError_t run_t(const FwdCall& fc, hipStream_t st)
 {
     using VC = VarCfg<TI, DK, VARIANT, APC>;
@@ -1145,17 +1237,29 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
     in.bytes_h = (uint32_t)(ntok * sizeof(TI));
     in.H = sa.H;
     in.mu = fc.mu;
+    in.mu_t = fc.ly.mu_t;
+    in.beta_eff = fc.ly.beta_eff;
+    in.r_min = fc.ly.r_min;
+    in.preact = fc.ly.preact;
+    in.qknorm = fc.ly.qknorm;
     float4* summ = (float4*)(ws + wm.summ);
     float2* carry = (float2*)(ws + wm.carry);
     const dim3 cgrid((unsigned)((size_t)wm.maxch * sa.H));
-    hipLaunchKernelGGL((summary_kernel<TI, VC>), cgrid, dim3(NTH), 0, st, in, cm, summ);
+    if constexpr (LAYER)
+        hipLaunchKernelGGL((summary_layer_kernel<TI, VC>), cgrid, dim3(NTH), 0, st, in, cm, summ);
+    else
+        hipLaunchKernelGGL((summary_kernel<TI, VC>), cgrid, dim3(NTH), 0, st, in, cm, summ);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_carry_scan(summ, fc.P0, cm, C, sa.H, VC::NCHAN, carry, fc.P_T, st)) !=
         hipSuccess)
         return e;
+    void (*prep)(PrepArgs) = [] {
+        if constexpr (LAYER) return &prep_layer_kernel<TI, PC>;
+        else return &prep_kernel<TI, PC>;
+    }();
     static bool attr_done = false;
     if (!attr_done) {
-        if ((e = set_lds(prep_kernel<TI, PC>, PC::TOTAL)) != hipSuccess) return e;
+        if ((e = set_lds(prep, PC::TOTAL)) != hipSuccess) return e;
         if ((e = set_lds(walk_kernel<TI, WC>, WC::TOTAL)) != hipSuccess) return e;
         attr_done = true;
     }
@@ -1165,7 +1269,7 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
     pa.carry = carry;
     pa.ops = ws + wm.ops;
     pa.P_T = fc.P_T;
-    hipLaunchKernelGGL((prep_kernel<TI, PC>), cgrid, dim3(NTH), PC::TOTAL, st, pa);
+    hipLaunchKernelGGL(prep, cgrid, dim3(NTH), PC::TOTAL, st, pa);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     WalkArgs wa;
     wa.v = fc.v;
@@ -1184,41 +1288,44 @@ hipError_t run_t(const FwdCall& fc, hipStream_t st)
     return hipGetLastError();
 }
 
-template <class TI, int DK, int DV>
+template <class TI, bool LAYER, int DK, int DV>
 hipError_t run_variant(const FwdCall& fc, hipStream_t st)
 {
-    if (fc.variant == 0) return run_t<TI, DK, DV, 0, true>(fc, st);
-    if (fc.apc) return run_t<TI, DK, DV, 1, true>(fc, st);
-    return run_t<TI, DK, DV, 1, false>(fc, st);
+    if (fc.variant == 0) return run_t<TI, LAYER, DK, DV, 0, true>(fc, st);
+    if (fc.apc) return run_t<TI, LAYER, DK, DV, 1, true>(fc, st);
+    return run_t<TI, LAYER, DK, DV, 1, false>(fc, st);
 }
 
-template <class TI, int DK>
+template <class TI, bool LAYER, int DK>
 hipError_t run_dv(const FwdCall& fc, hipStream_t st)
 {
     switch (fc.dv) {
-    case 16: return run_variant<TI, DK, 16>(fc, st);
-    case 32: return run_variant<TI, DK, 32>(fc, st);
-    case 64: return run_variant<TI, DK, 64>(fc, st);
-    case 128: return run_variant<TI, DK, 128>(fc, st);
+    case 16: return run_variant<TI, LAYER, DK, 16>(fc, st);
+    case 32: return run_variant<TI, LAYER, DK, 32>(fc, st);
+    case 64: return run_variant<TI, LAYER, DK, 64>(fc, st);
+    case 128: return run_variant<TI, LAYER, DK, 128>(fc, st);
     }
     return hipErrorInvalidValue;
 }
 
-template <class TI>
+template <class TI, bool LAYER>
 hipError_t run_forward(const FwdCall& fc, hipStream_t st)
 {
     switch (fc.dk) {
-    case 16: return run_dv<TI, 16>(fc, st);
-    case 32: return run_dv<TI, 32>(fc, st);
-    case 64: return run_dv<TI, 64>(fc, st);
-    case 128: return run_dv<TI, 128>(fc, st);
+    case 16: return run_dv<TI, LAYER, 16>(fc, st);
+    case 32: return run_dv<TI, LAYER, 32>(fc, st);
+    case 64: return run_dv<TI, LAYER, 64>(fc, st);
+    case 128: return run_dv<TI, LAYER, 128>(fc, st);
     }
     return hipErrorInvalidValue;
 }
 
-// instantiated once per dtype, in kdn_fwd_bf16.hip and kdn_fwd_f32.hip
-extern template hipError_t run_forward<float>(const FwdCall& fc, hipStream_t st);
-extern template hipError_t run_forward<bf16>(const FwdCall& fc, hipStream_t st);
+// instantiated once per dtype and mode, in kdn_fwd_{bf16,f32}.hip (the plain forward) and
+// kdn_fwd_layer_{bf16,f32}.hip (the layer forward)
+extern template hipError_t run_forward<float, false>(const FwdCall& fc, hipStream_t st);
+extern template hipError_t run_forward<bf16, false>(const FwdCall& fc, hipStream_t st);
+extern template hipError_t run_forward<float, true>(const FwdCall& fc, hipStream_t st);
+extern template hipError_t run_forward<bf16, true>(const FwdCall& fc, hipStream_t st);
 
 }  // namespace fwd
 }  // namespace kdn

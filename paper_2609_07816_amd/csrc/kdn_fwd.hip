@@ -1,5 +1,6 @@
-// Host entry of the chunked forward: chunk support, workspace size and the dtype dispatch to
-// the instantiations in kdn_fwd_bf16.hip and kdn_fwd_f32.hip (kernels in kdn_fwd.h).
+// Host entry of the chunked forward: chunk support, workspace size and the dispatch to the
+// instantiations per dtype and mode in kdn_fwd_{bf16,f32}.hip and kdn_fwd_layer_{bf16,f32}.hip
+// (kernels in kdn_fwd.h).
 #include "kdn_fwd.h"
 
 namespace kdn {
@@ -35,8 +36,12 @@ size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, in
 
 hipError_t launch_chunked(const FwdCall& fc, hipStream_t stream)
 {
-    if (fc.dtype == KDN_F32) return fwd::run_forward<float>(fc, stream);
-    return fwd::run_forward<bf16>(fc, stream);
+    if (fc.ly.on) {
+        if (fc.dtype == KDN_F32) return fwd::run_forward<float, true>(fc, stream);
+        return fwd::run_forward<bf16, true>(fc, stream);
+    }
+    if (fc.dtype == KDN_F32) return fwd::run_forward<float, false>(fc, stream);
+    return fwd::run_forward<bf16, false>(fc, stream);
 }
 
 }  // namespace kdn

@@ -3,6 +3,6 @@
 
 namespace kdn {
 namespace fwd {
-template hipError_t run_forward<bf16>(const FwdCall& fc, hipStream_t st);
+template hipError_t run_forward<bf16, false>(const FwdCall& fc, hipStream_t st);
 }  // namespace fwd
 }  // namespace kdn

@@ -64,6 +64,36 @@ __device__ __forceinline__ void renorm4(float& a, float& b, float& c, float& d)
 }
 
 // ------------------------------------------------------------------------------------------
+// the mixer layer's input maps (eqs. kla-box-parameterization and iso-kla-box-parameterization):
+// alpha = sigmoid(.), omega = softplus(.), r = r_min + softplus(.) of pre-activations
+// ------------------------------------------------------------------------------------------
+__device__ __forceinline__ float gate_sigmoid(float x)
+{
+    // 1 / (1 + e^-x): e^-x overflows to +inf for x < -88 and the result is then 0
+    return __builtin_amdgcn_rcpf(1.f + __expf(-x));
+}
+
+__device__ __forceinline__ float gate_softplus(float x)
+{
+    // max(x, 0) + log1p(e^-|x|). log1p(e) for e in (0, 1] as log(u) e / (u - 1) with u = 1 + e
+    // rounded (Goldberg's correction: it cancels the rounding of 1 + e), and e itself when u
+    // rounds to 1.
+    const float e = __expf(-fabsf(x));
+    const float u = 1.f + e;
+    const float l = u == 1.f ? e : __logf(u) * (e * __builtin_amdgcn_rcpf(u - 1.f));
+    return fmaxf(x, 0.f) + l;
+}
+
+// Options of the layer-mode calls (kdn_forward_layer, kdn_decode_step_layer).
+struct LayerOpts {
+    bool on;             // any of the below (the forward then runs its layer kernels)
+    int preact, qknorm;  // gates from pre-activations; q and k divided by their L2 norms
+    float r_min;
+    const void* mu_t;    // per-token information scale [.., H] (dtype), or nullptr
+    float* beta_eff;     // k^T kappa per token [.., H] float32, or nullptr
+};
+
+// ------------------------------------------------------------------------------------------
 // host-side launchers implemented in the kernel sources
 // ------------------------------------------------------------------------------------------
 struct SeqArgs {
@@ -75,7 +105,7 @@ hipError_t launch_decode(int variant, const void* q, const void* k, const void* 
                          const void* alpha, const void* omega, const void* r, float* S, float* P,
                          const int32_t* slot_idx, void* o, int R, int num_slots, int H, int dk,
                          int dv, kdn_dtype_t dtype, int alpha_per_channel, float mu, float scale,
-                         hipStream_t stream);
+                         const LayerOpts& ly, hipStream_t stream);
 
 size_t gain_workspace_bytes(int variant, int N, int B, int T, int H, int dk);
 hipError_t launch_gain(int variant, const void* k, const void* alpha, const void* omega,
@@ -96,6 +126,7 @@ struct FwdCall {
     kdn_dtype_t dtype;
     float mu, scale;
     void* workspace;  // chunked_workspace_bytes(...) bytes
+    LayerOpts ly;
 };
 bool chunked_supported(int chunk);
 size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,

@@ -14,6 +14,10 @@ Functions mirror the C entry points:
   -> o`` (S and P updated in place)
 * ``gain_diag(k, alpha, omega, r, P0=None, cu_seqlens=None, mu=None) -> (kappa, phat, P_T)``
 * ``gain_iso(...) -> (beta, bhat, P_T)``
+* ``forward_layer(variant, q, k, v, alpha, omega, r, ..., gates_preact=False, r_min=0.01,
+  qk_l2norm=False, mu_t=None, want_beta_eff=False) -> (o, S_T, P_T, beta_eff or None)``
+* ``decode_step_layer(variant, ..., gates_preact=False, r_min=0.01, qk_l2norm=False,
+  mu_t=None, beta_eff=None) -> o``
 """
 
 from __future__ import annotations
@@ -33,6 +37,13 @@ KDN_OK, KDN_ERR_INVALID_ARG, KDN_ERR_UNSUPPORTED, KDN_ERR_WORKSPACE, KDN_ERR_HIP
 KDN_F32, KDN_BF16 = 0, 1
 
 _lib = None
+
+
+class LayerOpts(ctypes.Structure):
+    """kdn_layer_opts of include/kdn.h."""
+    _fields_ = [("gates_preact", ctypes.c_int32), ("r_min", ctypes.c_float),
+                ("qk_l2norm", ctypes.c_int32), ("mu_t", ctypes.c_void_p),
+                ("beta_eff", ctypes.c_void_p)]
 
 
 class KdnError(RuntimeError):
@@ -67,10 +78,17 @@ def lib():
                                                                    vp]
     L.kdn_gain_diag.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, f32, vp, sz, vp]
     L.kdn_gain_iso.argtypes = [vp] * 9 + [i32] * 5 + [ctypes.c_int, i32, f32, vp, sz, vp]
+    L.kdn_forward_layer.argtypes = [i32] + [vp] * 12 + [i32] * 6 + [ctypes.c_int, i32, f32, f32,
+                                                                     ctypes.POINTER(LayerOpts),
+                                                                     vp, sz, vp]
+    L.kdn_decode_step_layer.argtypes = ([i32] + [vp] * 10 + [i32] * 5 +
+                                        [ctypes.c_int, i32, f32, f32, ctypes.POINTER(LayerOpts),
+                                         vp])
     L.kdn_forward_workspace_bytes.argtypes = [i32] * 7 + [ctypes.c_int, i32, i32]
     L.kdn_gain_workspace_bytes.argtypes = [i32] * 6
     for name in ("kdn_forward_diag", "kdn_forward_iso", "kdn_forward_diag_noalloc",
-                 "kdn_decode_step", "kdn_gain_diag", "kdn_gain_iso"):
+                 "kdn_decode_step", "kdn_gain_diag", "kdn_gain_iso", "kdn_forward_layer",
+                 "kdn_decode_step_layer"):
         getattr(L, name).restype = ctypes.c_int
     L.kdn_forward_workspace_bytes.restype = sz
     L.kdn_gain_workspace_bytes.restype = sz
@@ -244,3 +262,74 @@ def gain_diag(k, alpha, omega, r, P0=None, cu_seqlens=None, mu=None, want_phat=T
 def gain_iso(k, alpha, omega, r, P0=None, cu_seqlens=None, mu=None, want_phat=True):
     """Gain scan alone (isotropic): returns (beta, bhat or None, P_T)."""
     return _gain(1, k, alpha, omega, r, P0, cu_seqlens, mu, want_phat)
+
+
+def _layer_opts(gates_preact, r_min, qk_l2norm, mu_t, beta_eff):
+    return LayerOpts(int(bool(gates_preact)), float(r_min), int(bool(qk_l2norm)),
+                     None if mu_t is None else mu_t.data_ptr(),
+                     None if beta_eff is None else beta_eff.data_ptr())
+
+
+def forward_layer(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
+                  scale=None, gates_preact=False, r_min=0.01, qk_l2norm=False, mu_t=None,
+                  want_beta_eff=False):
+    """The forward with the layer options (variant "diag" or "iso"); alpha, omega and r are
+    pre-activations when gates_preact. Returns (o, S_T, P_T, beta_eff or None)."""
+    vid = {"diag": 0, "iso": 1}[variant] if isinstance(variant, str) else int(variant)
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    _same(k.dtype, q, v, alpha, omega, r, mu_t)
+    dev = k.device
+    N = B if cu_seqlens is None else cu_seqlens.numel() - 1
+    mu = float(dk if mu is None else mu)
+    scale = float(dk ** -0.5 if scale is None else scale)
+    if cu_seqlens is not None and cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    if mu_t is not None:
+        _ptr(mu_t)
+    o = torch.empty((B, T, H, dv), dtype=k.dtype, device=dev)
+    S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
+    P_T = torch.empty((N, H, dk) if vid == 0 else (N, H), dtype=torch.float32, device=dev)
+    beff = torch.empty((B, T, H), dtype=torch.float32, device=dev) if want_beta_eff else None
+    ws_bytes = lib().kdn_forward_workspace_bytes(vid, N, B, T, H, dk, dv, _dtype_code(k),
+                                                 int(cu_seqlens is not None), 0)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev) if ws_bytes else None
+    opts = _layer_opts(gates_preact, r_min, qk_l2norm, mu_t, beff)
+    apc = int(vid == 0 or alpha.dim() == 4)
+    st = lib().kdn_forward_layer(vid, _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(omega),
+                                 _ptr(r), _ptr(_f32(S0)), _ptr(_f32(P0)), _ptr(o), _ptr(S_T),
+                                 _ptr(P_T), _ptr(cu_seqlens), N, B, T, H, dk, dv, _dtype_code(k),
+                                 apc, ctypes.c_float(mu), ctypes.c_float(scale),
+                                 ctypes.byref(opts), _ptr(ws), ws_bytes, _stream(dev))
+    _check(st, "kdn_forward_layer")
+    return o, S_T, P_T, beff
+
+
+def decode_step_layer(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None,
+                      scale=None, o=None, gates_preact=False, r_min=0.01, qk_l2norm=False,
+                      mu_t=None, beta_eff=None):
+    """One decode step with the layer options; S, P (and beta_eff [R,H] float32 when given)
+    updated in place; returns o."""
+    vid = {"diag": 0, "iso": 1}[variant] if isinstance(variant, str) else int(variant)
+    R, H, dk = k.shape
+    dv = v.shape[-1]
+    _same(k.dtype, q, v, alpha, omega, r, mu_t)
+    if o is None:
+        o = torch.empty((R, H, dv), dtype=k.dtype, device=k.device)
+    if slot_idx is not None and slot_idx.dtype != torch.int32:
+        raise TypeError("slot_idx must be int32")
+    if beta_eff is not None and (beta_eff.dtype != torch.float32 or not beta_eff.is_contiguous()):
+        raise TypeError("beta_eff must be a contiguous float32 tensor")
+    if mu_t is not None:
+        _ptr(mu_t)
+    mu = float(dk if mu is None else mu)
+    scale = float(dk ** -0.5 if scale is None else scale)
+    apc = int(alpha.dim() == 3)
+    opts = _layer_opts(gates_preact, r_min, qk_l2norm, mu_t, beta_eff)
+    st = lib().kdn_decode_step_layer(vid, _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(omega),
+                                     _ptr(r), _ptr(_f32(S)), _ptr(_f32(P)), _ptr(slot_idx),
+                                     _ptr(o), R, S.shape[0], H, dk, dv, _dtype_code(k), apc,
+                                     ctypes.c_float(mu), ctypes.c_float(scale),
+                                     ctypes.byref(opts), _stream(k.device))
+    _check(st, "kdn_decode_step_layer")
+    return o

@@ -191,6 +191,44 @@ def draw_inputs(variant: str, dtype: str, B: int, T: int, H: int, dk: int, dv: i
                      scale=float(dk ** -0.5 if scale is None else scale))
 
 
+SID_MU_T = 9
+
+
+def draw_layer_inputs(variant: str, dtype: str, B: int, T: int, H: int, dk: int, dv: int, *,
+                      seed: int, stream: int = 0, alpha_per_channel: bool = True,
+                      lengths: Optional[Sequence[int]] = None, random_state: bool = False,
+                      mu_t: bool = False) -> KdnInputs:
+    """One batch of the layer's inputs, before the layer's maps: the stored "alpha", "omega"
+    and "r" are pre-activations and q, k are not normalised.
+
+    * q, k ~ N(0, 1) per element times a per-(token, head) scale ~ U(0.25, 4), so that rows of
+      very different norms reach the normalisation;
+    * gate pre-activations ~ N(2, 1) (their sigmoid has the law of the plain workloads' gates);
+    * process- and observation-noise pre-activations ~ N(0, 1);
+    * with ``mu_t`` a per-token information scale ~ U(dk / 4, 2 dk), stored as "mu_t".
+    Everything else (v, lengths, S0, P0, mu, scale) is drawn as in ``draw_inputs``.
+    """
+    x = draw_inputs(variant, dtype, B, T, H, dk, dv, seed=seed, stream=stream,
+                    alpha_per_channel=alpha_per_channel, lengths=lengths,
+                    random_state=random_state)
+    g = _rng(seed, stream + 1, SID_Q)
+    scale_q = g.uniform(0.25, 4.0, (B, T, H, 1))
+    x.stored["q"] = round_to(g.standard_normal((B, T, H, dk)) * scale_q, dtype)
+    g = _rng(seed, stream + 1, SID_K)
+    scale_k = g.uniform(0.25, 4.0, (B, T, H, 1))
+    x.stored["k"] = round_to(g.standard_normal((B, T, H, dk)) * scale_k, dtype)
+    ashape = x.stored["alpha"].shape
+    x.stored["alpha"] = round_to(_rng(seed, stream + 1, SID_ALPHA).standard_normal(ashape) + 2.0,
+                                 dtype)
+    oshape = x.stored["omega"].shape
+    x.stored["omega"] = round_to(_rng(seed, stream + 1, SID_OMEGA).standard_normal(oshape), dtype)
+    x.stored["r"] = round_to(_rng(seed, stream + 1, SID_R).standard_normal((B, T, H)), dtype)
+    if mu_t:
+        x.stored["mu_t"] = round_to(_rng(seed, stream + 1, SID_MU_T).uniform(dk / 4, 2 * dk,
+                                                                              (B, T, H)), dtype)
+    return x
+
+
 def draw_lengths(n: int, lo: int, hi: int, seed: int, stream: int = 0) -> np.ndarray:
     """Sequence lengths uniform on the integers [lo, hi]."""
     return _rng(seed, stream, SID_LEN).integers(lo, hi + 1, size=n)

@@ -145,3 +145,27 @@ def test_workspace_queries(L):
     small = L.kdn_gain_workspace_bytes(0, 1, 1, 64, 1, 128)
     big = L.kdn_gain_workspace_bytes(0, 4, 4, 4096, 16, 128)
     assert big > small > 0
+
+
+def test_layer_argument_errors(L):
+    p = [P(i) for i in range(7)]
+    args = p[:6] + [None, None, p[6], None, None, None, 1, 1, 8, 2, 64, 64, 1, 1, F(64.0),
+                    F(0.125)]
+    need = L.kdn_forward_workspace_bytes(0, 1, 1, 8, 2, 64, 64, 1, 0, 0)
+    ws = [P(40), need, None]
+    opts = kdn.LayerOpts(1, 0.0, 0, None, None)          # gates_preact needs r_min > 0
+    assert L.kdn_forward_layer(0, *args, ctypes.byref(opts), *ws) == kdn.KDN_ERR_INVALID_ARG
+    assert "r_min" in L.kdn_last_error().decode()
+    opts = kdn.LayerOpts(1, 0.01, 1, None, 0x1000000 * 3)  # beta_eff inside v
+    assert L.kdn_forward_layer(0, *args, ctypes.byref(opts), *ws) == kdn.KDN_ERR_INVALID_ARG
+    assert "beta_eff" in L.kdn_last_error().decode()
+    opts = kdn.LayerOpts(0, 0.0, 0, 0x7000000, 0x7000000)  # beta_eff aliases mu_t
+    assert L.kdn_forward_layer(0, *args, ctypes.byref(opts), *ws) == kdn.KDN_ERR_INVALID_ARG
+    assert L.kdn_forward_layer(2, *args, None, *ws) == kdn.KDN_ERR_INVALID_ARG
+    assert L.kdn_forward_layer(0, *args, None, P(40), need - 1, None) == kdn.KDN_ERR_WORKSPACE
+    dec = [0] + [P(i) for i in range(8)] + [None, P(10), 4, 4, 2, 64, 64, 1, 1, F(64.0),
+                                            F(0.125)]
+    opts = kdn.LayerOpts(1, -1.0, 0, None, None)
+    assert L.kdn_decode_step_layer(*dec, ctypes.byref(opts), None) == kdn.KDN_ERR_INVALID_ARG
+    opts = kdn.LayerOpts(0, 0.0, 0, None, 0x1000000 * 11)  # beta_eff inside o
+    assert L.kdn_decode_step_layer(*dec, ctypes.byref(opts), None) == kdn.KDN_ERR_INVALID_ARG
