@@ -2,8 +2,8 @@
 
 Plain float64 implementations of the Diagonal and Isotropic KDN recurrences written from the
 paper (arXiv 2609.07816; Prop. "Diagonal Kalman Delta Network" and Prop. "Isotropic Kalman Delta
-Network"), plus three Moebius-scan forms of the variance chain (App. "Hardware-Efficient
-Chunkwise Algorithm"). Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU
+Network"), their reverse-mode adjoint (``backward``, kdn_oracle_bwd.c), plus three Moebius-scan
+forms of the variance chain (App. "Hardware-Efficient Chunkwise Algorithm"). Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU
 baseline may import this package; the GPU library never does.
 
 The C source ``kdn_oracle.c`` is compiled with gcc (``build()``) into ``liboracle.so`` next to
@@ -21,17 +21,19 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "kdn_oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "kdn_oracle_bwd.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 
 def build(force: bool = True) -> str:
     """Compile liboracle.so with gcc (-O2, OpenMP, IEEE arithmetic: no fast-math, no FMA)."""
-    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= os.path.getmtime(_SRC):
+    if not force and os.path.exists(_LIB) and all(
+            os.path.getmtime(_LIB) >= os.path.getmtime(src) for src in _SRCS):
         return _LIB
     tmp = _LIB + f".tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
-           "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+           "-Wall", "-Wextra", "-o", tmp, *_SRCS, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB)
     return _LIB
@@ -53,8 +55,11 @@ def _load():
     for name in ("oracle_mobius_fold", "oracle_mobius_tree"):
         getattr(lib, name).argtypes = [d, d, d, cd, ctypes.c_int64, ci, d, d]
     lib.oracle_mobius_chunked.argtypes = [d, d, d, cd, ctypes.c_int64, ctypes.c_int64, ci, d, d]
+    lib.oracle_kdn_backward.argtypes = ([ci] + [d] * 8 + [i32p] + [ci] * 7 + [cd, cd] +
+                                        [d] * 13 + [ci])
     for name in ("oracle_kdn_forward_diag", "oracle_kdn_forward_iso", "oracle_kdn_decode_step",
-                 "oracle_mobius_fold", "oracle_mobius_tree", "oracle_mobius_chunked"):
+                 "oracle_mobius_fold", "oracle_mobius_tree", "oracle_mobius_chunked",
+                 "oracle_kdn_backward"):
         getattr(lib, name).restype = ci
     _lib = lib
     return lib
@@ -155,6 +160,37 @@ def decode_step(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None,
     if rc != 0:
         raise ValueError("oracle_kdn_decode_step rejected its arguments")
     return o
+
+
+def backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
+             scale=None, mu_t=None, dO=None, dS_T=None, dP_T=None, nthreads=0):
+    """Reverse-mode adjoint of forward_diag / forward_iso (kdn_oracle_bwd.c): given the adjoints
+    of o, S_T and P_T (None = zero), returns a dict of dq, dk, dv, dalpha, domega, dr, dS0, dP0
+    (and dmu_t when mu_t is given), each shaped like its input."""
+    q, k, v, alpha, omega, r, S0, P0, mu_t, dO, dS_T, dP_T = map(
+        _f64, (q, k, v, alpha, omega, r, S0, P0, mu_t, dO, dS_T, dP_T))
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    vid = {"diag": 0, "iso": 1}[variant]
+    per_channel = int(vid == 0 or alpha.ndim == 4)
+    cu = None if cu_seqlens is None else np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    N = B if cu is None else len(cu) - 1
+    mu = float(dk if mu is None else mu)
+    scale = float(dk ** -0.5 if scale is None else scale)
+    out = dict(dq=np.zeros_like(q), dk=np.zeros_like(k), dv=np.zeros_like(v),
+               dalpha=np.zeros_like(alpha), domega=np.zeros_like(omega), dr=np.zeros_like(r),
+               dS0=np.zeros((N, H, dk, dv)),
+               dP0=np.zeros((N, H, dk) if vid == 0 else (N, H)))
+    if mu_t is not None:
+        out["dmu_t"] = np.zeros_like(mu_t)
+    rc = _load().oracle_kdn_backward(
+        vid, _p(q), _p(k), _p(v), _p(alpha), _p(omega), _p(r), _p(S0), _p(P0), _pi(cu), N, B, T,
+        H, dk, dv, per_channel, mu, scale, _p(mu_t), _p(dO), _p(dS_T), _p(dP_T), _p(out["dq"]),
+        _p(out["dk"]), _p(out["dv"]), _p(out["dalpha"]), _p(out["domega"]), _p(out["dr"]),
+        _p(out["dS0"]), _p(out["dP0"]), _p(out.get("dmu_t")), nthreads)
+    if rc != 0:
+        raise ValueError("oracle_kdn_backward rejected its arguments")
+    return out
 
 
 def _mobius(name, a, w, u, p0, renorm, *extra):
