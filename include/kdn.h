@@ -244,6 +244,47 @@ kdn_status_t kdn_gain_iso(const void* k, const void* alpha, const void* omega, c
 size_t kdn_gain_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
                                 int32_t dk);
 
+/*
+ * Backward of the forward (variant 0: kdn_forward_diag, 1: kdn_forward_iso; chunk 64): the
+ * gradients of a scalar loss with respect to every input, given the loss's gradients with
+ * respect to the forward's outputs. The paper trains through its forward kernels (App.
+ * "Detailed Experimental Setup"); this is the reverse mode of the same recurrences
+ * (Prop. "Diagonal Kalman Delta Network", Prop. "Isotropic Kalman Delta Network"), taken
+ * through the chunked memory scan (App. "Hardware-Efficient Chunkwise Algorithm", Sec.
+ * "Chunkwise Memory Scan") with decay ratios formed from cumulative log-decays, and through the
+ * variance recurrence as a reverse linear recurrence of its adjoint.
+ *   Inputs: those of the forward (same layouts, dtype, packing, S0 / P0 NULL = 0 / 1, mu,
+ *   scale; alpha_per_channel as in kdn_forward_iso, ignored for variant 0), and
+ *   dO [B,T,H,dv] in the input dtype (NULL = 0), dS_T [N,H,dk,dv] and dP_T (shape of P_T)
+ *   float32 (NULL = 0).
+ *   Outputs (float32, caller-owned, each the shape of its input, fully overwritten for the
+ *   tokens of the batch's sequences): dq, dk, dv, dalpha, domega, dr; dS0 [N,H,dk,dv] and dP0
+ *   (shape of P0) or NULL (not written). No gradient may overlap another or any other buffer of
+ *   the call (KDN_ERR_INVALID_ARG). Tokens of a packed batch outside every sequence are not
+ *   written.
+ *   workspace: at least kdn_backward_workspace_bytes(...) bytes (KDN_ERR_WORKSPACE), about
+ *   8 KB per token and head at dk = dv = 128; no initialisation needed.
+ * Seven kernels run on `stream`: the forward's chunk summaries and carry scan, then a per-chunk
+ * replay of the gains and the chunk matrices, a forward walk that checkpoints the state at every
+ * chunk start, a reverse walk that carries the state's adjoint, the per-chunk gradients, the
+ * reverse scan of the variance adjoint and the per-token gradients of the gains. No gate floor
+ * applies (every decay ratio is at most one); the arithmetic is float32 throughout, with the
+ * cumulative log-decays in float64.
+ */
+kdn_status_t kdn_backward(int32_t variant, const void* q, const void* k, const void* v,
+                          const void* alpha, const void* omega, const void* r, const float* S0,
+                          const float* P0, const int32_t* cu_seqlens, int32_t N, int32_t B,
+                          int32_t T, int32_t H, int32_t dk, int32_t dv, kdn_dtype_t dtype,
+                          int32_t alpha_per_channel, float mu, float scale, const void* dO,
+                          const float* dS_T, const float* dP_T, float* dq, float* dk_out,
+                          float* dv_out, float* dalpha, float* domega, float* dr, float* dS0,
+                          float* dP0, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Device scratch (bytes) kdn_backward needs for these sizes (packed != 0 with cu_seqlens);
+ * 0 for arguments it rejects.                                                                 */
+size_t kdn_backward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                    int32_t dk, int32_t dv, int32_t packed);
+
 /* Static text for a status code.                                                             */
 const char* kdn_status_string(kdn_status_t status);
 

@@ -393,6 +393,82 @@ kdn_status_t kdn_decode_step_layer(int32_t variant, const void* q, const void* k
                          dk, dv, dtype, alpha_per_channel, mu, scale, opts, stream);
 }
 
+size_t kdn_backward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
+                                    int32_t dk, int32_t dv, int32_t packed)
+{
+    if (N <= 0 || B <= 0 || T <= 0 || H <= 0 || !head_ok(dk) || !head_ok(dv)) return 0;
+    if (variant != 0 && variant != 1) return 0;
+    return kdn::backward_workspace_bytes(variant, packed != 0, N, B, T, H, dk, dv);
+}
+
+kdn_status_t kdn_backward(int32_t variant, const void* q, const void* k, const void* v,
+                          const void* alpha, const void* omega, const void* r, const float* S0,
+                          const float* P0, const int32_t* cu_seqlens, int32_t N, int32_t B,
+                          int32_t T, int32_t H, int32_t dk, int32_t dv, kdn_dtype_t dtype,
+                          int32_t alpha_per_channel, float mu, float scale, const void* dO,
+                          const float* dS_T, const float* dP_T, float* dq, float* dk_out,
+                          float* dv_out, float* dalpha, float* domega, float* dr, float* dS0,
+                          float* dP0, void* workspace, size_t workspace_bytes, void* stream)
+{
+    if (variant != 0 && variant != 1)
+        return fail(KDN_ERR_INVALID_ARG, "variant must be 0 (diagonal) or 1 (isotropic)");
+    if (!q || !k || !v || !alpha || !omega || !r)
+        return fail(KDN_ERR_INVALID_ARG, "null required input (q, k, v, alpha, omega, r)");
+    if (!dq || !dk_out || !dv_out || !dalpha || !domega || !dr)
+        return fail(KDN_ERR_INVALID_ARG, "null required gradient (dq, dk, dv, dalpha, domega, dr)");
+    if (dtype != KDN_F32 && dtype != KDN_BF16)
+        return fail(KDN_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    kdn_status_t st = check_seq(cu_seqlens, N, B, T, H);
+    if (st != KDN_OK) return st;
+    if (!head_ok(dk) || !head_ok(dv))
+        return fail(KDN_ERR_UNSUPPORTED, "dk=%d dv=%d: head sizes must be 16, 32, 64 or 128", dk,
+                    dv);
+    if (!(mu > 0.f) || !(scale > 0.f))
+        return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
+                    scale);
+    const int apc = (variant == 0 || alpha_per_channel) ? 1 : 0;
+    const size_t rows = (size_t)B * T * H, es = esize(dtype);
+    const size_t pc = variant == 0 ? (size_t)dk : 1;
+    // every buffer the call reads or writes, with its extent; the gradients may overlap none
+    const void* bufs[14] = {q, k, v, alpha, omega, r, dO, S0, P0, dS_T, dP_T, cu_seqlens,
+                            workspace, nullptr};
+    const size_t bsz[14] = {rows * dk * es, rows * dk * es, rows * dv * es,
+                            rows * (apc ? dk : 1) * es, rows * pc * es, rows * es, rows * dv * es,
+                            (size_t)N * H * dk * dv * 4, (size_t)N * H * pc * 4,
+                            (size_t)N * H * dk * dv * 4, (size_t)N * H * pc * 4,
+                            cu_seqlens ? (size_t)(N + 1) * 4 : 0, workspace_bytes, 0};
+    float* outs[8] = {dq, dk_out, dv_out, dalpha, domega, dr, dS0, dP0};
+    const size_t osz[8] = {rows * dk * 4, rows * dk * 4, rows * dv * 4, rows * (apc ? dk : 1) * 4,
+                           rows * pc * 4, rows * 4, (size_t)N * H * dk * dv * 4,
+                           (size_t)N * H * pc * 4};
+    for (int o = 0; o < 8; ++o) {
+        for (int i = 0; i < 13; ++i)
+            if (overlaps(outs[o], osz[o], bufs[i], bsz[i]))
+                return fail(KDN_ERR_INVALID_ARG, "gradient %d overlaps argument buffer %d", o, i);
+        for (int o2 = 0; o2 < o; ++o2)
+            if (overlaps(outs[o], osz[o], outs[o2], osz[o2]))
+                return fail(KDN_ERR_INVALID_ARG, "gradients %d and %d overlap", o2, o);
+    }
+    const size_t nk = rows * dk * es, nv = rows * dv * es;
+    if (nk >= ((size_t)1 << 31) || nv >= ((size_t)1 << 31))
+        return fail(KDN_ERR_UNSUPPORTED, "each input tensor must be smaller than 2 GiB");
+    const size_t need = kdn::backward_workspace_bytes(variant, cu_seqlens != nullptr, N, B, T, H,
+                                                      dk, dv);
+    if (!workspace || workspace_bytes < need)
+        return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                    workspace ? workspace_bytes : (size_t)0);
+    kdn::BwdCall bc;
+    bc.variant = variant; bc.apc = apc;
+    bc.q = q; bc.k = k; bc.v = v; bc.alpha = alpha; bc.omega = omega; bc.r = r; bc.dO = dO;
+    bc.S0 = S0; bc.P0 = P0; bc.dS_T = dS_T; bc.dP_T = dP_T;
+    bc.gq = dq; bc.gk = dk_out; bc.gv = dv_out; bc.galpha = dalpha; bc.gomega = domega;
+    bc.gr = dr; bc.gS0 = dS0; bc.gP0 = dP0;
+    bc.sa = {cu_seqlens, N, B, T, H};
+    bc.dk = dk; bc.dv = dv; bc.dtype = dtype; bc.mu = mu; bc.scale = scale;
+    bc.workspace = workspace;
+    return hip_status(kdn::launch_backward(bc, (hipStream_t)stream), "kdn_backward launch");
+}
+
 static kdn_status_t gain_common(int variant, const void* k, const void* alpha, const void* omega,
                                 const void* r, const float* P0, float* gain_out, float* phat_out,
                                 float* P_T, const int32_t* cu, int32_t N, int32_t B, int32_t T,

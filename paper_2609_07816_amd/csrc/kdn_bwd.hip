@@ -1,0 +1,1062 @@
+// Backward pass of the chunked KDN forward (both variants) on gfx950.
+//
+// The forward's loss gradient is taken through its two stages (App. "Hardware-Efficient
+// Chunkwise Algorithm": the gain scan, then the memory scan):
+//
+//  memory scan, given the gains kappa_t. Within a chunk of C tokens with start state S_in,
+//  decays gamma_t = prod_{s <= t} alpha_s = exp(lambda_t) (lambda: cumulative log-decay, float64)
+//  and the ratios R_ts = gamma_t / gamma_s = exp(lambda_t - lambda_s) <= 1 (s <= t):
+//      (I + T) Delta = V - Kbar S_in,      T_ts = sum_i k_ti kappa_si R_ts,i   (s < t)
+//      O = scale (Qbar S_in + B Delta),    B_ts = sum_i q_ti kappa_si R_ts,i   (s <= t)
+//      S_out = diag(gamma_C) S_in + Ktail^T Delta,  Ktail_s = (gamma_C / gamma_s) kappa_s
+//  with Kbar = gamma k, Qbar = gamma q (eqs. chunk-memory-normalization to
+//  chunk-memory-output-state, written with kappa itself). Its adjoint runs a reverse walk over
+//  the chunks carrying dS (dS_in = scale Qbar^T dO + diag(gamma_C) dS_out - Kbar^T Psi with
+//  Psi = A^T (scale B^T dO + Ktail dS_out), A = (I + T)^-1; dV = Psi), then forms every
+//  chunk's gradients on q, k, kappa and the log-decays chunk-parallel from S_in (checkpointed
+//  by a forward walk), dS_out, Delta and Psi.
+//
+//  gain scan. kappa_t = p_hat_t k_t / (r_t + sum_i p_hat_ti k_ti^2) (diagonal) or beta_t k_t
+//  (isotropic), p_hat_t = alpha_t^2 p_{t-1} + omega_t (or a_t b_{t-1} + omega_t) and
+//  p_t = p_hat_t / (1 + u_t p_hat_t) (eqs. kla-box-gain, diag-cov-update; iso-kla-box-gain,
+//  iso-kla-box-cov-update). The adjoint of p_t obeys a linear recurrence backwards in time,
+//  lambda_p,{t-1} = A_t lambda_p,t + B_t, whose coefficients are token-local; it is run per
+//  channel in reverse, and every other gradient of the gain stage is token-local given it.
+//
+// Kernels, in launch order (summary and carry scan are the forward's):
+//   bw_prep   per (chunk, head): variance replay from the carry, kappa, lambda, T, B, A
+//   bw_fwalk  per (sequence, head, value tile): S_in of every chunk, Delta
+//   bw_rwalk  per (sequence, head, value tile), chunks in reverse: dS_out, dV, dS0
+//   bw_grad   per (chunk, head): dq, dk (memory part), dkappa, d(log-decay) -> dalpha part,
+//             the coefficients of the variance adjoint
+//   bw_scan   per (sequence, head, variance channel): the variance adjoint, dP0
+//   bw_final  per (chunk, head): dk, dalpha, domega, dr of the gain stage
+// Everything is float32 arithmetic (the log-decays float64); gradients are float32.
+#include "kdn_fwd.h"
+
+namespace kdn {
+namespace bwd {
+
+using fwd::C;
+constexpr int NTH = 256;
+
+// Per (chunk, head) record written by bw_prep.
+template <int DK>
+struct BwRec {
+    static constexpr size_t F = (size_t)C * DK * 4;
+    static constexpr size_t OFF_KAP = 0;        // kappa [C][DK]
+    static constexpr size_t OFF_PHAT = F;       // p_hat [C][DK] (isotropic: b_hat in [t][0])
+    static constexpr size_t OFF_PPRV = 2 * F;   // p_{t-1} [C][DK] (isotropic: [t][0])
+    static constexpr size_t OFF_KBAR = 3 * F;   // gamma k
+    static constexpr size_t OFF_QBAR = 4 * F;   // gamma q
+    static constexpr size_t OFF_KTL = 5 * F;    // (gamma_C / gamma) kappa
+    static constexpr size_t OFF_LAM = 6 * F;    // lambda [C][DK] float64
+    static constexpr size_t OFF_A = 8 * F;      // (I + T)^-1 [C][C]
+    static constexpr size_t OFF_B = OFF_A + (size_t)C * C * 4;  // B [C][C]
+    static constexpr size_t OFF_GC = OFF_B + (size_t)C * C * 4; // gamma_C [DK]
+    static constexpr size_t OFF_DEN = OFF_GC + (size_t)DK * 4;  // gain denominator [C]
+    static constexpr size_t BYTES = al256(OFF_DEN + (size_t)C * 4);
+};
+
+// Workspace of one backward call.
+struct BwMap {
+    size_t choff, summ, carry, rec, ckpt, dlt, dso, dkap, dlam, dal, acf, bcf, aux, lamp, total;
+    int maxch;
+};
+
+inline BwMap bw_map(int variant, bool packed, int N, int B, int T, int H, int dk, int dv,
+                    size_t rec_bytes)
+{
+    BwMap m;
+    m.maxch = packed ? (int)((size_t)B * T / C + (size_t)N) : N * ((T + C - 1) / C);
+    const size_t ch = (size_t)m.maxch * H;
+    const size_t nchan = variant == 0 ? (size_t)dk : 1;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off += al256(bytes);
+        return o;
+    };
+    m.choff = take(packed ? (size_t)(N + 1) * 4 : 0);
+    m.summ = take(ch * nchan * 16);
+    m.carry = take(ch * nchan * 8);
+    m.rec = take(ch * rec_bytes);
+    m.ckpt = take(ch * dk * dv * 4);
+    m.dlt = take(ch * C * dv * 4);
+    m.dso = take(ch * dk * dv * 4);
+    m.dkap = take(ch * C * dk * 4);
+    m.dlam = take(ch * C * dk * 4);
+    m.dal = take(ch * C * dk * 4);
+    m.acf = take(ch * C * nchan * 4);
+    m.bcf = take(ch * C * nchan * 4);
+    m.aux = take(ch * C * 4);
+    m.lamp = take(ch * C * nchan * 4);
+    m.total = off;
+    return m;
+}
+
+struct Args {
+    const void *q, *k, *v, *alpha, *omega, *r, *dO;
+    const float *S0, *dS_T, *dP_T;
+    float *dq, *dk, *dv, *dalpha, *domega, *dr, *dS0, *dP0;
+    ChunkMap cm;
+    int H, DV, BV;
+    float mu, scale;
+    const float2* carry;
+    char* rec;
+    float *ckpt, *dlt, *dso, *dkap, *dlam, *dal, *acf, *bcf, *aux, *lamp;
+};
+
+template <class TI>
+__device__ __forceinline__ float ld(const void* p, size_t i)
+{
+    return to_f32(((const TI*)p)[i]);
+}
+
+// ------------------------------------------------------------------------------------------
+// bw_prep
+// ------------------------------------------------------------------------------------------
+template <int DK>
+struct PrepLds {
+    static constexpr int SLB = DK < 32 ? DK : 32;     // channel slab of the T / B products
+    static constexpr size_t OFF_Z = 0;                                       // [C][DK+1]
+    static constexpr size_t OFF_DEN = OFF_Z + (size_t)C * (DK + 1) * 4;      // [C]
+    static constexpr size_t OFF_BETA = OFF_DEN + C * 4;
+    static constexpr size_t OFF_AA = OFF_BETA + C * 4;
+    static constexpr size_t OFF_NK = OFF_AA + C * 4;
+    static constexpr size_t OFF_SK = OFF_NK + C * 4;                         // [C][SLB+1]
+    static constexpr size_t OFF_SQ = OFF_SK + (size_t)C * (SLB + 1) * 4;
+    static constexpr size_t OFF_SP = OFF_SQ + (size_t)C * (SLB + 1) * 4;
+    static constexpr size_t OFF_SL = al16(OFF_SP + (size_t)C * (SLB + 1) * 4);  // double
+    static constexpr size_t OFF_T = OFF_SL + (size_t)C * (SLB + 1) * 8;      // [C][C+1]
+    static constexpr size_t OFF_A = OFF_T + (size_t)C * (C + 1) * 4;
+    static constexpr size_t TOTAL = al16(OFF_A + (size_t)C * (C + 1) * 4);
+};
+
+template <class TI, int DK, int VARIANT, bool APC>
+__global__ __launch_bounds__(NTH) void bw_prep(Args a)
+{
+    using R = BwRec<DK>;
+    using LY = PrepLds<DK>;
+    constexpr bool DIAG = VARIANT == 0;
+    constexpr int SLB = LY::SLB, LDZ = DK + 1, LDS_ = SLB + 1, LDC = C + 1;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* s_z = (float*)(smem + LY::OFF_Z);
+    float* s_den = (float*)(smem + LY::OFF_DEN);
+    float* s_beta = (float*)(smem + LY::OFF_BETA);
+    float* s_aa = (float*)(smem + LY::OFF_AA);
+    float* s_nk = (float*)(smem + LY::OFF_NK);
+    float* s_k = (float*)(smem + LY::OFF_SK);
+    float* s_q = (float*)(smem + LY::OFF_SQ);
+    float* s_p = (float*)(smem + LY::OFF_SP);
+    double* s_l = (double*)(smem + LY::OFF_SL);
+    float* s_T = (float*)(smem + LY::OFF_T);
+    float* s_A = (float*)(smem + LY::OFF_A);
+
+    const int H = a.H;
+    const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
+    int n, c0, c1;
+    bool last;
+    if (!locate_chunk<C>(a.cm, g, n, c0, c1, last)) return;
+    const int L = c1 - c0;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
+    float* kap = (float*)(rec + R::OFF_KAP);
+    float* phat = (float*)(rec + R::OFF_PHAT);
+    float* pprv = (float*)(rec + R::OFF_PPRV);
+    float* kbar = (float*)(rec + R::OFF_KBAR);
+    float* qbar = (float*)(rec + R::OFF_QBAR);
+    float* ktl = (float*)(rec + R::OFF_KTL);
+    double* lam = (double*)(rec + R::OFF_LAM);
+    float* Am = (float*)(rec + R::OFF_A);
+    float* Bm = (float*)(rec + R::OFF_B);
+    float* gC = (float*)(rec + R::OFF_GC);
+    float* den = (float*)(rec + R::OFF_DEN);
+    auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
+    auto alpha_at = [&](int t, int i) {
+        if (t >= L) return 1.f;
+        return APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
+    };
+
+    // ---- the variance chain through the chunk (eqs. kla-box-mobius / iso-kla-box-cov-update)
+    // from the carry, and the cumulative log-decay ----------------------------------------------
+    if constexpr (DIAG) {
+        if (tid < DK) {
+            const float2 cz = a.carry[((size_t)g * H + h) * DK + tid];
+            float p = cz.x / cz.y;
+            for (int t = 0; t < C; ++t) {
+                const bool ok = t < L;
+                const float al = alpha_at(t, tid);
+                const float om = ok ? ld<TI>(a.omega, row(t) * DK + tid) : 0.f;
+                const float kk = ok ? ld<TI>(a.k, row(t) * DK + tid) : 0.f;
+                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                pprv[t * DK + tid] = p;
+                const float ph = al * al * p + om;
+                phat[t * DK + tid] = ph;
+                s_z[t * LDZ + tid] = ph * kk * kk;
+                const float u = a.mu * kk * kk / rr;
+                p = ph / (1.f + u * ph);
+            }
+        }
+    } else {
+        // per-token mean alpha^2 and ||k||^2 (wave w: tokens 16 w .. 16 w + 15)
+        for (int j = 0; j < C / 4; ++j) {
+            const int t = (C / 4) * w + j;
+            float sa = 0.f, sk = 0.f;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = t < L ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+                sk += kk * kk;
+                if (APC) {
+                    const float al = alpha_at(t, i);
+                    sa += al * al;
+                }
+            }
+            sa = wave_sum(sa);
+            sk = wave_sum(sk);
+            if (lane == 0) {
+                float aa;
+                if (APC) aa = sa / (float)DK;
+                else {
+                    const float al = alpha_at(t, 0);
+                    aa = al * al;
+                }
+                s_aa[t] = t < L ? aa : 1.f;
+                s_nk[t] = sk;
+            }
+        }
+        __syncthreads();
+        if (tid == 0) {
+            const float2 cz = a.carry[(size_t)g * H + h];
+            float b = cz.x / cz.y;
+            for (int t = 0; t < C; ++t) {
+                const bool ok = t < L;
+                const float om = ok ? ld<TI>(a.omega, row(t)) : 0.f;
+                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                pprv[t * DK] = b;
+                const float bh = s_aa[t] * b + om;
+                phat[t * DK] = bh;
+                const float dn = rr + bh * s_nk[t];
+                s_den[t] = dn;
+                den[t] = dn;
+                s_beta[t] = bh / dn;
+                const float u = a.mu * s_nk[t] / ((float)DK * rr);
+                b = bh / (1.f + u * bh);
+            }
+        }
+    }
+    if (tid < DK) {
+        double lm = 0.0;
+        for (int t = 0; t < C; ++t) {
+            lm += (double)logf(alpha_at(t, tid));
+            lam[t * DK + tid] = lm;
+        }
+    }
+    __syncthreads();
+    if constexpr (DIAG) {  // gain denominators r + sum_i p_hat_i k_i^2
+        for (int j = 0; j < C / 4; ++j) {
+            const int t = (C / 4) * w + j;
+            float z = 0.f;
+            for (int i = lane; i < DK; i += 64) z += s_z[t * LDZ + i];
+            z = wave_sum(z);
+            if (lane == 0) {
+                const float dn = t < L ? ld<TI>(a.r, row(t)) + z : 1.f;
+                s_den[t] = dn;
+                den[t] = dn;
+            }
+        }
+        __syncthreads();
+    }
+
+    // ---- kappa, gamma-scaled operands, the tail operand and gamma_C -------------------------
+    if (tid < DK) {
+        const double lmC = lam[(C - 1) * DK + tid];
+        for (int t = 0; t < C; ++t) {
+            const bool ok = t < L;
+            const float kk = ok ? ld<TI>(a.k, row(t) * DK + tid) : 0.f;
+            const float qq = ok ? ld<TI>(a.q, row(t) * DK + tid) : 0.f;
+            const float kp = DIAG ? phat[t * DK + tid] * kk / s_den[t] : s_beta[t] * kk;
+            kap[t * DK + tid] = kp;
+            const double lm = lam[t * DK + tid];
+            const float gm = expf((float)lm);
+            kbar[t * DK + tid] = gm * kk;
+            qbar[t * DK + tid] = gm * qq;
+            ktl[t * DK + tid] = expf((float)(lmC - lm)) * kp;
+        }
+        gC[tid] = expf((float)lmC);
+    }
+    __syncthreads();
+
+    // ---- T (s < t) and B (s <= t) by channel slabs; thread (t, 16 consecutive s) ------------
+    float accT[16], accB[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) accT[e] = accB[e] = 0.f;
+    const int tr = tid >> 2, sg = (tid & 3) * 16;
+    for (int s0 = 0; s0 < DK; s0 += SLB) {
+        for (int e = tid; e < C * SLB; e += NTH) {
+            const int t = e / SLB, ii = e % SLB, i = s0 + ii;
+            const bool ok = t < L;
+            s_k[t * LDS_ + ii] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+            s_q[t * LDS_ + ii] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+            s_p[t * LDS_ + ii] = kap[t * DK + i];
+            s_l[t * LDS_ + ii] = lam[t * DK + i];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int s = sg + e;
+            if (s <= tr) {
+                float bt = 0.f, tt = 0.f;
+                for (int ii = 0; ii < SLB; ++ii) {
+                    const float rt = __expf((float)(s_l[tr * LDS_ + ii] - s_l[s * LDS_ + ii]));
+                    const float x = s_p[s * LDS_ + ii] * rt;
+                    bt = fmaf(s_q[tr * LDS_ + ii], x, bt);
+                    tt = fmaf(s_k[tr * LDS_ + ii], x, tt);
+                }
+                accB[e] += bt;
+                accT[e] += s < tr ? tt : 0.f;
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int s = sg + e;
+        Bm[tr * C + s] = s <= tr ? accB[e] : 0.f;
+        s_T[tr * LDC + s] = s < tr ? accT[e] : 0.f;
+    }
+    for (int e = tid; e < C * C; e += NTH) {
+        const int t = e / C, j = e % C;
+        s_A[t * LDC + j] = t == j ? 1.f : 0.f;
+    }
+    __syncthreads();
+    // ---- A = (I + T)^-1 by columns (forward substitution; thread j of wave 0: column j) -------
+    if (tid < C) {
+        const int j = tid;
+        for (int t = 1; t < C; ++t) {
+            float acc = 0.f;
+            for (int s = 0; s < t; ++s) acc = fmaf(s_T[t * LDC + s], s_A[s * LDC + j], acc);
+            if (t > j) s_A[t * LDC + j] = -acc;
+        }
+    }
+    __syncthreads();
+    for (int e = tid; e < C * C; e += NTH) Am[e] = s_A[(e / C) * LDC + (e % C)];
+}
+
+// ------------------------------------------------------------------------------------------
+// walks over the chunks of one (sequence, head, value tile)
+// ------------------------------------------------------------------------------------------
+template <int DK>
+struct WalkLds {
+    static constexpr int LDV = 33, LDK = DK + 1, LDC = C + 1;
+    static constexpr size_t OFF_S = 0;                                      // [DK][LDV]
+    static constexpr size_t OFF_R1 = OFF_S + (size_t)DK * LDV * 4;          // [C][LDK]
+    static constexpr size_t OFF_R2 = OFF_R1 + (size_t)C * LDK * 4;          // [C][LDK]
+    static constexpr size_t OFF_A = OFF_R2 + (size_t)C * LDK * 4;           // [C][LDC]
+    static constexpr size_t OFF_B = OFF_A + (size_t)C * LDC * 4;            // [C][LDC]
+    static constexpr size_t OFF_X = OFF_B + (size_t)C * LDC * 4;            // [C][LDV]
+    static constexpr size_t OFF_D = OFF_X + (size_t)C * LDV * 4;
+    static constexpr size_t OFF_P = OFF_D + (size_t)C * LDV * 4;
+    static constexpr size_t OFF_GC = OFF_P + (size_t)C * LDV * 4;           // [DK]
+    static constexpr size_t TOTAL = al16(OFF_GC + (size_t)DK * 4);
+};
+
+template <class TI, int DK>
+__global__ __launch_bounds__(NTH) void bw_fwalk(Args a)
+{
+    using R = BwRec<DK>;
+    using LY = WalkLds<DK>;
+    constexpr int LDV = LY::LDV, LDK = LY::LDK, LDC = LY::LDC;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* s_S = (float*)(smem + LY::OFF_S);
+    float* s_kb = (float*)(smem + LY::OFF_R1);
+    float* s_kt = (float*)(smem + LY::OFF_R2);
+    float* s_A = (float*)(smem + LY::OFF_A);
+    float* s_X = (float*)(smem + LY::OFF_X);
+    float* s_D = (float*)(smem + LY::OFF_D);
+    float* s_gc = (float*)(smem + LY::OFF_GC);
+
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV;
+    const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
+    if (slot >= a.cm.N * H) return;
+    const int n = slot / H, h = slot % H, j0 = vt * BV;
+    const int tid = threadIdx.x;
+    int t0, t1, g0, nch;
+    seq_span(a.cm, n, t0, t1);
+    seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
+    for (int e = tid; e < DK * BV; e += NTH) {
+        const int i = e / BV, j = e % BV;
+        s_S[i * LDV + j] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
+    }
+    for (int ci = 0; ci < nch; ++ci) {
+        const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
+        const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
+        const size_t gh = (size_t)g * H + h;
+        __syncthreads();
+        for (int e = tid; e < DK * BV; e += NTH) {
+            const int i = e / BV, j = e % BV;
+            a.ckpt[(gh * DK + i) * DV + j0 + j] = s_S[i * LDV + j];
+        }
+        const float* kbar = (const float*)(rec + R::OFF_KBAR);
+        const float* ktl = (const float*)(rec + R::OFF_KTL);
+        const float* Am = (const float*)(rec + R::OFF_A);
+        const float* gC = (const float*)(rec + R::OFF_GC);
+        for (int e = tid; e < C * DK; e += NTH) {
+            const int t = e / DK, i = e % DK;
+            s_kb[t * LDK + i] = kbar[e];
+            s_kt[t * LDK + i] = ktl[e];
+        }
+        for (int e = tid; e < C * C; e += NTH) s_A[(e / C) * LDC + e % C] = Am[e];
+        for (int e = tid; e < DK; e += NTH) s_gc[e] = gC[e];
+        for (int e = tid; e < C * BV; e += NTH) {
+            const int t = e / BV, j = e % BV;
+            s_X[t * LDV + j] =
+                t < L ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + j) : 0.f;
+        }
+        __syncthreads();
+        for (int e = tid; e < C * BV; e += NTH) {  // X = V - Kbar S_in
+            const int t = e / BV, j = e % BV;
+            float acc = s_X[t * LDV + j];
+            for (int i = 0; i < DK; ++i) acc = fmaf(-s_kb[t * LDK + i], s_S[i * LDV + j], acc);
+            s_X[t * LDV + j] = acc;
+        }
+        __syncthreads();
+        for (int e = tid; e < C * BV; e += NTH) {  // Delta = A X
+            const int t = e / BV, j = e % BV;
+            float acc = 0.f;
+            for (int s = 0; s <= t; ++s) acc = fmaf(s_A[t * LDC + s], s_X[s * LDV + j], acc);
+            s_D[t * LDV + j] = acc;
+            a.dlt[(gh * C + t) * DV + j0 + j] = acc;
+        }
+        __syncthreads();
+        for (int e = tid; e < DK * BV; e += NTH) {  // S_out = gamma_C S_in + Ktail^T Delta
+            const int i = e / BV, j = e % BV;
+            float acc = s_gc[i] * s_S[i * LDV + j];
+            for (int t = 0; t < C; ++t) acc = fmaf(s_kt[t * LDK + i], s_D[t * LDV + j], acc);
+            s_S[i * LDV + j] = acc;
+        }
+    }
+}
+
+template <class TI, int DK>
+__global__ __launch_bounds__(NTH) void bw_rwalk(Args a)
+{
+    using R = BwRec<DK>;
+    using LY = WalkLds<DK>;
+    constexpr int LDV = LY::LDV, LDK = LY::LDK, LDC = LY::LDC;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* s_dS = (float*)(smem + LY::OFF_S);
+    float* s_r1 = (float*)(smem + LY::OFF_R1);
+    float* s_r2 = (float*)(smem + LY::OFF_R2);
+    float* s_A = (float*)(smem + LY::OFF_A);
+    float* s_B = (float*)(smem + LY::OFF_B);
+    float* s_O = (float*)(smem + LY::OFF_X);   // scale dO
+    float* s_dD = (float*)(smem + LY::OFF_D);
+    float* s_P = (float*)(smem + LY::OFF_P);
+    float* s_gc = (float*)(smem + LY::OFF_GC);
+
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV;
+    const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
+    if (slot >= a.cm.N * H) return;
+    const int n = slot / H, h = slot % H, j0 = vt * BV;
+    const int tid = threadIdx.x;
+    int t0, t1, g0, nch;
+    seq_span(a.cm, n, t0, t1);
+    seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
+    for (int e = tid; e < DK * BV; e += NTH) {
+        const int i = e / BV, j = e % BV;
+        s_dS[i * LDV + j] = a.dS_T ? a.dS_T[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
+    }
+    for (int ci = nch - 1; ci >= 0; --ci) {
+        const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
+        const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
+        const size_t gh = (size_t)g * H + h;
+        __syncthreads();
+        for (int e = tid; e < DK * BV; e += NTH) {
+            const int i = e / BV, j = e % BV;
+            a.dso[(gh * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
+        }
+        const float* ktl = (const float*)(rec + R::OFF_KTL);
+        const float* Am = (const float*)(rec + R::OFF_A);
+        const float* Bm = (const float*)(rec + R::OFF_B);
+        const float* gC = (const float*)(rec + R::OFF_GC);
+        for (int e = tid; e < C * DK; e += NTH) s_r1[(e / DK) * LDK + e % DK] = ktl[e];
+        for (int e = tid; e < C * C; e += NTH) {
+            s_A[(e / C) * LDC + e % C] = Am[e];
+            s_B[(e / C) * LDC + e % C] = Bm[e];
+        }
+        for (int e = tid; e < DK; e += NTH) s_gc[e] = gC[e];
+        for (int e = tid; e < C * BV; e += NTH) {
+            const int t = e / BV, j = e % BV;
+            s_O[t * LDV + j] = (t < L && a.dO)
+                                   ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
+                                   : 0.f;
+        }
+        __syncthreads();
+        for (int e = tid; e < C * BV; e += NTH) {  // dDelta = B^T (scale dO) + Ktail dS_out
+            const int s = e / BV, j = e % BV;
+            float acc = 0.f;
+            for (int t = s; t < C; ++t) acc = fmaf(s_B[t * LDC + s], s_O[t * LDV + j], acc);
+            for (int i = 0; i < DK; ++i) acc = fmaf(s_r1[s * LDK + i], s_dS[i * LDV + j], acc);
+            s_dD[s * LDV + j] = acc;
+        }
+        __syncthreads();
+        for (int e = tid; e < C * BV; e += NTH) {  // Psi = A^T dDelta = dV
+            const int s = e / BV, j = e % BV;
+            float acc = 0.f;
+            for (int t = s; t < C; ++t) acc = fmaf(s_A[t * LDC + s], s_dD[t * LDV + j], acc);
+            s_P[s * LDV + j] = acc;
+            if (s < L) a.dv[((size_t)(c0 + s) * H + h) * DV + j0 + j] = acc;
+        }
+        __syncthreads();
+        const float* qbar = (const float*)(rec + R::OFF_QBAR);
+        const float* kbar = (const float*)(rec + R::OFF_KBAR);
+        for (int e = tid; e < C * DK; e += NTH) {
+            s_r1[(e / DK) * LDK + e % DK] = qbar[e];
+            s_r2[(e / DK) * LDK + e % DK] = kbar[e];
+        }
+        __syncthreads();
+        for (int e = tid; e < DK * BV; e += NTH) {  // dS_in
+            const int i = e / BV, j = e % BV;
+            float acc = s_gc[i] * s_dS[i * LDV + j];
+            for (int t = 0; t < C; ++t) {
+                acc = fmaf(s_r1[t * LDK + i], s_O[t * LDV + j], acc);
+                acc = fmaf(-s_r2[t * LDK + i], s_P[t * LDV + j], acc);
+            }
+            s_dS[i * LDV + j] = acc;
+        }
+    }
+    __syncthreads();
+    if (a.dS0)
+        for (int e = tid; e < DK * BV; e += NTH) {
+            const int i = e / BV, j = e % BV;
+            a.dS0[((size_t)slot * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
+        }
+}
+
+// ------------------------------------------------------------------------------------------
+// bw_grad: chunk-parallel gradients of the memory scan and the variance-adjoint coefficients
+// ------------------------------------------------------------------------------------------
+template <int DK>
+struct GradLds {
+    static constexpr int SLB = DK < 32 ? DK : 32, LDV = 33, LDC = C + 1, LDZ = DK + 1;
+    static constexpr int LDS_ = SLB + 1;
+    static constexpr size_t OFF_DB = 0;                                      // [C][LDC]
+    static constexpr size_t OFF_DT = OFF_DB + (size_t)C * LDC * 4;
+    static constexpr size_t OFF_W = OFF_DT + (size_t)C * LDC * 4;
+    // value slabs: Delta, Psi, dO [C][LDV]; S_in, dS_out [DK][LDV]
+    static constexpr size_t W_D = 0, W_P = W_D + (size_t)C * LDV * 4, W_O = W_P + (size_t)C * LDV * 4;
+    static constexpr size_t W_S = W_O + (size_t)C * LDV * 4, W_G = W_S + (size_t)DK * LDV * 4;
+    static constexpr size_t W1 = W_G + (size_t)DK * LDV * 4;
+    // channel slabs: q, k, kappa [C][LDS_], lambda [C][LDS_] double
+    static constexpr size_t W_Q = 0, W_K = W_Q + (size_t)C * LDS_ * 4, W_KP = W_K + (size_t)C * LDS_ * 4;
+    static constexpr size_t W_L = al16(W_KP + (size_t)C * LDS_ * 4);
+    static constexpr size_t W2 = W_L + (size_t)C * LDS_ * 8;
+    static constexpr size_t OFF_C = OFF_W + al16(cmax(W1, W2));              // [C][LDZ]
+    static constexpr size_t OFF_P6 = OFF_C + (size_t)C * LDZ * 4;            // [DK]
+    static constexpr size_t TOTAL = al16(OFF_P6 + (size_t)DK * 4);
+};
+
+template <class TI, int DK, int VARIANT, bool APC>
+__global__ __launch_bounds__(NTH) void bw_grad(Args a)
+{
+    using R = BwRec<DK>;
+    using LY = GradLds<DK>;
+    constexpr bool DIAG = VARIANT == 0;
+    constexpr int SLB = LY::SLB, LDV = LY::LDV, LDC = LY::LDC, LDZ = LY::LDZ, LDS_ = LY::LDS_;
+    constexpr int Q = DK / 4;  // channels per thread in the dk-wide products
+    constexpr int NCHAN = DIAG ? DK : 1;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* s_dB = (float*)(smem + LY::OFF_DB);
+    float* s_dT = (float*)(smem + LY::OFF_DT);
+    char* wr = smem + LY::OFF_W;
+    float* s_D = (float*)(wr + LY::W_D);
+    float* s_P = (float*)(wr + LY::W_P);
+    float* s_O = (float*)(wr + LY::W_O);
+    float* s_S = (float*)(wr + LY::W_S);
+    float* s_G = (float*)(wr + LY::W_G);
+    float* s_q = (float*)(wr + LY::W_Q);
+    float* s_k = (float*)(wr + LY::W_K);
+    float* s_kp = (float*)(wr + LY::W_KP);
+    double* s_l = (double*)(wr + LY::W_L);
+    float* s_c = (float*)(smem + LY::OFF_C);
+    float* s_p6 = (float*)(smem + LY::OFF_P6);
+
+    const int H = a.H, DV = a.DV;
+    const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
+    int n, c0, c1;
+    bool last;
+    if (!locate_chunk<C>(a.cm, g, n, c0, c1, last)) return;
+    const int L = c1 - c0;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const size_t gh = (size_t)g * H + h;
+    const char* rec = a.rec + gh * R::BYTES;
+    const float* kap = (const float*)(rec + R::OFF_KAP);
+    const float* phat = (const float*)(rec + R::OFF_PHAT);
+    const double* lam = (const double*)(rec + R::OFF_LAM);
+    const float* gC = (const float*)(rec + R::OFF_GC);
+    const float* den = (const float*)(rec + R::OFF_DEN);
+    float* dkap = a.dkap + gh * C * DK;
+    float* dlam = a.dlam + gh * C * DK;
+    float* dal = a.dal + gh * C * DK;
+    auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
+
+    // ---- products over the value columns, by slabs of 32 columns ---------------------------
+    //   P1 = dO Delta^T, P2 = Psi Delta^T (thread: row t, 16 columns s)
+    //   P3 = Psi S_in^T, P4 = dO S_in^T, P5 = Delta dS_out^T (thread: row t, Q channels)
+    //   P6_i = sum_j S_in,ij dS_out,ij
+    const int tr = tid >> 2, sg = (tid & 3) * 16, qd = (tid & 3) * Q;
+    float p1[16], p2[16], p3[Q], p4[Q], p5[Q], p6 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) p1[e] = p2[e] = 0.f;
+#pragma unroll
+    for (int e = 0; e < Q; ++e) p3[e] = p4[e] = p5[e] = 0.f;
+    for (int j0 = 0; j0 < DV; j0 += 32) {
+        const int SW = min(32, DV - j0);
+        __syncthreads();
+        for (int e = tid; e < C * SW; e += NTH) {
+            const int t = e / SW, j = e % SW;
+            const bool ok = t < L;
+            s_D[t * LDV + j] = a.dlt[(gh * C + t) * DV + j0 + j];
+            s_P[t * LDV + j] = ok ? a.dv[row(t) * DV + j0 + j] : 0.f;
+            s_O[t * LDV + j] = (ok && a.dO) ? ld<TI>(a.dO, row(t) * DV + j0 + j) : 0.f;
+        }
+        for (int e = tid; e < DK * SW; e += NTH) {
+            const int i = e / SW, j = e % SW;
+            s_S[i * LDV + j] = a.ckpt[(gh * DK + i) * DV + j0 + j];
+            s_G[i * LDV + j] = a.dso[(gh * DK + i) * DV + j0 + j];
+        }
+        __syncthreads();
+        for (int j = 0; j < SW; ++j) {
+            const float ot = s_O[tr * LDV + j], pt = s_P[tr * LDV + j], dt = s_D[tr * LDV + j];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const float ds = s_D[(sg + e) * LDV + j];
+                p1[e] = fmaf(ot, ds, p1[e]);
+                p2[e] = fmaf(pt, ds, p2[e]);
+            }
+#pragma unroll
+            for (int e = 0; e < Q; ++e) {
+                const float si = s_S[(qd + e) * LDV + j];
+                p3[e] = fmaf(pt, si, p3[e]);
+                p4[e] = fmaf(ot, si, p4[e]);
+                p5[e] = fmaf(dt, s_G[(qd + e) * LDV + j], p5[e]);
+            }
+        }
+        if (tid < DK)
+            for (int j = 0; j < SW; ++j) p6 = fmaf(s_S[tid * LDV + j], s_G[tid * LDV + j], p6);
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const int s = sg + e;
+        s_dB[tr * LDC + s] = s <= tr ? a.scale * p1[e] : 0.f;  // dB = scale dO Delta^T
+        s_dT[tr * LDC + s] = s < tr ? -p2[e] : 0.f;             // dT = -Psi Delta^T
+    }
+    if (tid < DK) s_p6[tid] = p6;
+    // terms through S_in and the tail operand (each entry owned by this thread)
+#pragma unroll
+    for (int e = 0; e < Q; ++e) {
+        const int i = qd + e, t = tr;
+        const double lm = lam[t * DK + i], lmC = lam[(C - 1) * DK + i];
+        const float gm = expf((float)lm), et = expf((float)(lmC - lm));
+        const bool ok = t < L;
+        const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+        const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+        const float kp = kap[t * DK + i];
+        const float dq = a.scale * gm * p4[e];  // O = scale Qbar S_in
+        const float dk = -gm * p3[e];           // X = V - Kbar S_in
+        const float dkp = et * p5[e];           // S_out = ... + Ktail^T Delta
+        if (ok) {
+            a.dq[row(t) * DK + i] = dq;
+            a.dk[row(t) * DK + i] = dk;
+        }
+        dkap[t * DK + i] = dkp;
+        dlam[t * DK + i] = qq * dq + kk * dk - kp * dkp;
+        s_c[t * LDZ + i] = kp * dkp;
+    }
+    __syncthreads();
+
+    // ---- terms through T and B (decay ratios from the log-decays), by channel slabs ---------
+    constexpr int EPT = SLB / 4;  // channels per thread in a slab
+    const int ce = (tid & 3) * EPT;
+    for (int s0 = 0; s0 < DK; s0 += SLB) {
+        for (int e = tid; e < C * SLB; e += NTH) {
+            const int t = e / SLB, ii = e % SLB, i = s0 + ii;
+            const bool ok = t < L;
+            s_q[t * LDS_ + ii] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+            s_k[t * LDS_ + ii] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+            s_kp[t * LDS_ + ii] = kap[t * DK + i];
+            s_l[t * LDS_ + ii] = lam[t * DK + i];
+        }
+        __syncthreads();
+        float dqB[EPT], dkT[EPT], dkpB[EPT], dkpT[EPT];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) dqB[e] = dkT[e] = dkpB[e] = dkpT[e] = 0.f;
+        // row tr as the later token t: sum over s <= t
+        for (int s = 0; s <= tr; ++s) {
+            const float b = s_dB[tr * LDC + s], tt = s_dT[tr * LDC + s];
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+                const int ii = ce + e;
+                const float rt = __expf((float)(s_l[tr * LDS_ + ii] - s_l[s * LDS_ + ii]));
+                const float x = s_kp[s * LDS_ + ii] * rt;
+                dqB[e] = fmaf(b, x, dqB[e]);
+                dkT[e] = fmaf(tt, x, dkT[e]);
+            }
+        }
+        // row tr as the earlier token s: sum over t >= s
+        for (int t = tr; t < C; ++t) {
+            const float b = s_dB[t * LDC + tr], tt = s_dT[t * LDC + tr];
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+                const int ii = ce + e;
+                const float rt = __expf((float)(s_l[t * LDS_ + ii] - s_l[tr * LDS_ + ii]));
+                dkpB[e] = fmaf(b, s_q[t * LDS_ + ii] * rt, dkpB[e]);
+                dkpT[e] = fmaf(tt, s_k[t * LDS_ + ii] * rt, dkpT[e]);
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int ii = ce + e, i = s0 + ii, t = tr;
+            const float dkp = dkpB[e] + dkpT[e];
+            if (t < L) {
+                a.dq[row(t) * DK + i] += dqB[e];
+                a.dk[row(t) * DK + i] += dkT[e];
+            }
+            dkap[t * DK + i] += dkp;
+            dlam[t * DK + i] += s_q[t * LDS_ + ii] * dqB[e] + s_k[t * LDS_ + ii] * dkT[e] -
+                                s_kp[t * LDS_ + ii] * dkp;
+        }
+        __syncthreads();
+    }
+
+    // ---- d(log-decay) -> dalpha (memory part): alpha_s dalpha_s = sum_{t >= s} dlambda_t, the
+    // chunk-end terms (gamma_C) entering at the last token ---------------------------------------
+    if (tid < DK) {
+        const int i = tid;
+        float acc = gC[i] * s_p6[i];
+        for (int t = 0; t < C; ++t) acc += s_c[t * LDZ + i];
+        for (int t = C - 1; t >= 0; --t) {
+            acc += dlam[t * DK + i];
+            float al = 1.f;
+            if (t < L) al = APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
+            dal[t * DK + i] = t < L ? acc / al : 0.f;
+        }
+    }
+
+    // ---- coefficients of the variance adjoint: lambda_{t-1} = A_t lambda_t + B_t ------------
+    for (int j = 0; j < C / 4; ++j) {
+        const int t = (C / 4) * w + j;
+        const bool ok = t < L;
+        const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+        const float dn = den[t];
+        if constexpr (DIAG) {
+            float s1 = 0.f;
+            for (int i = lane; i < DK; i += 64) s1 += dkap[t * DK + i] * kap[t * DK + i];
+            const float dden = -wave_sum(s1) / dn;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+                const float al = ok ? ld<TI>(a.alpha, row(t) * DK + i) : 1.f;
+                const float ph = phat[t * DK + i];
+                const float u = a.mu * kk * kk / rr, gg = 1.f + u * ph;
+                const float c = dkap[t * DK + i] * kk / dn + dden * kk * kk;
+                a.acf[(gh * C + t) * NCHAN + i] = ok ? al * al / (gg * gg) : 1.f;
+                a.bcf[(gh * C + t) * NCHAN + i] = ok ? al * al * c : 0.f;
+            }
+            if (lane == 0) a.aux[gh * C + t] = dden;
+        } else {
+            float sb = 0.f, sk = 0.f, sa = 0.f;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+                sb += dkap[t * DK + i] * kk;
+                sk += kk * kk;
+                if (APC) {
+                    const float al = ok ? ld<TI>(a.alpha, row(t) * DK + i) : 1.f;
+                    sa += al * al;
+                }
+            }
+            const float dbeta = wave_sum(sb), nk = wave_sum(sk);
+            float aa;
+            if (APC) aa = wave_sum(sa) / (float)DK;
+            else {
+                const float al = ok ? ld<TI>(a.alpha, row(t)) : 1.f;
+                aa = al * al;
+            }
+            if (lane == 0) {
+                const float bh = phat[t * DK];
+                const float u = a.mu * nk / ((float)DK * rr), gg = 1.f + u * bh;
+                a.acf[gh * C + t] = ok ? aa / (gg * gg) : 1.f;
+                a.bcf[gh * C + t] = ok ? aa * dbeta * rr / (dn * dn) : 0.f;
+                a.aux[gh * C + t] = dbeta;
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// bw_scan: the variance adjoint backwards in time, one thread per (sequence, head, channel)
+// ------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void bw_scan(Args a, int nchan)
+{
+    const int gid = (int)(blockIdx.x * 64 + threadIdx.x);
+    const int H = a.H;
+    if (gid >= a.cm.N * H * nchan) return;
+    const int slot = gid / nchan, c = gid % nchan, n = slot / H, h = slot % H;
+    int t0, t1, g0, nch;
+    seq_span(a.cm, n, t0, t1);
+    seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
+    float lp = a.dP_T ? a.dP_T[(size_t)slot * nchan + c] : 0.f;
+    for (int ci = nch - 1; ci >= 0; --ci) {
+        const size_t base = ((size_t)(g0 + ci) * H + h) * C;
+        for (int tb = C - 16; tb >= 0; tb -= 16) {
+            float av[16], bv[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                av[e] = a.acf[(base + tb + e) * nchan + c];
+                bv[e] = a.bcf[(base + tb + e) * nchan + c];
+            }
+#pragma unroll
+            for (int e = 15; e >= 0; --e) {
+                a.lamp[(base + tb + e) * nchan + c] = lp;
+                lp = fmaf(av[e], lp, bv[e]);
+            }
+        }
+    }
+    if (a.dP0) a.dP0[(size_t)slot * nchan + c] = lp;
+}
+
+// ------------------------------------------------------------------------------------------
+// bw_final: token-local gradients of the gain stage
+// ------------------------------------------------------------------------------------------
+template <class TI, int DK, int VARIANT, bool APC>
+__global__ __launch_bounds__(NTH) void bw_final(Args a)
+{
+    using R = BwRec<DK>;
+    constexpr bool DIAG = VARIANT == 0;
+    constexpr int NCHAN = DIAG ? DK : 1;
+    const int H = a.H;
+    const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
+    int n, c0, c1;
+    bool last;
+    if (!locate_chunk<C>(a.cm, g, n, c0, c1, last)) return;
+    const int L = c1 - c0;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const size_t gh = (size_t)g * H + h;
+    const char* rec = a.rec + gh * R::BYTES;
+    const float* phat = (const float*)(rec + R::OFF_PHAT);
+    const float* pprv = (const float*)(rec + R::OFF_PPRV);
+    const float* den = (const float*)(rec + R::OFF_DEN);
+    const float* dkap = a.dkap + gh * C * DK;
+    const float* dal = a.dal + gh * C * DK;
+    const float mu = a.mu;
+    for (int j = 0; j < C / 4; ++j) {
+        const int t = (C / 4) * w + j;
+        if (t >= L) break;  // uniform per wave
+        const size_t row = (size_t)(c0 + t) * H + h;
+        const float rr = ld<TI>(a.r, row), dn = den[t], aux = a.aux[gh * C + t];
+        if constexpr (DIAG) {
+            const float dden = aux;
+            float s2 = 0.f;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = ld<TI>(a.k, row * DK + i), al = ld<TI>(a.alpha, row * DK + i);
+                const float ph = phat[t * DK + i], pp = pprv[t * DK + i];
+                const float dkp = dkap[t * DK + i];
+                const float lp = a.lamp[(gh * C + t) * NCHAN + i];
+                const float u = mu * kk * kk / rr, gg = 1.f + u * ph, ig2 = 1.f / (gg * gg);
+                const float dph = dkp * kk / dn + dden * kk * kk + lp * ig2;
+                const float du = -lp * ph * ph * ig2;
+                a.dk[row * DK + i] += dkp * ph / dn + 2.f * dden * ph * kk + du * 2.f * mu * kk / rr;
+                s2 += du * mu * kk * kk;
+                a.dalpha[row * DK + i] = dal[t * DK + i] + dph * 2.f * al * pp;
+                a.domega[row * DK + i] = dph;
+            }
+            s2 = wave_sum(s2);
+            if (lane == 0) a.dr[row] = dden - s2 / (rr * rr);
+        } else {
+            const float dbeta = aux, bh = phat[t * DK], pp = pprv[t * DK];
+            const float lp = a.lamp[gh * C + t];
+            float sk = 0.f, sa = 0.f, sd = 0.f;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = ld<TI>(a.k, row * DK + i);
+                sk += kk * kk;
+                sd += dal[t * DK + i];
+            }
+            const float nk = wave_sum(sk);
+            sd = wave_sum(sd);
+            const float a0 = APC ? 0.f : ld<TI>(a.alpha, row);
+            (void)sa;
+            const float beta = bh / dn;
+            const float u = mu * nk / ((float)DK * rr), gg = 1.f + u * bh, ig2 = 1.f / (gg * gg);
+            const float dbh = lp * ig2 + dbeta * rr / (dn * dn);
+            const float du = -lp * bh * bh * ig2;
+            const float dr = -dbeta * bh / (dn * dn) - du * mu * nk / ((float)DK * rr * rr);
+            const float dnk = -dbeta * bh * bh / (dn * dn) + du * mu / ((float)DK * rr);
+            const float da = dbh * pp;
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = ld<TI>(a.k, row * DK + i);
+                a.dk[row * DK + i] += beta * dkap[t * DK + i] + 2.f * kk * dnk;
+                if (APC) {
+                    const float al = ld<TI>(a.alpha, row * DK + i);
+                    a.dalpha[row * DK + i] = dal[t * DK + i] + da * 2.f * al / (float)DK;
+                }
+            }
+            if (lane == 0) {
+                a.dr[row] = dr;
+                a.domega[row] = dbh;
+                if (!APC) a.dalpha[row] = sd + da * 2.f * a0;
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------------------
+// host side
+// ------------------------------------------------------------------------------------------
+template <class K>
+hipError_t lds_attr(K* kernel, size_t bytes)
+{
+    if (bytes <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+
+size_t rec_bytes(int dk)
+{
+    switch (dk) {
+    case 16: return BwRec<16>::BYTES;
+    case 32: return BwRec<32>::BYTES;
+    case 64: return BwRec<64>::BYTES;
+    default: return BwRec<128>::BYTES;
+    }
+}
+
+template <class TI, int DK, int VARIANT, bool APC>
+hipError_t run(const BwdCall& bc, hipStream_t st)
+{
+    using VC = fwd::VarCfg<TI, DK, VARIANT, APC>;
+    const SeqArgs& sa = bc.sa;
+    const bool packed = sa.cu_seqlens != nullptr;
+    const BwMap m = bw_map(VARIANT, packed, sa.N, sa.B, sa.T, sa.H, DK, bc.dv, BwRec<DK>::BYTES);
+    char* ws = (char*)bc.workspace;
+    hipError_t e;
+    ChunkMap cm;
+    cm.cu = sa.cu_seqlens;
+    cm.choff = packed ? (const int32_t*)(ws + m.choff) : nullptr;
+    cm.N = sa.N;
+    cm.T = sa.T;
+    cm.ntok = sa.B * sa.T;
+    cm.maxch = m.maxch;
+    if (packed &&
+        (e = launch_chunk_table(sa.cu_seqlens, sa.N, cm.ntok, C, m.maxch,
+                                (int32_t*)(ws + m.choff), st)) != hipSuccess)
+        return e;
+    const size_t ntok = (size_t)sa.B * sa.T * sa.H;
+    fwd::InArgs in = {};
+    in.q = bc.q; in.k = bc.k; in.alpha = bc.alpha; in.omega = bc.omega; in.r = bc.r;
+    in.bytes_k = (uint32_t)(ntok * DK * sizeof(TI));
+    in.bytes_h = (uint32_t)(ntok * sizeof(TI));
+    in.H = sa.H;
+    in.mu = bc.mu;
+    float4* summ = (float4*)(ws + m.summ);
+    float2* carry = (float2*)(ws + m.carry);
+    const dim3 cgrid((unsigned)((size_t)m.maxch * sa.H));
+    if (m.maxch > 0) {
+        hipLaunchKernelGGL((fwd::summary_kernel<TI, VC>), cgrid, dim3(NTH), 0, st, in, cm, summ);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_carry_scan(summ, bc.P0, cm, C, sa.H, VC::NCHAN, carry, nullptr, st)) !=
+            hipSuccess)
+            return e;
+    }
+    Args a = {};
+    a.q = bc.q; a.k = bc.k; a.v = bc.v; a.alpha = bc.alpha; a.omega = bc.omega; a.r = bc.r;
+    a.dO = bc.dO; a.S0 = bc.S0; a.dS_T = bc.dS_T; a.dP_T = bc.dP_T;
+    a.dq = bc.gq; a.dk = bc.gk; a.dv = bc.gv; a.dalpha = bc.galpha; a.domega = bc.gomega;
+    a.dr = bc.gr; a.dS0 = bc.gS0; a.dP0 = bc.gP0;
+    a.cm = cm;
+    a.H = sa.H;
+    a.DV = bc.dv;
+    a.BV = bc.dv < 32 ? bc.dv : 32;
+    a.mu = bc.mu;
+    a.scale = bc.scale;
+    a.carry = carry;
+    a.rec = ws + m.rec;
+    a.ckpt = (float*)(ws + m.ckpt);
+    a.dlt = (float*)(ws + m.dlt);
+    a.dso = (float*)(ws + m.dso);
+    a.dkap = (float*)(ws + m.dkap);
+    a.dlam = (float*)(ws + m.dlam);
+    a.dal = (float*)(ws + m.dal);
+    a.acf = (float*)(ws + m.acf);
+    a.bcf = (float*)(ws + m.bcf);
+    a.aux = (float*)(ws + m.aux);
+    a.lamp = (float*)(ws + m.lamp);
+    static bool attr = false;
+    if (!attr) {
+        if ((e = lds_attr(bw_prep<TI, DK, VARIANT, APC>, PrepLds<DK>::TOTAL)) != hipSuccess ||
+            (e = lds_attr(bw_fwalk<TI, DK>, WalkLds<DK>::TOTAL)) != hipSuccess ||
+            (e = lds_attr(bw_rwalk<TI, DK>, WalkLds<DK>::TOTAL)) != hipSuccess ||
+            (e = lds_attr(bw_grad<TI, DK, VARIANT, APC>, GradLds<DK>::TOTAL)) != hipSuccess)
+            return e;
+        attr = true;
+    }
+    if (m.maxch > 0) {
+        hipLaunchKernelGGL((bw_prep<TI, DK, VARIANT, APC>), cgrid, dim3(NTH), PrepLds<DK>::TOTAL,
+                           st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const int NV = bc.dv / a.BV;
+    const dim3 wgrid((unsigned)((size_t)sa.N * sa.H * NV));
+    hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTH), WalkLds<DK>::TOTAL, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTH), WalkLds<DK>::TOTAL, st, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (m.maxch > 0) {
+        hipLaunchKernelGGL((bw_grad<TI, DK, VARIANT, APC>), cgrid, dim3(NTH), GradLds<DK>::TOTAL,
+                           st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const int nthr = sa.N * sa.H * VC::NCHAN;
+    hipLaunchKernelGGL(bw_scan, dim3((unsigned)((nthr + 63) / 64)), dim3(64), 0, st, a,
+                       (int)VC::NCHAN);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (m.maxch > 0) {
+        hipLaunchKernelGGL((bw_final<TI, DK, VARIANT, APC>), cgrid, dim3(NTH), 0, st, a);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+template <class TI, int DK>
+hipError_t run_v(const BwdCall& bc, hipStream_t st)
+{
+    if (bc.variant == 0) return run<TI, DK, 0, true>(bc, st);
+    if (bc.apc) return run<TI, DK, 1, true>(bc, st);
+    return run<TI, DK, 1, false>(bc, st);
+}
+
+template <class TI>
+hipError_t run_dk(const BwdCall& bc, hipStream_t st)
+{
+    switch (bc.dk) {
+    case 16: return run_v<TI, 16>(bc, st);
+    case 32: return run_v<TI, 32>(bc, st);
+    case 64: return run_v<TI, 64>(bc, st);
+    case 128: return run_v<TI, 128>(bc, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace bwd
+
+size_t backward_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
+                                int dv)
+{
+    return bwd::bw_map(variant, packed, N, B, T, H, dk, dv, bwd::rec_bytes(dk)).total;
+}
+
+hipError_t launch_backward(const BwdCall& bc, hipStream_t stream)
+{
+    if (bc.dtype == KDN_F32) return bwd::run_dk<float>(bc, stream);
+    return bwd::run_dk<bf16>(bc, stream);
+}
+
+}  // namespace kdn

@@ -128,6 +128,22 @@ struct FwdCall {
     void* workspace;  // chunked_workspace_bytes(...) bytes
     LayerOpts ly;
 };
+// Backward of the chunked forward (kdn_bwd.hip). Gradients are float32.
+struct BwdCall {
+    int variant, apc;
+    const void *q, *k, *v, *alpha, *omega, *r, *dO;  // dO in the input dtype, or nullptr
+    const float *S0, *P0, *dS_T, *dP_T;
+    float *gq, *gk, *gv, *galpha, *gomega, *gr, *gS0, *gP0;
+    SeqArgs sa;
+    int dk, dv;
+    kdn_dtype_t dtype;
+    float mu, scale;
+    void* workspace;  // backward_workspace_bytes(...) bytes
+};
+size_t backward_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
+                                int dv);
+hipError_t launch_backward(const BwdCall& bc, hipStream_t stream);
+
 bool chunked_supported(int chunk);
 size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
                                kdn_dtype_t dtype);

@@ -18,6 +18,8 @@ Functions mirror the C entry points:
   qk_l2norm=False, mu_t=None, want_beta_eff=False) -> (o, S_T, P_T, beta_eff or None)``
 * ``decode_step_layer(variant, ..., gates_preact=False, r_min=0.01, qk_l2norm=False,
   mu_t=None, beta_eff=None) -> o``
+* ``backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
+  scale=None, dO=None, dS_T=None, dP_T=None) -> dict`` of float32 gradients
 """
 
 from __future__ import annotations
@@ -84,11 +86,15 @@ def lib():
     L.kdn_decode_step_layer.argtypes = ([i32] + [vp] * 10 + [i32] * 5 +
                                         [ctypes.c_int, i32, f32, f32, ctypes.POINTER(LayerOpts),
                                          vp])
+    L.kdn_backward.argtypes = ([i32] + [vp] * 9 + [i32] * 6 + [ctypes.c_int, i32, f32, f32] +
+                               [vp] * 11 + [vp, sz, vp])
+    L.kdn_backward_workspace_bytes.argtypes = [i32] * 8
+    L.kdn_backward_workspace_bytes.restype = sz
     L.kdn_forward_workspace_bytes.argtypes = [i32] * 7 + [ctypes.c_int, i32, i32]
     L.kdn_gain_workspace_bytes.argtypes = [i32] * 6
     for name in ("kdn_forward_diag", "kdn_forward_iso", "kdn_forward_diag_noalloc",
                  "kdn_decode_step", "kdn_gain_diag", "kdn_gain_iso", "kdn_forward_layer",
-                 "kdn_decode_step_layer"):
+                 "kdn_decode_step_layer", "kdn_backward"):
         getattr(L, name).restype = ctypes.c_int
     L.kdn_forward_workspace_bytes.restype = sz
     L.kdn_gain_workspace_bytes.restype = sz
@@ -333,3 +339,39 @@ def decode_step_layer(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu
                                      ctypes.byref(opts), _stream(k.device))
     _check(st, "kdn_decode_step_layer")
     return o
+
+
+def backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
+             scale=None, dO=None, dS_T=None, dP_T=None):
+    """Gradients of a loss through the forward, given its gradients dO (input dtype), dS_T and
+    dP_T (float32); None = zero. Returns a dict of float32 tensors dq, dk, dv, dalpha, domega,
+    dr, dS0, dP0 shaped like the inputs (dS0 / dP0 like S_T / P_T)."""
+    vid = {"diag": 0, "iso": 1}[variant] if isinstance(variant, str) else int(variant)
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    _same(k.dtype, q, v, alpha, omega, r, dO)
+    dev = k.device
+    N = B if cu_seqlens is None else cu_seqlens.numel() - 1
+    mu = float(dk if mu is None else mu)
+    scale = float(dk ** -0.5 if scale is None else scale)
+    if cu_seqlens is not None and cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = dict(dq=torch.empty(q.shape, **f32), dk=torch.empty(k.shape, **f32),
+             dv=torch.empty(v.shape, **f32), dalpha=torch.empty(alpha.shape, **f32),
+             domega=torch.empty(omega.shape, **f32), dr=torch.empty(r.shape, **f32),
+             dS0=torch.empty((N, H, dk, dv), **f32),
+             dP0=torch.empty((N, H, dk) if vid == 0 else (N, H), **f32))
+    ws_bytes = lib().kdn_backward_workspace_bytes(vid, N, B, T, H, dk, dv,
+                                                  int(cu_seqlens is not None))
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    apc = int(vid == 0 or alpha.dim() == 4)
+    st = lib().kdn_backward(vid, _ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(omega), _ptr(r),
+                            _ptr(_f32(S0)), _ptr(_f32(P0)), _ptr(cu_seqlens), N, B, T, H, dk, dv,
+                            _dtype_code(k), apc, ctypes.c_float(mu), ctypes.c_float(scale),
+                            _ptr(dO), _ptr(_f32(dS_T)), _ptr(_f32(dP_T)), _ptr(g["dq"]),
+                            _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["dalpha"]), _ptr(g["domega"]),
+                            _ptr(g["dr"]), _ptr(g["dS0"]), _ptr(g["dP0"]), _ptr(ws), ws_bytes,
+                            _stream(dev))
+    _check(st, "kdn_backward")
+    return g
