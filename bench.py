@@ -13,7 +13,8 @@ Prints one JSON line: tokens/s of the headline forward, the roofline position of
 (algorithmic bytes per call / the HIP-event duration of the call on the caller's stream, against
 the 8 TB/s HBM peak), the CPU oracle timed on a bounded sample of the same workload, and one
 object per other workload of the path (the isotropic forward, the packed variable-length batch,
-the decode workload's prefill and decode steps, the gain scan alone), each timed the same way.
+the decode workload's prefill and decode steps, the gain scan alone, the backward, the layer
+forward with its maps fused), each timed the same way.
 The larger workloads draw their inputs on the GPU with the same laws (timing only; their parity
 is checked by the tests on host-drawn inputs).
 """
@@ -219,6 +220,70 @@ def bench_gain(torch, kdn, x, steps):
                     "kernels": "gain scan: chunk summaries, carry scan, emission"})
 
 
+def backward_bytes(tokens, H, dk, dv, es):
+    """Minimum traffic of one diagonal backward: the forward's inputs and dO read once, the
+    float32 gradients of q, k, v, alpha, omega and r written once."""
+    return tokens * H * ((5 * dk + 2 * dv) * es + es + (4 * dk + dv + 1) * 4)
+
+
+def bench_backward(torch, kdn, x, steps):
+    """kdn_backward at the headline shape, with random incoming adjoints of o, S_T and P_T."""
+    B, T, H, d = x["k"].shape
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    dO = torch.randn((B, T, H, d), generator=g, device="cuda").to(torch.bfloat16)
+    dS = torch.randn((B, H, d, d), generator=g, device="cuda")
+    dP = torch.randn((B, H, d), generator=g, device="cuda")
+    ms = time_calls(torch, lambda: kdn.backward("diag", *[x[n] for n in NAMES], mu=float(d),
+                                                dO=dO, dS_T=dS, dP_T=dP), steps, 3)
+    return summary(ms, backward_bytes(B * T, H, d, d, 2), B * T,
+                   {"workload": "diag-bwd-B4-H16-T4096-d128 (float32 gradients)",
+                    "kernels": "backward: chunk summaries, carry scan, per-chunk replay, forward "
+                               "walk, reverse walk, per-chunk gradients, variance-adjoint scan, "
+                               "per-token gain gradients"})
+
+
+def bench_layer(torch, kdn, steps):
+    """The layer forward (kdn_forward_layer: gate pre-activations, q/k L2 norm, effective-write
+    output) at the headline shape, and beside it the same layer done unfused: the maps as torch
+    elementwise ops, then the plain forward."""
+    B, T, H, d = 4, 4096, 16, 128
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    bf = torch.bfloat16
+
+    def normal(shape, shift=0.0):
+        return (torch.randn(shape, generator=g, device="cuda") + shift).to(bf)
+
+    q, k, v = normal((B, T, H, d)), normal((B, T, H, d)), normal((B, T, H, d))
+    a_pre, w_pre, r_pre = normal((B, T, H, d), 2.0), normal((B, T, H, d)), normal((B, T, H))
+    sp = torch.nn.functional.softplus
+
+    def fused():
+        return kdn.forward_layer("diag", q, k, v, a_pre, w_pre, r_pre, mu=float(d),
+                                 gates_preact=True, r_min=0.01, qk_l2norm=True,
+                                 want_beta_eff=True)
+
+    def unfused():
+        qn = (q.float() / q.float().norm(dim=-1, keepdim=True)).to(bf)
+        kn = (k.float() / k.float().norm(dim=-1, keepdim=True)).to(bf)
+        a = torch.sigmoid(a_pre.float()).to(bf)
+        w = sp(w_pre.float()).to(bf)
+        r = (0.01 + sp(r_pre.float())).to(bf)
+        return kdn.forward_diag(qn, kn, v, a, w, r, mu=float(d))
+
+    ms = time_calls(torch, fused, steps, 3)
+    ms_u = time_calls(torch, unfused, steps, 3)
+    rec = summary(ms, forward_bytes(B * T, B, H, d, d, 2, "diag") + B * T * H * 4, B * T,
+                  {"workload": "diag-layer-fwd-B4-H16-T4096-d128 (pre-activation gates, q/k "
+                               "L2 norm, beta_eff out)",
+                   "kernels": "layer forward: the forward's 4 kernels with the maps fused"})
+    rec["unfused_ms_median"] = round(float(np.median(ms_u)), 4)
+    rec["unfused"] = "torch sigmoid / softplus / L2 norm in float32, rounded to bf16, then the " \
+                     "plain forward"
+    return rec
+
+
 # ---------------------------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the headline workload
 # ---------------------------------------------------------------------------------------------
@@ -287,7 +352,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    choices=["all", "headline", "iso", "varlen", "decode", "gain"],
+                    choices=["all", "headline", "iso", "varlen", "decode", "gain", "backward",
+                             "layer"],
                     help="run only the headline forward or one other workload (profiling runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (used to "
@@ -314,10 +380,11 @@ def main():
                           "launches": 5}))
         return
     kdn.lib()
-    if args.only in ("iso", "varlen", "decode"):
+    if args.only in ("iso", "varlen", "decode", "layer"):
         fn = {"iso": lambda: bench_iso(torch, kdn, args.steps),
               "varlen": lambda: bench_varlen(torch, kdn, W, args.steps),
-              "decode": lambda: bench_decode_workload(torch, kdn, args.steps)}[args.only]
+              "decode": lambda: bench_decode_workload(torch, kdn, args.steps),
+              "layer": lambda: bench_layer(torch, kdn, args.steps)}[args.only]
         print(json.dumps({args.only: fn()}), flush=True)
         return
 
@@ -327,6 +394,9 @@ def main():
            for n in NAMES}
     if args.only == "gain":
         print(json.dumps({"gain": bench_gain(torch, kdn, dev, args.steps)}), flush=True)
+        return
+    if args.only == "backward":
+        print(json.dumps({"backward": bench_backward(torch, kdn, dev, args.steps)}), flush=True)
         return
 
     def step():
@@ -390,7 +460,9 @@ def main():
     if args.only == "all":
         rec["workloads"] = {"iso_forward": bench_iso(torch, kdn, args.steps),
                             "varlen_forward": bench_varlen(torch, kdn, W, args.steps),
-                            "gain_scan": bench_gain(torch, kdn, dev, args.steps)}
+                            "gain_scan": bench_gain(torch, kdn, dev, args.steps),
+                            "backward": bench_backward(torch, kdn, dev, args.steps),
+                            "layer_forward": bench_layer(torch, kdn, args.steps)}
         rec["workloads"].update(bench_decode_workload(torch, kdn, args.steps))
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(x, min(16, os.cpu_count() or 1))
