@@ -38,7 +38,10 @@ namespace kdn {
 namespace bwd {
 
 using fwd::C;
-constexpr int NTH = 256;
+constexpr int NTH = 256;  // bw_final and the forward's summary kernel
+// bw_prep, the walks and bw_grad hold a whole chunk in LDS (one workgroup per CU): 512 threads
+// put two waves on every SIMD to hide the LDS and memory latency
+constexpr int NTB = 512, NWB = NTB / 64;
 
 // Per (chunk, head) record written by bw_prep.
 template <int DK>
@@ -60,7 +63,7 @@ struct BwRec {
 
 // Workspace of one backward call.
 struct BwMap {
-    size_t choff, summ, carry, rec, ckpt, dlt, dso, dkap, dlam, dal, acf, bcf, aux, lamp, total;
+    size_t choff, summ, carry, rec, ckpt, dlt, dso, dkap, dal, acf, bcf, aux, lamp, total;
     int maxch;
 };
 
@@ -85,7 +88,6 @@ inline BwMap bw_map(int variant, bool packed, int N, int B, int T, int H, int dk
     m.dlt = take(ch * C * dv * 4);
     m.dso = take(ch * dk * dv * 4);
     m.dkap = take(ch * C * dk * 4);
-    m.dlam = take(ch * C * dk * 4);
     m.dal = take(ch * C * dk * 4);
     m.acf = take(ch * C * nchan * 4);
     m.bcf = take(ch * C * nchan * 4);
@@ -104,7 +106,7 @@ struct Args {
     float mu, scale;
     const float2* carry;
     char* rec;
-    float *ckpt, *dlt, *dso, *dkap, *dlam, *dal, *acf, *bcf, *aux, *lamp;
+    float *ckpt, *dlt, *dso, *dkap, *dal, *acf, *bcf, *aux, *lamp;
 };
 
 template <class TI>
@@ -118,40 +120,48 @@ __device__ __forceinline__ float ld(const void* p, size_t i)
 // ------------------------------------------------------------------------------------------
 template <int DK>
 struct PrepLds {
-    static constexpr int SLB = DK < 32 ? DK : 32;     // channel slab of the T / B products
-    static constexpr size_t OFF_Z = 0;                                       // [C][DK+1]
-    static constexpr size_t OFF_DEN = OFF_Z + (size_t)C * (DK + 1) * 4;      // [C]
-    static constexpr size_t OFF_BETA = OFF_DEN + C * 4;
-    static constexpr size_t OFF_AA = OFF_BETA + C * 4;
-    static constexpr size_t OFF_NK = OFF_AA + C * 4;
-    static constexpr size_t OFF_SK = OFF_NK + C * 4;                         // [C][SLB+1]
-    static constexpr size_t OFF_SQ = OFF_SK + (size_t)C * (SLB + 1) * 4;
-    static constexpr size_t OFF_SP = OFF_SQ + (size_t)C * (SLB + 1) * 4;
-    static constexpr size_t OFF_SL = al16(OFF_SP + (size_t)C * (SLB + 1) * 4);  // double
-    static constexpr size_t OFF_T = OFF_SL + (size_t)C * (SLB + 1) * 8;      // [C][C+1]
-    static constexpr size_t OFF_A = OFF_T + (size_t)C * (C + 1) * 4;
-    static constexpr size_t TOTAL = al16(OFF_A + (size_t)C * (C + 1) * 4);
+    static constexpr int SLB = DK < 32 ? DK : 32;  // channel slab of the T / B products
+    static constexpr int LDK = DK + 1, LDC = C + 1, LDL = SLB + 1;
+    static constexpr size_t SZ_CK = (size_t)C * LDK * 4;
+    static constexpr size_t OFF_K = 0;                    // k [C][LDK]
+    static constexpr size_t OFF_AQ = OFF_K + SZ_CK;       // alpha, then q [C][LDK]
+    static constexpr size_t OFF_WP = OFF_AQ + SZ_CK;      // omega, then p_hat, then kappa
+    static constexpr size_t OFF_R = OFF_WP + SZ_CK;       // r [C]
+    static constexpr size_t OFF_DEN = OFF_R + C * 4;      // gain denominators [C]
+    static constexpr size_t OFF_BETA = OFF_DEN + C * 4;   // isotropic beta [C]
+    static constexpr size_t OFF_AA = OFF_BETA + C * 4;    // isotropic mean alpha^2 [C]
+    static constexpr size_t OFF_NK = OFF_AA + C * 4;      // isotropic ||k||^2 [C]
+    static constexpr size_t OFF_W1 = OFF_NK + C * 4;      // isotropic omega [C]
+    static constexpr size_t OFF_LC = al16(OFF_W1 + C * 4);            // lambda_C [DK] double
+    static constexpr size_t OFF_L = al16(OFF_LC + (size_t)DK * 8);    // lambda slab [C][LDL]
+    static constexpr size_t OFF_T = OFF_L + (size_t)C * LDL * 8;      // T [C][LDC]
+    static constexpr size_t OFF_A = OFF_T + (size_t)C * LDC * 4;      // (I + T)^-1 [C][LDC]
+    static constexpr size_t OFF_X = OFF_A + (size_t)C * LDC * 4;      // block products [3][16][17]
+    static constexpr size_t TOTAL = al16(OFF_X + (size_t)3 * 16 * 17 * 4);
 };
 
 template <class TI, int DK, int VARIANT, bool APC>
-__global__ __launch_bounds__(NTH) void bw_prep(Args a)
+__global__ __launch_bounds__(NTB) void bw_prep(Args a)
 {
     using R = BwRec<DK>;
     using LY = PrepLds<DK>;
     constexpr bool DIAG = VARIANT == 0;
-    constexpr int SLB = LY::SLB, LDZ = DK + 1, LDS_ = SLB + 1, LDC = C + 1;
+    constexpr int SLB = LY::SLB, LDK = LY::LDK, LDC = LY::LDC, LDL = LY::LDL;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    float* s_z = (float*)(smem + LY::OFF_Z);
+    float* s_k = (float*)(smem + LY::OFF_K);
+    float* s_aq = (float*)(smem + LY::OFF_AQ);
+    float* s_wp = (float*)(smem + LY::OFF_WP);
+    float* s_r = (float*)(smem + LY::OFF_R);
     float* s_den = (float*)(smem + LY::OFF_DEN);
     float* s_beta = (float*)(smem + LY::OFF_BETA);
     float* s_aa = (float*)(smem + LY::OFF_AA);
     float* s_nk = (float*)(smem + LY::OFF_NK);
-    float* s_k = (float*)(smem + LY::OFF_SK);
-    float* s_q = (float*)(smem + LY::OFF_SQ);
-    float* s_p = (float*)(smem + LY::OFF_SP);
-    double* s_l = (double*)(smem + LY::OFF_SL);
+    float* s_w1 = (float*)(smem + LY::OFF_W1);
+    double* s_lc = (double*)(smem + LY::OFF_LC);
+    double* s_l = (double*)(smem + LY::OFF_L);
     float* s_T = (float*)(smem + LY::OFF_T);
     float* s_A = (float*)(smem + LY::OFF_A);
+    float* s_X = (float*)(smem + LY::OFF_X);
 
     const int H = a.H;
     const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
@@ -161,66 +171,65 @@ __global__ __launch_bounds__(NTH) void bw_prep(Args a)
     const int L = c1 - c0;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
-    float* kap = (float*)(rec + R::OFF_KAP);
-    float* phat = (float*)(rec + R::OFF_PHAT);
-    float* pprv = (float*)(rec + R::OFF_PPRV);
-    float* kbar = (float*)(rec + R::OFF_KBAR);
-    float* qbar = (float*)(rec + R::OFF_QBAR);
-    float* ktl = (float*)(rec + R::OFF_KTL);
-    double* lam = (double*)(rec + R::OFF_LAM);
-    float* Am = (float*)(rec + R::OFF_A);
-    float* Bm = (float*)(rec + R::OFF_B);
-    float* gC = (float*)(rec + R::OFF_GC);
-    float* den = (float*)(rec + R::OFF_DEN);
+    float* __restrict__ kap = (float*)(rec + R::OFF_KAP);
+    float* __restrict__ phat = (float*)(rec + R::OFF_PHAT);
+    float* __restrict__ pprv = (float*)(rec + R::OFF_PPRV);
+    float* __restrict__ kbar = (float*)(rec + R::OFF_KBAR);
+    float* __restrict__ qbar = (float*)(rec + R::OFF_QBAR);
+    float* __restrict__ ktl = (float*)(rec + R::OFF_KTL);
+    double* __restrict__ lam = (double*)(rec + R::OFF_LAM);
+    float* __restrict__ Am = (float*)(rec + R::OFF_A);
+    float* __restrict__ Bm = (float*)(rec + R::OFF_B);
+    float* __restrict__ gC = (float*)(rec + R::OFF_GC);
+    float* __restrict__ den = (float*)(rec + R::OFF_DEN);
     auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
-    auto alpha_at = [&](int t, int i) {
-        if (t >= L) return 1.f;
-        return APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
-    };
 
-    // ---- the variance chain through the chunk (eqs. kla-box-mobius / iso-kla-box-cov-update)
-    // from the carry, and the cumulative log-decay ----------------------------------------------
+    // ---- the chunk's inputs in LDS (padding tokens: alpha 1, k 0, omega 0, r 1) -----------
+    for (int e = tid; e < C * DK; e += NTB) {
+        const int t = e / DK, i = e % DK;
+        const bool ok = t < L;
+        s_k[t * LDK + i] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+        s_aq[t * LDK + i] =
+            ok ? (APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t))) : 1.f;
+        if (DIAG) s_wp[t * LDK + i] = ok ? ld<TI>(a.omega, row(t) * DK + i) : 0.f;
+    }
+    if (tid < C) {
+        const bool ok = tid < L;
+        s_r[tid] = ok ? ld<TI>(a.r, row(tid)) : 1.f;
+        if (!DIAG) s_w1[tid] = ok ? ld<TI>(a.omega, row(tid)) : 0.f;
+    }
+    __syncthreads();
+
+    // ---- the variance chain through the chunk from the carry (eq. kla-box-mobius, or
+    // iso-kla-box-cov-update) and the cumulative log-decay -------------------------------------
     if constexpr (DIAG) {
         if (tid < DK) {
             const float2 cz = a.carry[((size_t)g * H + h) * DK + tid];
             float p = cz.x / cz.y;
             for (int t = 0; t < C; ++t) {
-                const bool ok = t < L;
-                const float al = alpha_at(t, tid);
-                const float om = ok ? ld<TI>(a.omega, row(t) * DK + tid) : 0.f;
-                const float kk = ok ? ld<TI>(a.k, row(t) * DK + tid) : 0.f;
-                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                const float al = s_aq[t * LDK + tid], kk = s_k[t * LDK + tid];
                 pprv[t * DK + tid] = p;
-                const float ph = al * al * p + om;
+                const float ph = al * al * p + s_wp[t * LDK + tid];
                 phat[t * DK + tid] = ph;
-                s_z[t * LDZ + tid] = ph * kk * kk;
-                const float u = a.mu * kk * kk / rr;
+                s_wp[t * LDK + tid] = ph;
+                const float u = a.mu * kk * kk / s_r[t];
                 p = ph / (1.f + u * ph);
             }
         }
     } else {
-        // per-token mean alpha^2 and ||k||^2 (wave w: tokens 16 w .. 16 w + 15)
-        for (int j = 0; j < C / 4; ++j) {
-            const int t = (C / 4) * w + j;
+        for (int j = 0; j < C / NWB; ++j) {  // per-token mean alpha^2 and ||k||^2
+            const int t = (C / NWB) * w + j;
             float sa = 0.f, sk = 0.f;
             for (int i = lane; i < DK; i += 64) {
-                const float kk = t < L ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+                const float kk = s_k[t * LDK + i], al = s_aq[t * LDK + i];
                 sk += kk * kk;
-                if (APC) {
-                    const float al = alpha_at(t, i);
-                    sa += al * al;
-                }
+                sa += al * al;
             }
             sa = wave_sum(sa);
             sk = wave_sum(sk);
             if (lane == 0) {
-                float aa;
-                if (APC) aa = sa / (float)DK;
-                else {
-                    const float al = alpha_at(t, 0);
-                    aa = al * al;
-                }
-                s_aa[t] = t < L ? aa : 1.f;
+                const float a0 = s_aq[t * LDK];
+                s_aa[t] = APC ? sa / (float)DK : a0 * a0;
                 s_nk[t] = sk;
             }
         }
@@ -229,11 +238,9 @@ __global__ __launch_bounds__(NTH) void bw_prep(Args a)
             const float2 cz = a.carry[(size_t)g * H + h];
             float b = cz.x / cz.y;
             for (int t = 0; t < C; ++t) {
-                const bool ok = t < L;
-                const float om = ok ? ld<TI>(a.omega, row(t)) : 0.f;
-                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                const float rr = s_r[t];
                 pprv[t * DK] = b;
-                const float bh = s_aa[t] * b + om;
+                const float bh = s_aa[t] * b + s_w1[t];
                 phat[t * DK] = bh;
                 const float dn = rr + bh * s_nk[t];
                 s_den[t] = dn;
@@ -247,19 +254,24 @@ __global__ __launch_bounds__(NTH) void bw_prep(Args a)
     if (tid < DK) {
         double lm = 0.0;
         for (int t = 0; t < C; ++t) {
-            lm += (double)logf(alpha_at(t, tid));
+            lm += (double)logf(s_aq[t * LDK + tid]);
             lam[t * DK + tid] = lm;
         }
+        s_lc[tid] = lm;
+        gC[tid] = expf((float)lm);
     }
     __syncthreads();
     if constexpr (DIAG) {  // gain denominators r + sum_i p_hat_i k_i^2
-        for (int j = 0; j < C / 4; ++j) {
-            const int t = (C / 4) * w + j;
+        for (int j = 0; j < C / NWB; ++j) {
+            const int t = (C / NWB) * w + j;
             float z = 0.f;
-            for (int i = lane; i < DK; i += 64) z += s_z[t * LDZ + i];
+            for (int i = lane; i < DK; i += 64) {
+                const float kk = s_k[t * LDK + i];
+                z += s_wp[t * LDK + i] * kk * kk;
+            }
             z = wave_sum(z);
             if (lane == 0) {
-                const float dn = t < L ? ld<TI>(a.r, row(t)) + z : 1.f;
+                const float dn = t < L ? s_r[t] + z : 1.f;
                 s_den[t] = dn;
                 den[t] = dn;
             }
@@ -267,87 +279,105 @@ __global__ __launch_bounds__(NTH) void bw_prep(Args a)
         __syncthreads();
     }
 
-    // ---- kappa, gamma-scaled operands, the tail operand and gamma_C -------------------------
-    if (tid < DK) {
-        const double lmC = lam[(C - 1) * DK + tid];
-        for (int t = 0; t < C; ++t) {
-            const bool ok = t < L;
-            const float kk = ok ? ld<TI>(a.k, row(t) * DK + tid) : 0.f;
-            const float qq = ok ? ld<TI>(a.q, row(t) * DK + tid) : 0.f;
-            const float kp = DIAG ? phat[t * DK + tid] * kk / s_den[t] : s_beta[t] * kk;
-            kap[t * DK + tid] = kp;
-            const double lm = lam[t * DK + tid];
-            const float gm = expf((float)lm);
-            kbar[t * DK + tid] = gm * kk;
-            qbar[t * DK + tid] = gm * qq;
-            ktl[t * DK + tid] = expf((float)(lmC - lm)) * kp;
-        }
-        gC[tid] = expf((float)lmC);
+    // ---- kappa, gamma-scaled operands and the tail operand; q into LDS (alpha is dead) ------
+    for (int e = tid; e < C * DK; e += NTB) {
+        const int t = e / DK, i = e % DK;
+        const float kk = s_k[t * LDK + i];
+        const float qq = t < L ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+        const float kp = DIAG ? s_wp[t * LDK + i] * kk / s_den[t] : s_beta[t] * kk;
+        const double lm = lam[e];
+        const float gm = expf((float)lm);
+        kap[e] = kp;
+        kbar[e] = gm * kk;
+        qbar[e] = gm * qq;
+        ktl[e] = expf((float)(s_lc[i] - lm)) * kp;
+        s_wp[t * LDK + i] = kp;
+        s_aq[t * LDK + i] = qq;
     }
     __syncthreads();
 
-    // ---- T (s < t) and B (s <= t) by channel slabs; thread (t, 16 consecutive s) ------------
-    float accT[16], accB[16];
+    // ---- T (s < t) and B (s <= t), channel slab by channel slab; thread: row t, 16 columns s
+    float accT[8], accB[8];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) accT[e] = accB[e] = 0.f;
-    const int tr = tid >> 2, sg = (tid & 3) * 16;
+    for (int e = 0; e < 8; ++e) accT[e] = accB[e] = 0.f;
+    const int tr = tid >> 3, cl = tid & 7;  // row tr; columns s = cl + 8 e
     for (int s0 = 0; s0 < DK; s0 += SLB) {
-        for (int e = tid; e < C * SLB; e += NTH) {
-            const int t = e / SLB, ii = e % SLB, i = s0 + ii;
-            const bool ok = t < L;
-            s_k[t * LDS_ + ii] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-            s_q[t * LDS_ + ii] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
-            s_p[t * LDS_ + ii] = kap[t * DK + i];
-            s_l[t * LDS_ + ii] = lam[t * DK + i];
+        for (int e = tid; e < C * SLB; e += NTB) {
+            const int t = e / SLB, ii = e % SLB;
+            s_l[t * LDL + ii] = lam[t * DK + s0 + ii];
         }
         __syncthreads();
+#pragma unroll 1
+        for (int ii = 0; ii < SLB; ++ii) {
+            const double lt = s_l[tr * LDL + ii];
+            const float qt = s_aq[tr * LDK + s0 + ii], kt = s_k[tr * LDK + s0 + ii];
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int s = sg + e;
-            if (s <= tr) {
-                float bt = 0.f, tt = 0.f;
-                for (int ii = 0; ii < SLB; ++ii) {
-                    const float rt = __expf((float)(s_l[tr * LDS_ + ii] - s_l[s * LDS_ + ii]));
-                    const float x = s_p[s * LDS_ + ii] * rt;
-                    bt = fmaf(s_q[tr * LDS_ + ii], x, bt);
-                    tt = fmaf(s_k[tr * LDS_ + ii], x, tt);
-                }
-                accB[e] += bt;
-                accT[e] += s < tr ? tt : 0.f;
+            for (int e = 0; e < 8; ++e) {
+                const int s = cl + 8 * e;
+                const float rt = s <= tr ? __expf((float)(lt - s_l[s * LDL + ii])) : 0.f;
+                const float x = s_wp[s * LDK + s0 + ii] * rt;
+                accB[e] = fmaf(qt, x, accB[e]);
+                accT[e] = fmaf(kt, x, accT[e]);
             }
         }
         __syncthreads();
     }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-        const int s = sg + e;
+    for (int e = 0; e < 8; ++e) {
+        const int s = cl + 8 * e;
         Bm[tr * C + s] = s <= tr ? accB[e] : 0.f;
         s_T[tr * LDC + s] = s < tr ? accT[e] : 0.f;
     }
-    for (int e = tid; e < C * C; e += NTH) {
-        const int t = e / C, j = e % C;
-        s_A[t * LDC + j] = t == j ? 1.f : 0.f;
-    }
+    for (int e = tid; e < C * C; e += NTB) s_A[(e / C) * LDC + e % C] = 0.f;
     __syncthreads();
-    // ---- A = (I + T)^-1 by columns (forward substitution; thread j of wave 0: column j) -------
+
+    // ---- A = (I + T)^-1 by 16 x 16 blocks: the diagonal blocks by forward substitution
+    // (thread: one column of one block), then the blocks below the diagonal by distance,
+    // A_bc = -A_bb sum_{c <= m < b} T_bm A_mc ---------------------------------------------------
     if (tid < C) {
-        const int j = tid;
-        for (int t = 1; t < C; ++t) {
-            float acc = 0.f;
-            for (int s = 0; s < t; ++s) acc = fmaf(s_T[t * LDC + s], s_A[s * LDC + j], acc);
-            if (t > j) s_A[t * LDC + j] = -acc;
+        const int b = tid >> 4, j = tid & 15, o = 16 * b;
+        float y[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float acc = r == j ? 1.f : 0.f;
+#pragma unroll
+            for (int s = 0; s < r; ++s) acc = fmaf(-s_T[(o + r) * LDC + o + s], y[s], acc);
+            y[r] = r < j ? 0.f : acc;
         }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s_A[(o + r) * LDC + o + j] = y[r];
     }
     __syncthreads();
-    for (int e = tid; e < C * C; e += NTH) Am[e] = s_A[(e / C) * LDC + (e % C)];
+    for (int d = 1; d < 4; ++d) {
+        const int nb = 4 - d;
+        for (int e = tid; e < nb * 256; e += NTB) {  // X = sum_m T_bm A_mc
+            const int c = e >> 8, b = c + d, r = (e >> 4) & 15, j = e & 15;
+            float acc = 0.f;
+            for (int m = 16 * c; m < 16 * b; ++m)
+                acc = fmaf(s_T[(16 * b + r) * LDC + m], s_A[m * LDC + 16 * c + j], acc);
+            s_X[(c * 16 + r) * 17 + j] = acc;
+        }
+        __syncthreads();
+        for (int e = tid; e < nb * 256; e += NTB) {  // A_bc = -A_bb X
+            const int c = e >> 8, b = c + d, r = (e >> 4) & 15, j = e & 15;
+            float acc = 0.f;
+            for (int s = 0; s <= r; ++s)
+                acc = fmaf(s_A[(16 * b + r) * LDC + 16 * b + s], s_X[(c * 16 + s) * 17 + j], acc);
+            s_A[(16 * b + r) * LDC + 16 * c + j] = -acc;
+        }
+        __syncthreads();
+    }
+    for (int e = tid; e < C * C; e += NTB) Am[e] = s_A[(e / C) * LDC + (e % C)];
 }
 
 // ------------------------------------------------------------------------------------------
-// walks over the chunks of one (sequence, head, value tile)
+// walks over the chunks of one (sequence, head, value tile). Products are register-blocked:
+// a thread computes 2 x 4 (chunk rows x value columns) or 4 x 4 (key rows x value columns)
+// outputs from float4 reads of LDS rows padded to multiples of four floats.
 // ------------------------------------------------------------------------------------------
 template <int DK>
 struct WalkLds {
-    static constexpr int LDV = 33, LDK = DK + 1, LDC = C + 1;
+    static constexpr int LDV = 36, LDK = DK + 4, LDC = C + 4;
     static constexpr size_t OFF_S = 0;                                      // [DK][LDV]
     static constexpr size_t OFF_R1 = OFF_S + (size_t)DK * LDV * 4;          // [C][LDK]
     static constexpr size_t OFF_R2 = OFF_R1 + (size_t)C * LDK * 4;          // [C][LDK]
@@ -360,8 +390,38 @@ struct WalkLds {
     static constexpr size_t TOTAL = al16(OFF_GC + (size_t)DK * 4);
 };
 
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void fma4(float4& acc, float a, float4 b)
+{
+    acc.x = fmaf(a, b.x, acc.x);
+    acc.y = fmaf(a, b.y, acc.y);
+    acc.z = fmaf(a, b.z, acc.z);
+    acc.w = fmaf(a, b.w, acc.w);
+}
+
+// record operands [C][DK] (and [C][C]) from global memory into padded LDS rows
+template <int DK>
+__device__ __forceinline__ void stage_ck(float* dst, const float* __restrict__ src, int tid)
+    
+{
+    constexpr int LDK = WalkLds<DK>::LDK, Q = DK / 4;
+    for (int e = tid; e < C * Q; e += NTB) {
+        const int t = e / Q, i4 = e % Q;
+        st4(dst + t * LDK + 4 * i4, ld4(src + (size_t)t * DK + 4 * i4));
+    }
+}
+__device__ __forceinline__ void stage_cc(float* dst, const float* __restrict__ src, int tid)
+{
+    constexpr int LDC = C + 4;
+    for (int e = tid; e < C * C / 4; e += NTB) {
+        const int t = e / (C / 4), s4 = e % (C / 4);
+        st4(dst + t * LDC + 4 * s4, ld4(src + (size_t)t * C + 4 * s4));
+    }
+}
+
 template <class TI, int DK>
-__global__ __launch_bounds__(NTH) void bw_fwalk(Args a)
+__global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
@@ -375,15 +435,17 @@ __global__ __launch_bounds__(NTH) void bw_fwalk(Args a)
     float* s_D = (float*)(smem + LY::OFF_D);
     float* s_gc = (float*)(smem + LY::OFF_GC);
 
-    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV;
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJ = BV / 4;
     const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
     if (slot >= a.cm.N * H) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
     const int tid = threadIdx.x;
+    float* __restrict__ ckpt = a.ckpt;
+    float* __restrict__ dlt = a.dlt;
     int t0, t1, g0, nch;
     seq_span(a.cm, n, t0, t1);
     seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
-    for (int e = tid; e < DK * BV; e += NTH) {
+    for (int e = tid; e < DK * BV; e += NTB) {
         const int i = e / BV, j = e % BV;
         s_S[i * LDV + j] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
@@ -392,53 +454,74 @@ __global__ __launch_bounds__(NTH) void bw_fwalk(Args a)
         const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
         const size_t gh = (size_t)g * H + h;
         __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTH) {
+        for (int e = tid; e < DK * BV; e += NTB) {
             const int i = e / BV, j = e % BV;
-            a.ckpt[(gh * DK + i) * DV + j0 + j] = s_S[i * LDV + j];
+            ckpt[(gh * DK + i) * DV + j0 + j] = s_S[i * LDV + j];
         }
-        const float* kbar = (const float*)(rec + R::OFF_KBAR);
-        const float* ktl = (const float*)(rec + R::OFF_KTL);
-        const float* Am = (const float*)(rec + R::OFF_A);
-        const float* gC = (const float*)(rec + R::OFF_GC);
-        for (int e = tid; e < C * DK; e += NTH) {
-            const int t = e / DK, i = e % DK;
-            s_kb[t * LDK + i] = kbar[e];
-            s_kt[t * LDK + i] = ktl[e];
-        }
-        for (int e = tid; e < C * C; e += NTH) s_A[(e / C) * LDC + e % C] = Am[e];
-        for (int e = tid; e < DK; e += NTH) s_gc[e] = gC[e];
-        for (int e = tid; e < C * BV; e += NTH) {
+        stage_ck<DK>(s_kb, (const float*)(rec + R::OFF_KBAR), tid);
+        stage_ck<DK>(s_kt, (const float*)(rec + R::OFF_KTL), tid);
+        stage_cc(s_A, (const float*)(rec + R::OFF_A), tid);
+        for (int e = tid; e < DK; e += NTB) s_gc[e] = ((const float*)(rec + R::OFF_GC))[e];
+        for (int e = tid; e < C * BV; e += NTB) {
             const int t = e / BV, j = e % BV;
             s_X[t * LDV + j] =
                 t < L ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + j) : 0.f;
         }
         __syncthreads();
-        for (int e = tid; e < C * BV; e += NTH) {  // X = V - Kbar S_in
-            const int t = e / BV, j = e % BV;
-            float acc = s_X[t * LDV + j];
-            for (int i = 0; i < DK; ++i) acc = fmaf(-s_kb[t * LDK + i], s_S[i * LDV + j], acc);
-            s_X[t * LDV + j] = acc;
+        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // X = V - Kbar S_in
+            const int t = 2 * (e / NJ), j = 4 * (e % NJ);
+            float4 x0 = ld4(s_X + t * LDV + j), x1 = ld4(s_X + (t + 1) * LDV + j);
+            for (int i = 0; i < DK; ++i) {
+                const float4 sv = ld4(s_S + i * LDV + j);
+                fma4(x0, -s_kb[t * LDK + i], sv);
+                fma4(x1, -s_kb[(t + 1) * LDK + i], sv);
+            }
+            st4(s_X + t * LDV + j, x0);
+            st4(s_X + (t + 1) * LDV + j, x1);
         }
         __syncthreads();
-        for (int e = tid; e < C * BV; e += NTH) {  // Delta = A X
-            const int t = e / BV, j = e % BV;
-            float acc = 0.f;
-            for (int s = 0; s <= t; ++s) acc = fmaf(s_A[t * LDC + s], s_X[s * LDV + j], acc);
-            s_D[t * LDV + j] = acc;
-            a.dlt[(gh * C + t) * DV + j0 + j] = acc;
+        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // Delta = A X
+            const int t = 2 * (e / NJ), j = 4 * (e % NJ);
+            float4 d0 = make_float4(0.f, 0.f, 0.f, 0.f), d1 = d0;
+            for (int s2 = 0; s2 <= t + 1; ++s2) {
+                const float4 xv = ld4(s_X + s2 * LDV + j);
+                fma4(d0, s_A[t * LDC + s2], xv);
+                fma4(d1, s_A[(t + 1) * LDC + s2], xv);
+            }
+            st4(s_D + t * LDV + j, d0);
+            st4(s_D + (t + 1) * LDV + j, d1);
         }
         __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTH) {  // S_out = gamma_C S_in + Ktail^T Delta
-            const int i = e / BV, j = e % BV;
-            float acc = s_gc[i] * s_S[i * LDV + j];
-            for (int t = 0; t < C; ++t) acc = fmaf(s_kt[t * LDK + i], s_D[t * LDV + j], acc);
-            s_S[i * LDV + j] = acc;
+        for (int e = tid; e < C * BV; e += NTB) {
+            const int t = e / BV, j = e % BV;
+            dlt[(gh * C + t) * DV + j0 + j] = s_D[t * LDV + j];
+        }
+        for (int e = tid; e < (DK / 4) * NJ; e += NTB) {  // S_out = gamma_C S_in + Ktail^T Delta
+            const int i = 4 * (e / NJ), j = 4 * (e % NJ);
+            float4 r0 = ld4(s_S + i * LDV + j), r1 = ld4(s_S + (i + 1) * LDV + j);
+            float4 r2 = ld4(s_S + (i + 2) * LDV + j), r3 = ld4(s_S + (i + 3) * LDV + j);
+            const float4 gc = ld4(s_gc + i);
+            r0.x *= gc.x; r0.y *= gc.x; r0.z *= gc.x; r0.w *= gc.x;
+            r1.x *= gc.y; r1.y *= gc.y; r1.z *= gc.y; r1.w *= gc.y;
+            r2.x *= gc.z; r2.y *= gc.z; r2.z *= gc.z; r2.w *= gc.z;
+            r3.x *= gc.w; r3.y *= gc.w; r3.z *= gc.w; r3.w *= gc.w;
+            for (int t = 0; t < C; ++t) {
+                const float4 kt = ld4(s_kt + t * LDK + i), dv = ld4(s_D + t * LDV + j);
+                fma4(r0, kt.x, dv);
+                fma4(r1, kt.y, dv);
+                fma4(r2, kt.z, dv);
+                fma4(r3, kt.w, dv);
+            }
+            st4(s_S + i * LDV + j, r0);
+            st4(s_S + (i + 1) * LDV + j, r1);
+            st4(s_S + (i + 2) * LDV + j, r2);
+            st4(s_S + (i + 3) * LDV + j, r3);
         }
     }
 }
 
 template <class TI, int DK>
-__global__ __launch_bounds__(NTH) void bw_rwalk(Args a)
+__global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
@@ -454,15 +537,17 @@ __global__ __launch_bounds__(NTH) void bw_rwalk(Args a)
     float* s_P = (float*)(smem + LY::OFF_P);
     float* s_gc = (float*)(smem + LY::OFF_GC);
 
-    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV;
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJ = BV / 4;
     const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
     if (slot >= a.cm.N * H) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
     const int tid = threadIdx.x;
+    float* __restrict__ dso = a.dso;
+    float* __restrict__ gv = a.dv;
     int t0, t1, g0, nch;
     seq_span(a.cm, n, t0, t1);
     seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
-    for (int e = tid; e < DK * BV; e += NTH) {
+    for (int e = tid; e < DK * BV; e += NTB) {
         const int i = e / BV, j = e % BV;
         s_dS[i * LDV + j] = a.dS_T ? a.dS_T[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
@@ -471,63 +556,85 @@ __global__ __launch_bounds__(NTH) void bw_rwalk(Args a)
         const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
         const size_t gh = (size_t)g * H + h;
         __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTH) {
+        for (int e = tid; e < DK * BV; e += NTB) {
             const int i = e / BV, j = e % BV;
-            a.dso[(gh * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
+            dso[(gh * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
         }
-        const float* ktl = (const float*)(rec + R::OFF_KTL);
-        const float* Am = (const float*)(rec + R::OFF_A);
-        const float* Bm = (const float*)(rec + R::OFF_B);
-        const float* gC = (const float*)(rec + R::OFF_GC);
-        for (int e = tid; e < C * DK; e += NTH) s_r1[(e / DK) * LDK + e % DK] = ktl[e];
-        for (int e = tid; e < C * C; e += NTH) {
-            s_A[(e / C) * LDC + e % C] = Am[e];
-            s_B[(e / C) * LDC + e % C] = Bm[e];
-        }
-        for (int e = tid; e < DK; e += NTH) s_gc[e] = gC[e];
-        for (int e = tid; e < C * BV; e += NTH) {
+        stage_ck<DK>(s_r1, (const float*)(rec + R::OFF_KTL), tid);
+        stage_cc(s_A, (const float*)(rec + R::OFF_A), tid);
+        stage_cc(s_B, (const float*)(rec + R::OFF_B), tid);
+        for (int e = tid; e < DK; e += NTB) s_gc[e] = ((const float*)(rec + R::OFF_GC))[e];
+        for (int e = tid; e < C * BV; e += NTB) {
             const int t = e / BV, j = e % BV;
             s_O[t * LDV + j] = (t < L && a.dO)
                                    ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
                                    : 0.f;
         }
         __syncthreads();
-        for (int e = tid; e < C * BV; e += NTH) {  // dDelta = B^T (scale dO) + Ktail dS_out
-            const int s = e / BV, j = e % BV;
-            float acc = 0.f;
-            for (int t = s; t < C; ++t) acc = fmaf(s_B[t * LDC + s], s_O[t * LDV + j], acc);
-            for (int i = 0; i < DK; ++i) acc = fmaf(s_r1[s * LDK + i], s_dS[i * LDV + j], acc);
-            s_dD[s * LDV + j] = acc;
-        }
-        __syncthreads();
-        for (int e = tid; e < C * BV; e += NTH) {  // Psi = A^T dDelta = dV
-            const int s = e / BV, j = e % BV;
-            float acc = 0.f;
-            for (int t = s; t < C; ++t) acc = fmaf(s_A[t * LDC + s], s_dD[t * LDV + j], acc);
-            s_P[s * LDV + j] = acc;
-            if (s < L) a.dv[((size_t)(c0 + s) * H + h) * DV + j0 + j] = acc;
-        }
-        __syncthreads();
-        const float* qbar = (const float*)(rec + R::OFF_QBAR);
-        const float* kbar = (const float*)(rec + R::OFF_KBAR);
-        for (int e = tid; e < C * DK; e += NTH) {
-            s_r1[(e / DK) * LDK + e % DK] = qbar[e];
-            s_r2[(e / DK) * LDK + e % DK] = kbar[e];
-        }
-        __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTH) {  // dS_in
-            const int i = e / BV, j = e % BV;
-            float acc = s_gc[i] * s_dS[i * LDV + j];
-            for (int t = 0; t < C; ++t) {
-                acc = fmaf(s_r1[t * LDK + i], s_O[t * LDV + j], acc);
-                acc = fmaf(-s_r2[t * LDK + i], s_P[t * LDV + j], acc);
+        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // dDelta = B^T (scale dO) + Ktail dS_out
+            const int s2 = 2 * (e / NJ), j = 4 * (e % NJ);
+            float4 d0 = make_float4(0.f, 0.f, 0.f, 0.f), d1 = d0;
+            for (int t = s2; t < C; ++t) {
+                const float4 ov = ld4(s_O + t * LDV + j);
+                const float2 bb = *reinterpret_cast<const float2*>(s_B + t * LDC + s2);
+                fma4(d0, bb.x, ov);
+                fma4(d1, bb.y, ov);
             }
-            s_dS[i * LDV + j] = acc;
+            for (int i = 0; i < DK; ++i) {
+                const float4 sv = ld4(s_dS + i * LDV + j);
+                fma4(d0, s_r1[s2 * LDK + i], sv);
+                fma4(d1, s_r1[(s2 + 1) * LDK + i], sv);
+            }
+            st4(s_dD + s2 * LDV + j, d0);
+            st4(s_dD + (s2 + 1) * LDV + j, d1);
+        }
+        __syncthreads();
+        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // Psi = A^T dDelta = dV
+            const int s2 = 2 * (e / NJ), j = 4 * (e % NJ);
+            float4 p0 = make_float4(0.f, 0.f, 0.f, 0.f), p1 = p0;
+            for (int t = s2; t < C; ++t) {
+                const float4 dv = ld4(s_dD + t * LDV + j);
+                const float2 aa = *reinterpret_cast<const float2*>(s_A + t * LDC + s2);
+                fma4(p0, aa.x, dv);
+                fma4(p1, aa.y, dv);
+            }
+            st4(s_P + s2 * LDV + j, p0);
+            st4(s_P + (s2 + 1) * LDV + j, p1);
+        }
+        __syncthreads();
+        for (int e = tid; e < C * BV; e += NTB) {
+            const int t = e / BV, j = e % BV;
+            if (t < L) gv[((size_t)(c0 + t) * H + h) * DV + j0 + j] = s_P[t * LDV + j];
+        }
+        stage_ck<DK>(s_r1, (const float*)(rec + R::OFF_QBAR), tid);
+        stage_ck<DK>(s_r2, (const float*)(rec + R::OFF_KBAR), tid);
+        __syncthreads();
+        for (int e = tid; e < (DK / 4) * NJ; e += NTB) {  // dS_in
+            const int i = 4 * (e / NJ), j = 4 * (e % NJ);
+            float4 r0 = ld4(s_dS + i * LDV + j), r1 = ld4(s_dS + (i + 1) * LDV + j);
+            float4 r2 = ld4(s_dS + (i + 2) * LDV + j), r3 = ld4(s_dS + (i + 3) * LDV + j);
+            const float4 gc = ld4(s_gc + i);
+            r0.x *= gc.x; r0.y *= gc.x; r0.z *= gc.x; r0.w *= gc.x;
+            r1.x *= gc.y; r1.y *= gc.y; r1.z *= gc.y; r1.w *= gc.y;
+            r2.x *= gc.z; r2.y *= gc.z; r2.z *= gc.z; r2.w *= gc.z;
+            r3.x *= gc.w; r3.y *= gc.w; r3.z *= gc.w; r3.w *= gc.w;
+            for (int t = 0; t < C; ++t) {
+                const float4 qb = ld4(s_r1 + t * LDK + i), kb = ld4(s_r2 + t * LDK + i);
+                const float4 ov = ld4(s_O + t * LDV + j), pv = ld4(s_P + t * LDV + j);
+                fma4(r0, qb.x, ov); fma4(r0, -kb.x, pv);
+                fma4(r1, qb.y, ov); fma4(r1, -kb.y, pv);
+                fma4(r2, qb.z, ov); fma4(r2, -kb.z, pv);
+                fma4(r3, qb.w, ov); fma4(r3, -kb.w, pv);
+            }
+            st4(s_dS + i * LDV + j, r0);
+            st4(s_dS + (i + 1) * LDV + j, r1);
+            st4(s_dS + (i + 2) * LDV + j, r2);
+            st4(s_dS + (i + 3) * LDV + j, r3);
         }
     }
     __syncthreads();
     if (a.dS0)
-        for (int e = tid; e < DK * BV; e += NTH) {
+        for (int e = tid; e < DK * BV; e += NTB) {
             const int i = e / BV, j = e % BV;
             a.dS0[((size_t)slot * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
         }
@@ -552,18 +659,19 @@ struct GradLds {
     static constexpr size_t W_L = al16(W_KP + (size_t)C * LDS_ * 4);
     static constexpr size_t W2 = W_L + (size_t)C * LDS_ * 8;
     static constexpr size_t OFF_C = OFF_W + al16(cmax(W1, W2));              // [C][LDZ]
-    static constexpr size_t OFF_P6 = OFF_C + (size_t)C * LDZ * 4;            // [DK]
+    static constexpr size_t OFF_DL = OFF_C + (size_t)C * LDZ * 4;            // dlambda [C][LDZ]
+    static constexpr size_t OFF_P6 = OFF_DL + (size_t)C * LDZ * 4;           // [DK]
     static constexpr size_t TOTAL = al16(OFF_P6 + (size_t)DK * 4);
 };
 
 template <class TI, int DK, int VARIANT, bool APC>
-__global__ __launch_bounds__(NTH) void bw_grad(Args a)
+__global__ __launch_bounds__(NTB) void bw_grad(Args a)
 {
     using R = BwRec<DK>;
     using LY = GradLds<DK>;
     constexpr bool DIAG = VARIANT == 0;
     constexpr int SLB = LY::SLB, LDV = LY::LDV, LDC = LY::LDC, LDZ = LY::LDZ, LDS_ = LY::LDS_;
-    constexpr int Q = DK / 4;  // channels per thread in the dk-wide products
+    constexpr int Q = DK / 8;  // channels per thread in the dk-wide products
     constexpr int NCHAN = DIAG ? DK : 1;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_dB = (float*)(smem + LY::OFF_DB);
@@ -579,6 +687,7 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
     float* s_kp = (float*)(wr + LY::W_KP);
     double* s_l = (double*)(wr + LY::W_L);
     float* s_c = (float*)(smem + LY::OFF_C);
+    float* s_dl = (float*)(smem + LY::OFF_DL);
     float* s_p6 = (float*)(smem + LY::OFF_P6);
 
     const int H = a.H, DV = a.DV;
@@ -590,37 +699,40 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const size_t gh = (size_t)g * H + h;
     const char* rec = a.rec + gh * R::BYTES;
-    const float* kap = (const float*)(rec + R::OFF_KAP);
-    const float* phat = (const float*)(rec + R::OFF_PHAT);
-    const double* lam = (const double*)(rec + R::OFF_LAM);
-    const float* gC = (const float*)(rec + R::OFF_GC);
-    const float* den = (const float*)(rec + R::OFF_DEN);
-    float* dkap = a.dkap + gh * C * DK;
-    float* dlam = a.dlam + gh * C * DK;
-    float* dal = a.dal + gh * C * DK;
+    const float* __restrict__ kap = (const float*)(rec + R::OFF_KAP);
+    const float* __restrict__ phat = (const float*)(rec + R::OFF_PHAT);
+    const double* __restrict__ lam = (const double*)(rec + R::OFF_LAM);
+    const float* __restrict__ gC = (const float*)(rec + R::OFF_GC);
+    const float* __restrict__ den = (const float*)(rec + R::OFF_DEN);
+    float* __restrict__ dkap = a.dkap + gh * C * DK;
+    float* __restrict__ dal = a.dal + gh * C * DK;
+    float* __restrict__ gq = a.dq;
+    float* __restrict__ gk = a.dk;
     auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
 
     // ---- products over the value columns, by slabs of 32 columns ---------------------------
     //   P1 = dO Delta^T, P2 = Psi Delta^T (thread: row t, 16 columns s)
     //   P3 = Psi S_in^T, P4 = dO S_in^T, P5 = Delta dS_out^T (thread: row t, Q channels)
     //   P6_i = sum_j S_in,ij dS_out,ij
-    const int tr = tid >> 2, sg = (tid & 3) * 16, qd = (tid & 3) * Q;
-    float p1[16], p2[16], p3[Q], p4[Q], p5[Q], p6 = 0.f;
+    // lanes 8 r + c: row r; columns s = c + 8 e and channels i = c + 8 e (interleaved, so that
+    // the eight lanes of a row read eight consecutive LDS rows: no bank conflicts)
+    const int tr = tid >> 3, cl = tid & 7;
+    float p1[8], p2[8], p3[Q], p4[Q], p5[Q], p6 = 0.f;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) p1[e] = p2[e] = 0.f;
+    for (int e = 0; e < 8; ++e) p1[e] = p2[e] = 0.f;
 #pragma unroll
     for (int e = 0; e < Q; ++e) p3[e] = p4[e] = p5[e] = 0.f;
     for (int j0 = 0; j0 < DV; j0 += 32) {
         const int SW = min(32, DV - j0);
         __syncthreads();
-        for (int e = tid; e < C * SW; e += NTH) {
+        for (int e = tid; e < C * SW; e += NTB) {
             const int t = e / SW, j = e % SW;
             const bool ok = t < L;
             s_D[t * LDV + j] = a.dlt[(gh * C + t) * DV + j0 + j];
             s_P[t * LDV + j] = ok ? a.dv[row(t) * DV + j0 + j] : 0.f;
             s_O[t * LDV + j] = (ok && a.dO) ? ld<TI>(a.dO, row(t) * DV + j0 + j) : 0.f;
         }
-        for (int e = tid; e < DK * SW; e += NTH) {
+        for (int e = tid; e < DK * SW; e += NTB) {
             const int i = e / SW, j = e % SW;
             s_S[i * LDV + j] = a.ckpt[(gh * DK + i) * DV + j0 + j];
             s_G[i * LDV + j] = a.dso[(gh * DK + i) * DV + j0 + j];
@@ -629,25 +741,25 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
         for (int j = 0; j < SW; ++j) {
             const float ot = s_O[tr * LDV + j], pt = s_P[tr * LDV + j], dt = s_D[tr * LDV + j];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float ds = s_D[(sg + e) * LDV + j];
+            for (int e = 0; e < 8; ++e) {
+                const float ds = s_D[(cl + 8 * e) * LDV + j];
                 p1[e] = fmaf(ot, ds, p1[e]);
                 p2[e] = fmaf(pt, ds, p2[e]);
             }
 #pragma unroll
             for (int e = 0; e < Q; ++e) {
-                const float si = s_S[(qd + e) * LDV + j];
+                const float si = s_S[(cl + 8 * e) * LDV + j];
                 p3[e] = fmaf(pt, si, p3[e]);
                 p4[e] = fmaf(ot, si, p4[e]);
-                p5[e] = fmaf(dt, s_G[(qd + e) * LDV + j], p5[e]);
+                p5[e] = fmaf(dt, s_G[(cl + 8 * e) * LDV + j], p5[e]);
             }
         }
         if (tid < DK)
             for (int j = 0; j < SW; ++j) p6 = fmaf(s_S[tid * LDV + j], s_G[tid * LDV + j], p6);
     }
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-        const int s = sg + e;
+    for (int e = 0; e < 8; ++e) {
+        const int s = cl + 8 * e;
         s_dB[tr * LDC + s] = s <= tr ? a.scale * p1[e] : 0.f;  // dB = scale dO Delta^T
         s_dT[tr * LDC + s] = s < tr ? -p2[e] : 0.f;             // dT = -Psi Delta^T
     }
@@ -655,7 +767,7 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
     // terms through S_in and the tail operand (each entry owned by this thread)
 #pragma unroll
     for (int e = 0; e < Q; ++e) {
-        const int i = qd + e, t = tr;
+        const int i = cl + 8 * e, t = tr;
         const double lm = lam[t * DK + i], lmC = lam[(C - 1) * DK + i];
         const float gm = expf((float)lm), et = expf((float)(lmC - lm));
         const bool ok = t < L;
@@ -666,20 +778,19 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
         const float dk = -gm * p3[e];           // X = V - Kbar S_in
         const float dkp = et * p5[e];           // S_out = ... + Ktail^T Delta
         if (ok) {
-            a.dq[row(t) * DK + i] = dq;
-            a.dk[row(t) * DK + i] = dk;
+            gq[row(t) * DK + i] = dq;
+            gk[row(t) * DK + i] = dk;
         }
         dkap[t * DK + i] = dkp;
-        dlam[t * DK + i] = qq * dq + kk * dk - kp * dkp;
+        s_dl[t * LDZ + i] = qq * dq + kk * dk - kp * dkp;
         s_c[t * LDZ + i] = kp * dkp;
     }
     __syncthreads();
 
     // ---- terms through T and B (decay ratios from the log-decays), by channel slabs ---------
-    constexpr int EPT = SLB / 4;  // channels per thread in a slab
-    const int ce = (tid & 3) * EPT;
+    constexpr int EPT = SLB / 8;  // channels per thread in a slab: ii = cl + 8 e
     for (int s0 = 0; s0 < DK; s0 += SLB) {
-        for (int e = tid; e < C * SLB; e += NTH) {
+        for (int e = tid; e < C * SLB; e += NTB) {
             const int t = e / SLB, ii = e % SLB, i = s0 + ii;
             const bool ok = t < L;
             s_q[t * LDS_ + ii] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
@@ -696,7 +807,7 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
             const float b = s_dB[tr * LDC + s], tt = s_dT[tr * LDC + s];
 #pragma unroll
             for (int e = 0; e < EPT; ++e) {
-                const int ii = ce + e;
+                const int ii = cl + 8 * e;
                 const float rt = __expf((float)(s_l[tr * LDS_ + ii] - s_l[s * LDS_ + ii]));
                 const float x = s_kp[s * LDS_ + ii] * rt;
                 dqB[e] = fmaf(b, x, dqB[e]);
@@ -708,7 +819,7 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
             const float b = s_dB[t * LDC + tr], tt = s_dT[t * LDC + tr];
 #pragma unroll
             for (int e = 0; e < EPT; ++e) {
-                const int ii = ce + e;
+                const int ii = cl + 8 * e;
                 const float rt = __expf((float)(s_l[t * LDS_ + ii] - s_l[tr * LDS_ + ii]));
                 dkpB[e] = fmaf(b, s_q[t * LDS_ + ii] * rt, dkpB[e]);
                 dkpT[e] = fmaf(tt, s_k[t * LDS_ + ii] * rt, dkpT[e]);
@@ -716,36 +827,41 @@ __global__ __launch_bounds__(NTH) void bw_grad(Args a)
         }
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
-            const int ii = ce + e, i = s0 + ii, t = tr;
+            const int ii = cl + 8 * e, i = s0 + ii, t = tr;
             const float dkp = dkpB[e] + dkpT[e];
             if (t < L) {
-                a.dq[row(t) * DK + i] += dqB[e];
-                a.dk[row(t) * DK + i] += dkT[e];
+                gq[row(t) * DK + i] += dqB[e];
+                gk[row(t) * DK + i] += dkT[e];
             }
             dkap[t * DK + i] += dkp;
-            dlam[t * DK + i] += s_q[t * LDS_ + ii] * dqB[e] + s_k[t * LDS_ + ii] * dkT[e] -
-                                s_kp[t * LDS_ + ii] * dkp;
+            s_dl[t * LDZ + i] += s_q[t * LDS_ + ii] * dqB[e] + s_k[t * LDS_ + ii] * dkT[e] -
+                                 s_kp[t * LDS_ + ii] * dkp;
         }
         __syncthreads();
     }
 
     // ---- d(log-decay) -> dalpha (memory part): alpha_s dalpha_s = sum_{t >= s} dlambda_t, the
     // chunk-end terms (gamma_C) entering at the last token ---------------------------------------
-    if (tid < DK) {
+    if (tid < DK) {  // suffix sums over the chunk, in LDS
         const int i = tid;
         float acc = gC[i] * s_p6[i];
         for (int t = 0; t < C; ++t) acc += s_c[t * LDZ + i];
         for (int t = C - 1; t >= 0; --t) {
-            acc += dlam[t * DK + i];
-            float al = 1.f;
-            if (t < L) al = APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
-            dal[t * DK + i] = t < L ? acc / al : 0.f;
+            acc += s_dl[t * LDZ + i];
+            s_dl[t * LDZ + i] = acc;
         }
+    }
+    __syncthreads();
+    for (int e = tid; e < C * DK; e += NTB) {
+        const int t = e / DK, i = e % DK;
+        float al = 1.f;
+        if (t < L) al = APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
+        dal[e] = t < L ? s_dl[t * LDZ + i] / al : 0.f;
     }
 
     // ---- coefficients of the variance adjoint: lambda_{t-1} = A_t lambda_t + B_t ------------
-    for (int j = 0; j < C / 4; ++j) {
-        const int t = (C / 4) * w + j;
+    for (int j = 0; j < C / NWB; ++j) {
+        const int t = (C / NWB) * w + j;
         const bool ok = t < L;
         const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
         const float dn = den[t];
@@ -983,7 +1099,6 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
     a.dlt = (float*)(ws + m.dlt);
     a.dso = (float*)(ws + m.dso);
     a.dkap = (float*)(ws + m.dkap);
-    a.dlam = (float*)(ws + m.dlam);
     a.dal = (float*)(ws + m.dal);
     a.acf = (float*)(ws + m.acf);
     a.bcf = (float*)(ws + m.bcf);
@@ -999,18 +1114,18 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
         attr = true;
     }
     if (m.maxch > 0) {
-        hipLaunchKernelGGL((bw_prep<TI, DK, VARIANT, APC>), cgrid, dim3(NTH), PrepLds<DK>::TOTAL,
+        hipLaunchKernelGGL((bw_prep<TI, DK, VARIANT, APC>), cgrid, dim3(NTB), PrepLds<DK>::TOTAL,
                            st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const int NV = bc.dv / a.BV;
     const dim3 wgrid((unsigned)((size_t)sa.N * sa.H * NV));
-    hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTH), WalkLds<DK>::TOTAL, st, a);
+    hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::TOTAL, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTH), WalkLds<DK>::TOTAL, st, a);
+    hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::TOTAL, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (m.maxch > 0) {
-        hipLaunchKernelGGL((bw_grad<TI, DK, VARIANT, APC>), cgrid, dim3(NTH), GradLds<DK>::TOTAL,
+        hipLaunchKernelGGL((bw_grad<TI, DK, VARIANT, APC>), cgrid, dim3(NTB), GradLds<DK>::TOTAL,
                            st, a);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
