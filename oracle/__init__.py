@@ -55,6 +55,8 @@ def _load():
     for name in ("oracle_mobius_fold", "oracle_mobius_tree"):
         getattr(lib, name).argtypes = [d, d, d, cd, ctypes.c_int64, ci, d, d]
     lib.oracle_mobius_chunked.argtypes = [d, d, d, cd, ctypes.c_int64, ctypes.c_int64, ci, d, d]
+    lib.oracle_kdn_forward_kam.argtypes = [d] * 11 + [i32p] + [ci] * 6 + [cd, ci]
+    lib.oracle_kdn_forward_kam.restype = ci
     lib.oracle_kdn_backward.argtypes = ([ci] + [d] * 8 + [i32p] + [ci] * 7 + [cd, cd] +
                                         [d] * 13 + [ci])
     for name in ("oracle_kdn_forward_diag", "oracle_kdn_forward_iso", "oracle_kdn_decode_step",
@@ -160,6 +162,26 @@ def decode_step(variant, q, k, v, alpha, omega, r, S, P, slot_idx=None, mu=None,
     if rc != 0:
         raise ValueError("oracle_kdn_decode_step rejected its arguments")
     return o
+
+
+def forward_kam(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, scale=None,
+                nthreads=0):
+    """Kalman Associative Memory (the exact filter, dense dk x dk covariance per head): returns
+    o, S_T and P_T [N,H,dk,dk]. P0 [N,H,dk,dk] (None = identity); alpha, omega [B,T,H,dk]."""
+    q, k, v, alpha, omega, r, S0, P0 = map(_f64, (q, k, v, alpha, omega, r, S0, P0))
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    cu = None if cu_seqlens is None else np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    N = B if cu is None else len(cu) - 1
+    scale = float(dk ** -0.5 if scale is None else scale)
+    out = dict(o=np.zeros((B, T, H, dv)), S_T=np.zeros((N, H, dk, dv)),
+               P_T=np.zeros((N, H, dk, dk)))
+    rc = _load().oracle_kdn_forward_kam(
+        _p(q), _p(k), _p(v), _p(alpha), _p(omega), _p(r), _p(S0), _p(P0), _p(out["o"]),
+        _p(out["S_T"]), _p(out["P_T"]), _pi(cu), N, B, T, H, dk, dv, scale, nthreads)
+    if rc != 0:
+        raise ValueError("oracle_kdn_forward_kam rejected its arguments")
+    return out
 
 
 def backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,

@@ -456,3 +456,93 @@ int oracle_mobius_chunked(const double* a, const double* w, const double* u, dou
     free(zin);
     return 0;
 }
+
+/* ------------------------------------------------------------------------------------------ */
+/* Kalman Associative Memory: the exact filter with a dense dk x dk covariance per (sequence,  */
+/* head) (Prop. "Kalman Associative Memory", eq. kalman-optimal-update-box), with the          */
+/* transition D = diag(alpha) and process noise Omega = diag(omega) of the KDN inputs:         */
+/*   P_hat = D P D^T + Omega;  kappa = P_hat k / (r + k^T P_hat k)                            */
+/*   S = D S + kappa (v - (D S)^T k)^T;  P = (I - kappa k^T) P_hat;  o = scale S^T q          */
+/* P0 [N,H,dk,dk] (NULL = identity), P_T [N,H,dk,dk]; other arguments as the diagonal forward. */
+/* ------------------------------------------------------------------------------------------ */
+int oracle_kdn_forward_kam(const double* q, const double* k, const double* v, const double* alpha,
+                           const double* omega, const double* r, const double* S0,
+                           const double* P0, double* o, double* S_T, double* P_T,
+                           const int32_t* cu_seqlens, int N, int B, int T, int H, int dk, int dv,
+                           double scale, int nthreads)
+{
+    if (check_dims(N, B, T, H, dk, dv, cu_seqlens)) return -1;
+    for (int n = 0; n < N; ++n) {
+        seq_span s;
+        if (span_of(cu_seqlens, n, T, &s)) return -1;
+    }
+    set_threads(nthreads);
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+    for (int nh = 0; nh < N * H; ++nh) {
+        const int n = nh / H, h = nh % H;
+        seq_span s;
+        span_of(cu_seqlens, n, T, &s);
+        const size_t SZ = (size_t)dk * dv, PZ = (size_t)dk * dk;
+        double* S = malloc(sizeof(double) * SZ);
+        double* P = malloc(sizeof(double) * PZ);
+        double* Pk = malloc(sizeof(double) * dk);   /* P_hat k            */
+        double* kP = malloc(sizeof(double) * dk);   /* k^T P_hat          */
+        double* del = malloc(sizeof(double) * dv);  /* v - S_hat^T k      */
+        if (!S || !P || !Pk || !kP || !del) {
+            bad |= 1;
+        } else {
+            for (size_t e = 0; e < SZ; ++e) S[e] = S0 ? S0[(size_t)nh * SZ + e] : 0.0;
+            for (int i = 0; i < dk; ++i)
+                for (int j = 0; j < dk; ++j)
+                    P[i * dk + j] = P0 ? P0[(size_t)nh * PZ + (size_t)i * dk + j] : (i == j);
+            for (int t = 0; t < s.len; ++t) {
+                const int64_t row = ((int64_t)(s.t0 + t)) * H + h;
+                const double *qt = q + row * dk, *kt = k + row * dk, *vt = v + row * dv;
+                const double *at = alpha + row * dk, *wt = omega + row * dk;
+                /* predict: P_hat = D P D + Omega, S_hat = D S */
+                for (int i = 0; i < dk; ++i)
+                    for (int j = 0; j < dk; ++j)
+                        P[i * dk + j] = at[i] * P[i * dk + j] * at[j] + (i == j ? wt[i] : 0.0);
+                for (int i = 0; i < dk; ++i)
+                    for (int j = 0; j < dv; ++j) S[i * dv + j] *= at[i];
+                /* kappa = P_hat k / c with c = r + k^T P_hat k */
+                for (int i = 0; i < dk; ++i) {
+                    double acc = 0.0, acc2 = 0.0;
+                    for (int j = 0; j < dk; ++j) {
+                        acc += P[i * dk + j] * kt[j];
+                        acc2 += kt[j] * P[j * dk + i];
+                    }
+                    Pk[i] = acc;
+                    kP[i] = acc2;
+                }
+                double c = r[row];
+                for (int i = 0; i < dk; ++i) c += kt[i] * Pk[i];
+                /* S = S_hat + kappa (v - S_hat^T k)^T */
+                for (int j = 0; j < dv; ++j) {
+                    double acc = 0.0;
+                    for (int i = 0; i < dk; ++i) acc += S[i * dv + j] * kt[i];
+                    del[j] = vt[j] - acc;
+                }
+                for (int i = 0; i < dk; ++i)
+                    for (int j = 0; j < dv; ++j) S[i * dv + j] += Pk[i] / c * del[j];
+                /* P = (I - kappa k^T) P_hat = P_hat - kappa (k^T P_hat) */
+                for (int i = 0; i < dk; ++i)
+                    for (int j = 0; j < dk; ++j) P[i * dk + j] -= Pk[i] / c * kP[j];
+                /* o = scale S^T q (read after the write) */
+                if (o) {
+                    for (int j = 0; j < dv; ++j) {
+                        double acc = 0.0;
+                        for (int i = 0; i < dk; ++i) acc += S[i * dv + j] * qt[i];
+                        o[row * dv + j] = scale * acc;
+                    }
+                }
+            }
+            for (size_t e = 0; e < SZ; ++e) S_T[(size_t)nh * SZ + e] = S[e];
+            if (P_T)
+                for (size_t e = 0; e < PZ; ++e) P_T[(size_t)nh * PZ + e] = P[e];
+        }
+        free(S); free(P); free(Pk); free(kP); free(del);
+    }
+    return bad ? -2 : 0;
+}
