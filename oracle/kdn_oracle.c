@@ -497,7 +497,7 @@ int oracle_kdn_forward_kam(const double* q, const double* k, const double* v, co
                 for (int j = 0; j < dk; ++j)
                     P[i * dk + j] = P0 ? P0[(size_t)nh * PZ + (size_t)i * dk + j] : (i == j);
             for (int t = 0; t < s.len; ++t) {
-                const int64_t row = ((int64_t)(s.t0 + t)) * H + h;
+                const int64_t row = ((int64_t)s.b * T + s.t0 + t) * H + h;
                 const double *qt = q + row * dk, *kt = k + row * dk, *vt = v + row * dv;
                 const double *at = alpha + row * dk, *wt = omega + row * dk;
                 /* predict: P_hat = D P D + Omega, S_hat = D S */

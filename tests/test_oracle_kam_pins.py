@@ -84,3 +84,20 @@ def test_kam_covariance_symmetric_positive_and_packed_batches_separate():
             np.testing.assert_array_equal(out["o"][:, t0:t1], one["o"])
             np.testing.assert_array_equal(out["P_T"][n], one["P_T"][0])
     np.testing.assert_array_equal(out["P_T"][1], np.broadcast_to(np.eye(dk), (H, dk, dk)))
+
+
+def test_kam_batch_rows_and_heads_are_independent_chains():
+    """A fixed-length batch of two rows equals the two rows run alone (the row offset of every
+    token); heads likewise."""
+    g = np.random.default_rng(53)
+    B, T, H, dk, dv = 2, 7, 2, 3, 2
+    x = [g.standard_normal((B, T, H, dk)), g.standard_normal((B, T, H, dk)),
+         g.standard_normal((B, T, H, dv)), g.uniform(0.4, 1.0, (B, T, H, dk)),
+         g.uniform(0.01, 0.3, (B, T, H, dk)), g.uniform(0.2, 1.0, (B, T, H))]
+    both = oracle.forward_kam(*x)
+    for b in range(B):
+        for h in range(H):
+            one = oracle.forward_kam(*[a[b:b + 1, :, h:h + 1] for a in x])
+            np.testing.assert_array_equal(both["o"][b:b + 1, :, h:h + 1], one["o"])
+            np.testing.assert_array_equal(both["S_T"][b, h], one["S_T"][0, 0])
+            np.testing.assert_array_equal(both["P_T"][b, h], one["P_T"][0, 0])
