@@ -285,6 +285,26 @@ kdn_status_t kdn_backward(int32_t variant, const void* q, const void* k, const v
 size_t kdn_backward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
                                     int32_t dk, int32_t dv, int32_t packed);
 
+/*
+ * Kalman Associative Memory: the exact Kalman filter of the memory with a dense dk x dk
+ * covariance per (sequence, head) (Prop. "Kalman Associative Memory", eq.
+ * kalman-optimal-update-box), the model the diagonal and isotropic variants approximate, as a
+ * reference for small heads (its state and work per token grow as dk^2):
+ *   P_hat = diag(alpha) P diag(alpha) + diag(omega);  kappa = P_hat k / (r + k^T P_hat k)
+ *   S = diag(alpha) S + kappa (v - (diag(alpha) S)^T k)^T;  P = (I - kappa k^T) P_hat
+ *   o = scale * S^T q
+ *   q, k, alpha, omega: [B,T,H,dk]; v, o: [B,T,H,dv]; r: [B,T,H] (dtype); packing as the
+ *   forward. S0, S_T: [N,H,dk,dv]; P0, P_T: [N,H,dk,dk] float32 (P0 NULL = identity, S0 NULL =
+ *   0; S_T, P_T NULL = not written; S_T / P_T may alias S0 / P0 exactly). No information scale
+ *   (the exact filter has none) and no workspace. One workgroup walks each (sequence, head)
+ *   token by token: intended for checking and analysis, not for long sequences at dk = 128.
+ */
+kdn_status_t kdn_forward_kam(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* omega, const void* r, const float* S0, const float* P0,
+                             void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                             int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, float scale, void* stream);
+
 /* Static text for a status code.                                                             */
 const char* kdn_status_string(kdn_status_t status);
 

@@ -393,6 +393,42 @@ kdn_status_t kdn_decode_step_layer(int32_t variant, const void* q, const void* k
                          dk, dv, dtype, alpha_per_channel, mu, scale, opts, stream);
 }
 
+kdn_status_t kdn_forward_kam(const void* q, const void* k, const void* v, const void* alpha,
+                             const void* omega, const void* r, const float* S0, const float* P0,
+                             void* o, float* S_T, float* P_T, const int32_t* cu_seqlens,
+                             int32_t N, int32_t B, int32_t T, int32_t H, int32_t dk, int32_t dv,
+                             kdn_dtype_t dtype, float scale, void* stream)
+{
+    if (!q || !k || !v || !alpha || !omega || !r || !o)
+        return fail(KDN_ERR_INVALID_ARG, "null required pointer (q, k, v, alpha, omega, r, o)");
+    if (dtype != KDN_F32 && dtype != KDN_BF16)
+        return fail(KDN_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    kdn_status_t st = check_seq(cu_seqlens, N, B, T, H);
+    if (st != KDN_OK) return st;
+    if (!head_ok(dk) || !head_ok(dv))
+        return fail(KDN_ERR_UNSUPPORTED, "dk=%d dv=%d: head sizes must be 16, 32, 64 or 128", dk,
+                    dv);
+    if (!(scale > 0.f)) return fail(KDN_ERR_INVALID_ARG, "scale must be positive (%g)", scale);
+    const size_t rows = (size_t)B * T * H, es = esize(dtype);
+    const size_t nk = rows * dk * es, nv = rows * dv * es;
+    const void* ins[6] = {q, k, v, alpha, omega, r};
+    const size_t insz[6] = {nk, nk, nv, nk, nk, rows * es};
+    for (int i = 0; i < 6; ++i)
+        if (overlaps(o, nv, ins[i], insz[i]))
+            return fail(KDN_ERR_INVALID_ARG, "output o overlaps input %d", i);
+    const size_t ns = (size_t)N * H * dk * dv * 4, np = (size_t)N * H * dk * dk * 4;
+    if (S_T && S_T != S0 && overlaps(S_T, ns, S0, ns))
+        return fail(KDN_ERR_INVALID_ARG, "S_T partially overlaps S0");
+    if (P_T && P_T != P0 && overlaps(P_T, np, P0, np))
+        return fail(KDN_ERR_INVALID_ARG, "P_T partially overlaps P0");
+    if (overlaps(o, nv, S_T, ns) || overlaps(o, nv, P_T, np) || overlaps(S_T, ns, P_T, np))
+        return fail(KDN_ERR_INVALID_ARG, "o, S_T and P_T must not overlap");
+    kdn::SeqArgs sa = {cu_seqlens, N, B, T, H};
+    return hip_status(kdn::launch_kam(q, k, v, alpha, omega, r, S0, P0, o, S_T, P_T, sa, dk, dv,
+                                      dtype, scale, (hipStream_t)stream),
+                      "kdn_forward_kam launch");
+}
+
 size_t kdn_backward_workspace_bytes(int32_t variant, int32_t N, int32_t B, int32_t T, int32_t H,
                                     int32_t dk, int32_t dv, int32_t packed)
 {

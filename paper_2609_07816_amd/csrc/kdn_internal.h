@@ -144,6 +144,12 @@ size_t backward_workspace_bytes(int variant, bool packed, int N, int B, int T, i
                                 int dv);
 hipError_t launch_backward(const BwdCall& bc, hipStream_t stream);
 
+// Kalman Associative Memory, dense covariance (kdn_kam.hip).
+hipError_t launch_kam(const void* q, const void* k, const void* v, const void* alpha,
+                      const void* omega, const void* r, const float* S0, const float* P0,
+                      void* o, float* S_T, float* P_T, const SeqArgs& sa, int dk, int dv,
+                      kdn_dtype_t dtype, float scale, hipStream_t stream);
+
 bool chunked_supported(int chunk);
 size_t chunked_workspace_bytes(int variant, bool packed, int N, int B, int T, int H, int dk,
                                kdn_dtype_t dtype);

@@ -20,6 +20,8 @@ Functions mirror the C entry points:
   mu_t=None, beta_eff=None) -> o``
 * ``backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, mu=None,
   scale=None, dO=None, dS_T=None, dP_T=None) -> dict`` of float32 gradients
+* ``forward_kam(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, scale=None)
+  -> (o, S_T, P_T)`` -- the dense-covariance Kalman Associative Memory
 """
 
 from __future__ import annotations
@@ -88,6 +90,8 @@ def lib():
                                          vp])
     L.kdn_backward.argtypes = ([i32] + [vp] * 9 + [i32] * 6 + [ctypes.c_int, i32, f32, f32] +
                                [vp] * 11 + [vp, sz, vp])
+    L.kdn_forward_kam.argtypes = [vp] * 12 + [i32] * 6 + [ctypes.c_int, f32, vp]
+    L.kdn_forward_kam.restype = ctypes.c_int
     L.kdn_backward_workspace_bytes.argtypes = [i32] * 8
     L.kdn_backward_workspace_bytes.restype = sz
     L.kdn_forward_workspace_bytes.argtypes = [i32] * 7 + [ctypes.c_int, i32, i32]
@@ -375,3 +379,24 @@ def backward(variant, q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=Non
                             _stream(dev))
     _check(st, "kdn_backward")
     return g
+
+
+def forward_kam(q, k, v, alpha, omega, r, S0=None, P0=None, cu_seqlens=None, scale=None):
+    """Kalman Associative Memory (dense dk x dk covariance); returns (o, S_T, P_T)."""
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    _same(k.dtype, q, v, alpha, omega, r)
+    dev = k.device
+    N = B if cu_seqlens is None else cu_seqlens.numel() - 1
+    scale = float(dk ** -0.5 if scale is None else scale)
+    if cu_seqlens is not None and cu_seqlens.dtype != torch.int32:
+        raise TypeError("cu_seqlens must be int32")
+    o = torch.empty((B, T, H, dv), dtype=k.dtype, device=dev)
+    S_T = torch.empty((N, H, dk, dv), dtype=torch.float32, device=dev)
+    P_T = torch.empty((N, H, dk, dk), dtype=torch.float32, device=dev)
+    st = lib().kdn_forward_kam(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(omega), _ptr(r),
+                               _ptr(_f32(S0)), _ptr(_f32(P0)), _ptr(o), _ptr(S_T), _ptr(P_T),
+                               _ptr(cu_seqlens), N, B, T, H, dk, dv, _dtype_code(k),
+                               ctypes.c_float(scale), _stream(dev))
+    _check(st, "kdn_forward_kam")
+    return o, S_T, P_T
