@@ -371,53 +371,54 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
 }
 
 // ------------------------------------------------------------------------------------------
-// walks over the chunks of one (sequence, head, value tile). Products are register-blocked:
-// a thread computes 2 x 4 (chunk rows x value columns) or 4 x 4 (key rows x value columns)
-// outputs from float4 reads of LDS rows padded to multiples of four floats.
+// walks over the chunks of one (sequence, head, value tile of up to 32 columns): every product
+// on float32 MFMA (16 x 16 x 4) from LDS operands laid out so that both sides are contiguous
+// in the contraction index (the state and the chunk's value-side tiles are kept transposed).
+// Wave w of 8 takes 16 x 16 output tiles w, w + 8, ...
 // ------------------------------------------------------------------------------------------
 template <int DK>
 struct WalkLds {
-    static constexpr int LDV = 36, LDK = DK + 4, LDC = C + 4;
-    static constexpr size_t OFF_S = 0;                                      // [DK][LDV]
-    static constexpr size_t OFF_R1 = OFF_S + (size_t)DK * LDV * 4;          // [C][LDK]
-    static constexpr size_t OFF_R2 = OFF_R1 + (size_t)C * LDK * 4;          // [C][LDK]
-    static constexpr size_t OFF_A = OFF_R2 + (size_t)C * LDK * 4;           // [C][LDC]
-    static constexpr size_t OFF_B = OFF_A + (size_t)C * LDC * 4;            // [C][LDC]
-    static constexpr size_t OFF_X = OFF_B + (size_t)C * LDC * 4;            // [C][LDV]
-    static constexpr size_t OFF_D = OFF_X + (size_t)C * LDV * 4;
-    static constexpr size_t OFF_P = OFF_D + (size_t)C * LDV * 4;
-    static constexpr size_t OFF_GC = OFF_P + (size_t)C * LDV * 4;           // [DK]
-    static constexpr size_t TOTAL = al16(OFF_GC + (size_t)DK * 4);
+    static constexpr int LDK = DK + 4, LDC = C + 4, BVM = 32;
+    // forward walk
+    static constexpr size_t F_ST = 0;                                      // S^T [BVM][LDK]
+    static constexpr size_t F_KB = F_ST + (size_t)BVM * LDK * 4;           // Kbar [C][LDK]
+    static constexpr size_t F_KT = F_KB + (size_t)C * LDK * 4;             // Ktail^T [DK][LDC]
+    static constexpr size_t F_A = F_KT + (size_t)DK * LDC * 4;             // A [C][LDC]
+    static constexpr size_t F_XT = F_A + (size_t)C * LDC * 4;              // X^T [BVM][LDC]
+    static constexpr size_t F_DT = F_XT + (size_t)BVM * LDC * 4;           // Delta^T
+    static constexpr size_t F_GC = F_DT + (size_t)BVM * LDC * 4;           // gamma_C [DK]
+    static constexpr size_t F_TOTAL = al16(F_GC + (size_t)DK * 4);
+    // reverse walk
+    static constexpr size_t R_ST = 0;                                      // dS^T [BVM][LDK]
+    static constexpr size_t R_BT = R_ST + (size_t)BVM * LDK * 4;           // B^T [C][LDC]
+    static constexpr size_t R_AT = R_BT + (size_t)C * LDC * 4;             // A^T [C][LDC]
+    static constexpr size_t R_OT = R_AT + (size_t)C * LDC * 4;             // scale dO^T [BVM][LDC]
+    static constexpr size_t R_DT = R_OT + (size_t)BVM * LDC * 4;           // dDelta^T
+    static constexpr size_t R_PT = R_DT + (size_t)BVM * LDC * 4;           // Psi^T
+    static constexpr size_t R_GC = R_PT + (size_t)BVM * LDC * 4;           // gamma_C [DK]
+    static constexpr size_t R_R = al16(R_GC + (size_t)DK * 4);             // Ktail [C][LDK], or
+    static constexpr size_t R_R2 = R_R + (size_t)DK * LDC * 4;             // Qbar^T, Kbar^T [DK][LDC]
+    static constexpr size_t R_TOTAL = al16(R_R + cmax((size_t)C * LDK * 4,
+                                                      (size_t)2 * DK * LDC * 4));
+    static constexpr size_t TOTAL = cmax(F_TOTAL, R_TOTAL);
 };
 
-__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
-__device__ __forceinline__ void st4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
-__device__ __forceinline__ void fma4(float4& acc, float a, float4 b)
-{
-    acc.x = fmaf(a, b.x, acc.x);
-    acc.y = fmaf(a, b.y, acc.y);
-    acc.z = fmaf(a, b.z, acc.z);
-    acc.w = fmaf(a, b.w, acc.w);
-}
+using FF = Frag<float, 16>;  // one 16-deep step of a float32 product: four 16 x 16 x 4 MFMAs
 
-// record operands [C][DK] (and [C][C]) from global memory into padded LDS rows
-template <int DK>
-__device__ __forceinline__ void stage_ck(float* dst, const float* __restrict__ src, int tid)
-    
+// acc += A[ar0 + 16 rows][k0 .. k0 + 16 * nk) * B[k][br0 + 16 columns], A row-major (lda), B
+// stored transposed (row = output column, ldb), k-steps ks0 .. ks1 - 1 of 16
+__device__ __forceinline__ floatx4 mfma_rows(floatx4 acc, const float* A, int lda,
+                                             const float* Bt, int ldb, int ks0, int ks1,
+                                             int lane, bool negA = false)
 {
-    constexpr int LDK = WalkLds<DK>::LDK, Q = DK / 4;
-    for (int e = tid; e < C * Q; e += NTB) {
-        const int t = e / Q, i4 = e % Q;
-        st4(dst + t * LDK + 4 * i4, ld4(src + (size_t)t * DK + 4 * i4));
+    const int li = lane & 15, lg = lane >> 4;
+    for (int ks = ks0; ks < ks1; ++ks) {
+        FF::V av = FF::ld(A + li * lda + 16 * ks + 4 * lg);
+        const FF::V bv = FF::ld(Bt + li * ldb + 16 * ks + 4 * lg);
+        if (negA) av ^= make_uint4(0x80000000u, 0x80000000u, 0x80000000u, 0x80000000u);
+        acc = FF::mma(acc, av, bv);
     }
-}
-__device__ __forceinline__ void stage_cc(float* dst, const float* __restrict__ src, int tid)
-{
-    constexpr int LDC = C + 4;
-    for (int e = tid; e < C * C / 4; e += NTB) {
-        const int t = e / (C / 4), s4 = e % (C / 4);
-        st4(dst + t * LDC + 4 * s4, ld4(src + (size_t)t * C + 4 * s4));
-    }
+    return acc;
 }
 
 template <class TI, int DK>
@@ -425,21 +426,21 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
-    constexpr int LDV = LY::LDV, LDK = LY::LDK, LDC = LY::LDC;
+    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    float* s_S = (float*)(smem + LY::OFF_S);
-    float* s_kb = (float*)(smem + LY::OFF_R1);
-    float* s_kt = (float*)(smem + LY::OFF_R2);
-    float* s_A = (float*)(smem + LY::OFF_A);
-    float* s_X = (float*)(smem + LY::OFF_X);
-    float* s_D = (float*)(smem + LY::OFF_D);
-    float* s_gc = (float*)(smem + LY::OFF_GC);
+    float* s_St = (float*)(smem + LY::F_ST);
+    float* s_kb = (float*)(smem + LY::F_KB);
+    float* s_ktT = (float*)(smem + LY::F_KT);
+    float* s_A = (float*)(smem + LY::F_A);
+    float* s_XT = (float*)(smem + LY::F_XT);
+    float* s_DT = (float*)(smem + LY::F_DT);
+    float* s_gc = (float*)(smem + LY::F_GC);
 
-    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJ = BV / 4;
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJT = BV / 16;
     const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
     if (slot >= a.cm.N * H) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, li = lane & 15, lg = lane >> 4;
     float* __restrict__ ckpt = a.ckpt;
     float* __restrict__ dlt = a.dlt;
     int t0, t1, g0, nch;
@@ -447,75 +448,80 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
     seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
     for (int e = tid; e < DK * BV; e += NTB) {
         const int i = e / BV, j = e % BV;
-        s_S[i * LDV + j] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
+        s_St[j * LDK + i] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
     for (int ci = 0; ci < nch; ++ci) {
         const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
         const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
         const size_t gh = (size_t)g * H + h;
+        const float* __restrict__ kbar = (const float*)(rec + R::OFF_KBAR);
+        const float* __restrict__ ktl = (const float*)(rec + R::OFF_KTL);
+        const float* __restrict__ Am = (const float*)(rec + R::OFF_A);
+        const float* __restrict__ gC = (const float*)(rec + R::OFF_GC);
         __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTB) {
+        for (int e = tid; e < DK * BV; e += NTB) {  // checkpoint: S_in of this chunk
             const int i = e / BV, j = e % BV;
-            ckpt[(gh * DK + i) * DV + j0 + j] = s_S[i * LDV + j];
+            ckpt[(gh * DK + i) * DV + j0 + j] = s_St[j * LDK + i];
         }
-        stage_ck<DK>(s_kb, (const float*)(rec + R::OFF_KBAR), tid);
-        stage_ck<DK>(s_kt, (const float*)(rec + R::OFF_KTL), tid);
-        stage_cc(s_A, (const float*)(rec + R::OFF_A), tid);
-        for (int e = tid; e < DK; e += NTB) s_gc[e] = ((const float*)(rec + R::OFF_GC))[e];
-        for (int e = tid; e < C * BV; e += NTB) {
-            const int t = e / BV, j = e % BV;
-            s_X[t * LDV + j] =
-                t < L ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + j) : 0.f;
+        for (int e = tid; e < C * DK / 4; e += NTB) {
+            const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
+            *reinterpret_cast<float4*>(s_kb + t * LDK + i4) =
+                *reinterpret_cast<const float4*>(kbar + (size_t)t * DK + i4);
+        }
+        for (int e = tid; e < C * DK; e += NTB) {  // Ktail^T: coalesced reads, transposed writes
+            const int t = e / DK, i = e % DK;
+            s_ktT[i * LDC + t] = ktl[e];
+        }
+        for (int e = tid; e < C * C / 4; e += NTB) {
+            const int t = e / (C / 4), s4 = 4 * (e % (C / 4));
+            *reinterpret_cast<float4*>(s_A + t * LDC + s4) =
+                *reinterpret_cast<const float4*>(Am + (size_t)t * C + s4);
+        }
+        for (int e = tid; e < DK; e += NTB) s_gc[e] = gC[e];
+        __syncthreads();
+        // X = V - Kbar S_in (tile: rows 16 tb, columns 16 jb); stored as X^T
+        for (int tile = w; tile < 4 * NJT; tile += NWB) {
+            const int tb = tile / NJT, jb = tile % NJT;
+            floatx4 acc = zero4();
+            acc = mfma_rows(acc, s_kb + 16 * tb * LDK, LDK, s_St + 16 * jb * LDK, LDK, 0, NKT,
+                            lane);
+            float x[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * tb + 4 * lg + r;
+                const float vv =
+                    t < L ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + 16 * jb + li) : 0.f;
+                x[r] = vv - acc[r];
+            }
+            *reinterpret_cast<float4*>(s_XT + (16 * jb + li) * LDC + 16 * tb + 4 * lg) =
+                make_float4(x[0], x[1], x[2], x[3]);
         }
         __syncthreads();
-        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // X = V - Kbar S_in
-            const int t = 2 * (e / NJ), j = 4 * (e % NJ);
-            float4 x0 = ld4(s_X + t * LDV + j), x1 = ld4(s_X + (t + 1) * LDV + j);
-            for (int i = 0; i < DK; ++i) {
-                const float4 sv = ld4(s_S + i * LDV + j);
-                fma4(x0, -s_kb[t * LDK + i], sv);
-                fma4(x1, -s_kb[(t + 1) * LDK + i], sv);
-            }
-            st4(s_X + t * LDV + j, x0);
-            st4(s_X + (t + 1) * LDV + j, x1);
+        // Delta = A X (A lower triangular: k-steps up to the row tile); stored as Delta^T and
+        // to the workspace
+        for (int tile = w; tile < 4 * NJT; tile += NWB) {
+            const int tb = tile / NJT, jb = tile % NJT;
+            floatx4 acc = zero4();
+            acc = mfma_rows(acc, s_A + 16 * tb * LDC, LDC, s_XT + 16 * jb * LDC, LDC, 0, tb + 1,
+                            lane);
+            *reinterpret_cast<float4*>(s_DT + (16 * jb + li) * LDC + 16 * tb + 4 * lg) =
+                make_float4(acc[0], acc[1], acc[2], acc[3]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                dlt[(gh * C + 16 * tb + 4 * lg + r) * DV + j0 + 16 * jb + li] = acc[r];
         }
         __syncthreads();
-        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // Delta = A X
-            const int t = 2 * (e / NJ), j = 4 * (e % NJ);
-            float4 d0 = make_float4(0.f, 0.f, 0.f, 0.f), d1 = d0;
-            for (int s2 = 0; s2 <= t + 1; ++s2) {
-                const float4 xv = ld4(s_X + s2 * LDV + j);
-                fma4(d0, s_A[t * LDC + s2], xv);
-                fma4(d1, s_A[(t + 1) * LDC + s2], xv);
-            }
-            st4(s_D + t * LDV + j, d0);
-            st4(s_D + (t + 1) * LDV + j, d1);
-        }
-        __syncthreads();
-        for (int e = tid; e < C * BV; e += NTB) {
-            const int t = e / BV, j = e % BV;
-            dlt[(gh * C + t) * DV + j0 + j] = s_D[t * LDV + j];
-        }
-        for (int e = tid; e < (DK / 4) * NJ; e += NTB) {  // S_out = gamma_C S_in + Ktail^T Delta
-            const int i = 4 * (e / NJ), j = 4 * (e % NJ);
-            float4 r0 = ld4(s_S + i * LDV + j), r1 = ld4(s_S + (i + 1) * LDV + j);
-            float4 r2 = ld4(s_S + (i + 2) * LDV + j), r3 = ld4(s_S + (i + 3) * LDV + j);
-            const float4 gc = ld4(s_gc + i);
-            r0.x *= gc.x; r0.y *= gc.x; r0.z *= gc.x; r0.w *= gc.x;
-            r1.x *= gc.y; r1.y *= gc.y; r1.z *= gc.y; r1.w *= gc.y;
-            r2.x *= gc.z; r2.y *= gc.z; r2.z *= gc.z; r2.w *= gc.z;
-            r3.x *= gc.w; r3.y *= gc.w; r3.z *= gc.w; r3.w *= gc.w;
-            for (int t = 0; t < C; ++t) {
-                const float4 kt = ld4(s_kt + t * LDK + i), dv = ld4(s_D + t * LDV + j);
-                fma4(r0, kt.x, dv);
-                fma4(r1, kt.y, dv);
-                fma4(r2, kt.z, dv);
-                fma4(r3, kt.w, dv);
-            }
-            st4(s_S + i * LDV + j, r0);
-            st4(s_S + (i + 1) * LDV + j, r1);
-            st4(s_S + (i + 2) * LDV + j, r2);
-            st4(s_S + (i + 3) * LDV + j, r3);
+        // S_out^T = S_in^T diag(gamma_C) + Delta^T Ktail (tile: rows 16 jb of S^T, columns 16 ib)
+        for (int tile = w; tile < NJT * NKT; tile += NWB) {
+            const int jb = tile % NJT, ib = tile / NJT;
+            const float gc = s_gc[16 * ib + li];
+            floatx4 acc;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[r] = s_St[(16 * jb + 4 * lg + r) * LDK + 16 * ib + li] * gc;
+            acc = mfma_rows(acc, s_DT + 16 * jb * LDC, LDC, s_ktT + 16 * ib * LDC, LDC, 0, 4,
+                            lane);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s_St[(16 * jb + 4 * lg + r) * LDK + 16 * ib + li] = acc[r];
         }
     }
 }
@@ -525,23 +531,24 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
-    constexpr int LDV = LY::LDV, LDK = LY::LDK, LDC = LY::LDC;
+    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    float* s_dS = (float*)(smem + LY::OFF_S);
-    float* s_r1 = (float*)(smem + LY::OFF_R1);
-    float* s_r2 = (float*)(smem + LY::OFF_R2);
-    float* s_A = (float*)(smem + LY::OFF_A);
-    float* s_B = (float*)(smem + LY::OFF_B);
-    float* s_O = (float*)(smem + LY::OFF_X);   // scale dO
-    float* s_dD = (float*)(smem + LY::OFF_D);
-    float* s_P = (float*)(smem + LY::OFF_P);
-    float* s_gc = (float*)(smem + LY::OFF_GC);
+    float* s_dST = (float*)(smem + LY::R_ST);
+    float* s_BT = (float*)(smem + LY::R_BT);
+    float* s_AT = (float*)(smem + LY::R_AT);
+    float* s_OT = (float*)(smem + LY::R_OT);
+    float* s_dDT = (float*)(smem + LY::R_DT);
+    float* s_PT = (float*)(smem + LY::R_PT);
+    float* s_gc = (float*)(smem + LY::R_GC);
+    float* s_kt = (float*)(smem + LY::R_R);    // Ktail [C][LDK] (first half of the chunk)
+    float* s_qT = (float*)(smem + LY::R_R);    // Qbar^T [DK][LDC] (second half)
+    float* s_kT = (float*)(smem + LY::R_R2);   // Kbar^T [DK][LDC]
 
-    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJ = BV / 4;
+    const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJT = BV / 16;
     const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
     if (slot >= a.cm.N * H) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, li = lane & 15, lg = lane >> 4;
     float* __restrict__ dso = a.dso;
     float* __restrict__ gv = a.dv;
     int t0, t1, g0, nch;
@@ -549,94 +556,94 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
     seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
     for (int e = tid; e < DK * BV; e += NTB) {
         const int i = e / BV, j = e % BV;
-        s_dS[i * LDV + j] = a.dS_T ? a.dS_T[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
+        s_dST[j * LDK + i] = a.dS_T ? a.dS_T[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
     for (int ci = nch - 1; ci >= 0; --ci) {
         const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
         const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
         const size_t gh = (size_t)g * H + h;
+        const float* __restrict__ ktl = (const float*)(rec + R::OFF_KTL);
+        const float* __restrict__ Am = (const float*)(rec + R::OFF_A);
+        const float* __restrict__ Bm = (const float*)(rec + R::OFF_B);
+        const float* __restrict__ gC = (const float*)(rec + R::OFF_GC);
+        const float* __restrict__ qbar = (const float*)(rec + R::OFF_QBAR);
+        const float* __restrict__ kbar = (const float*)(rec + R::OFF_KBAR);
         __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTB) {
+        for (int e = tid; e < DK * BV; e += NTB) {  // dS_out of this chunk
             const int i = e / BV, j = e % BV;
-            dso[(gh * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
+            dso[(gh * DK + i) * DV + j0 + j] = s_dST[j * LDK + i];
         }
-        stage_ck<DK>(s_r1, (const float*)(rec + R::OFF_KTL), tid);
-        stage_cc(s_A, (const float*)(rec + R::OFF_A), tid);
-        stage_cc(s_B, (const float*)(rec + R::OFF_B), tid);
-        for (int e = tid; e < DK; e += NTB) s_gc[e] = ((const float*)(rec + R::OFF_GC))[e];
-        for (int e = tid; e < C * BV; e += NTB) {
+        for (int e = tid; e < C * DK / 4; e += NTB) {
+            const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
+            *reinterpret_cast<float4*>(s_kt + t * LDK + i4) =
+                *reinterpret_cast<const float4*>(ktl + (size_t)t * DK + i4);
+        }
+        for (int e = tid; e < C * C; e += NTB) {  // B^T and A^T
+            const int t = e / C, s2 = e % C;
+            s_BT[s2 * LDC + t] = Bm[e];
+            s_AT[s2 * LDC + t] = Am[e];
+        }
+        for (int e = tid; e < DK; e += NTB) s_gc[e] = gC[e];
+        for (int e = tid; e < C * BV; e += NTB) {  // scale dO, transposed
             const int t = e / BV, j = e % BV;
-            s_O[t * LDV + j] = (t < L && a.dO)
-                                   ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
-                                   : 0.f;
+            s_OT[j * LDC + t] = (t < L && a.dO)
+                                    ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
+                                    : 0.f;
         }
         __syncthreads();
-        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // dDelta = B^T (scale dO) + Ktail dS_out
-            const int s2 = 2 * (e / NJ), j = 4 * (e % NJ);
-            float4 d0 = make_float4(0.f, 0.f, 0.f, 0.f), d1 = d0;
-            for (int t = s2; t < C; ++t) {
-                const float4 ov = ld4(s_O + t * LDV + j);
-                const float2 bb = *reinterpret_cast<const float2*>(s_B + t * LDC + s2);
-                fma4(d0, bb.x, ov);
-                fma4(d1, bb.y, ov);
-            }
-            for (int i = 0; i < DK; ++i) {
-                const float4 sv = ld4(s_dS + i * LDV + j);
-                fma4(d0, s_r1[s2 * LDK + i], sv);
-                fma4(d1, s_r1[(s2 + 1) * LDK + i], sv);
-            }
-            st4(s_dD + s2 * LDV + j, d0);
-            st4(s_dD + (s2 + 1) * LDV + j, d1);
+        // dDelta = B^T (scale dO) + Ktail dS_out (tile: rows 16 sb, columns 16 jb), stored
+        // transposed; B^T is upper triangular: k-steps from the row tile on
+        for (int tile = w; tile < 4 * NJT; tile += NWB) {
+            const int sb = tile / NJT, jb = tile % NJT;
+            floatx4 acc = zero4();
+            acc = mfma_rows(acc, s_BT + 16 * sb * LDC, LDC, s_OT + 16 * jb * LDC, LDC, sb, 4,
+                            lane);
+            acc = mfma_rows(acc, s_kt + 16 * sb * LDK, LDK, s_dST + 16 * jb * LDK, LDK, 0, NKT,
+                            lane);
+            *reinterpret_cast<float4*>(s_dDT + (16 * jb + li) * LDC + 16 * sb + 4 * lg) =
+                make_float4(acc[0], acc[1], acc[2], acc[3]);
         }
         __syncthreads();
-        for (int e = tid; e < (C / 2) * NJ; e += NTB) {  // Psi = A^T dDelta = dV
-            const int s2 = 2 * (e / NJ), j = 4 * (e % NJ);
-            float4 p0 = make_float4(0.f, 0.f, 0.f, 0.f), p1 = p0;
-            for (int t = s2; t < C; ++t) {
-                const float4 dv = ld4(s_dD + t * LDV + j);
-                const float2 aa = *reinterpret_cast<const float2*>(s_A + t * LDC + s2);
-                fma4(p0, aa.x, dv);
-                fma4(p1, aa.y, dv);
+        // Psi = A^T dDelta = dV (A^T upper triangular), stored transposed and to dv
+        for (int tile = w; tile < 4 * NJT; tile += NWB) {
+            const int sb = tile / NJT, jb = tile % NJT;
+            floatx4 acc = zero4();
+            acc = mfma_rows(acc, s_AT + 16 * sb * LDC, LDC, s_dDT + 16 * jb * LDC, LDC, sb, 4,
+                            lane);
+            *reinterpret_cast<float4*>(s_PT + (16 * jb + li) * LDC + 16 * sb + 4 * lg) =
+                make_float4(acc[0], acc[1], acc[2], acc[3]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * sb + 4 * lg + r;
+                if (t < L) gv[((size_t)(c0 + t) * H + h) * DV + j0 + 16 * jb + li] = acc[r];
             }
-            st4(s_P + s2 * LDV + j, p0);
-            st4(s_P + (s2 + 1) * LDV + j, p1);
         }
         __syncthreads();
-        for (int e = tid; e < C * BV; e += NTB) {
-            const int t = e / BV, j = e % BV;
-            if (t < L) gv[((size_t)(c0 + t) * H + h) * DV + j0 + j] = s_P[t * LDV + j];
+        for (int e = tid; e < C * DK; e += NTB) {  // Qbar^T and Kbar^T over the Ktail area
+            const int t = e / DK, i = e % DK;
+            s_qT[i * LDC + t] = qbar[e];
+            s_kT[i * LDC + t] = kbar[e];
         }
-        stage_ck<DK>(s_r1, (const float*)(rec + R::OFF_QBAR), tid);
-        stage_ck<DK>(s_r2, (const float*)(rec + R::OFF_KBAR), tid);
         __syncthreads();
-        for (int e = tid; e < (DK / 4) * NJ; e += NTB) {  // dS_in
-            const int i = 4 * (e / NJ), j = 4 * (e % NJ);
-            float4 r0 = ld4(s_dS + i * LDV + j), r1 = ld4(s_dS + (i + 1) * LDV + j);
-            float4 r2 = ld4(s_dS + (i + 2) * LDV + j), r3 = ld4(s_dS + (i + 3) * LDV + j);
-            const float4 gc = ld4(s_gc + i);
-            r0.x *= gc.x; r0.y *= gc.x; r0.z *= gc.x; r0.w *= gc.x;
-            r1.x *= gc.y; r1.y *= gc.y; r1.z *= gc.y; r1.w *= gc.y;
-            r2.x *= gc.z; r2.y *= gc.z; r2.z *= gc.z; r2.w *= gc.z;
-            r3.x *= gc.w; r3.y *= gc.w; r3.z *= gc.w; r3.w *= gc.w;
-            for (int t = 0; t < C; ++t) {
-                const float4 qb = ld4(s_r1 + t * LDK + i), kb = ld4(s_r2 + t * LDK + i);
-                const float4 ov = ld4(s_O + t * LDV + j), pv = ld4(s_P + t * LDV + j);
-                fma4(r0, qb.x, ov); fma4(r0, -kb.x, pv);
-                fma4(r1, qb.y, ov); fma4(r1, -kb.y, pv);
-                fma4(r2, qb.z, ov); fma4(r2, -kb.z, pv);
-                fma4(r3, qb.w, ov); fma4(r3, -kb.w, pv);
-            }
-            st4(s_dS + i * LDV + j, r0);
-            st4(s_dS + (i + 1) * LDV + j, r1);
-            st4(s_dS + (i + 2) * LDV + j, r2);
-            st4(s_dS + (i + 3) * LDV + j, r3);
+        // dS_in^T = dS_out^T diag(gamma_C) + (scale dO)^T Qbar - Psi^T Kbar
+        for (int tile = w; tile < NJT * NKT; tile += NWB) {
+            const int jb = tile % NJT, ib = tile / NJT;
+            const float gc = s_gc[16 * ib + li];
+            floatx4 acc;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[r] = s_dST[(16 * jb + 4 * lg + r) * LDK + 16 * ib + li] * gc;
+            acc = mfma_rows(acc, s_OT + 16 * jb * LDC, LDC, s_qT + 16 * ib * LDC, LDC, 0, 4, lane);
+            acc = mfma_rows(acc, s_PT + 16 * jb * LDC, LDC, s_kT + 16 * ib * LDC, LDC, 0, 4, lane,
+                            true);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) s_dST[(16 * jb + 4 * lg + r) * LDK + 16 * ib + li] = acc[r];
         }
     }
     __syncthreads();
     if (a.dS0)
         for (int e = tid; e < DK * BV; e += NTB) {
             const int i = e / BV, j = e % BV;
-            a.dS0[((size_t)slot * DK + i) * DV + j0 + j] = s_dS[i * LDV + j];
+            a.dS0[((size_t)slot * DK + i) * DV + j0 + j] = s_dST[j * LDK + i];
         }
 }
 
@@ -1107,8 +1114,8 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
     static bool attr = false;
     if (!attr) {
         if ((e = lds_attr(bw_prep<TI, DK, VARIANT, APC>, PrepLds<DK>::TOTAL)) != hipSuccess ||
-            (e = lds_attr(bw_fwalk<TI, DK>, WalkLds<DK>::TOTAL)) != hipSuccess ||
-            (e = lds_attr(bw_rwalk<TI, DK>, WalkLds<DK>::TOTAL)) != hipSuccess ||
+            (e = lds_attr(bw_fwalk<TI, DK>, WalkLds<DK>::F_TOTAL)) != hipSuccess ||
+            (e = lds_attr(bw_rwalk<TI, DK>, WalkLds<DK>::R_TOTAL)) != hipSuccess ||
             (e = lds_attr(bw_grad<TI, DK, VARIANT, APC>, GradLds<DK>::TOTAL)) != hipSuccess)
             return e;
         attr = true;
@@ -1120,9 +1127,9 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
     }
     const int NV = bc.dv / a.BV;
     const dim3 wgrid((unsigned)((size_t)sa.N * sa.H * NV));
-    hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::TOTAL, st, a);
+    hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::F_TOTAL, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::TOTAL, st, a);
+    hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::R_TOTAL, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (m.maxch > 0) {
         hipLaunchKernelGGL((bw_grad<TI, DK, VARIANT, APC>), cgrid, dim3(NTB), GradLds<DK>::TOTAL,
