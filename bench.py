@@ -10,11 +10,12 @@ chunk summaries of the variance chain, the log-depth carry scan, the per-chunk p
 and the chunk operands, and the walk that carries the memory through the chunks).
 
 Prints one JSON line: tokens/s of the headline forward, the roofline position of one forward call
-(algorithmic bytes per call / the HIP-event duration of the call on the caller's stream, against
-the 8 TB/s HBM peak), the CPU oracle timed on a bounded sample of the same workload, and one
-object per other workload of the path (the isotropic forward, the packed variable-length batch,
-the decode workload's prefill and decode steps, the gain scan alone, the backward, the layer
-forward with its maps fused), each timed the same way.
+(algorithmic bytes per call / the GPU time per call, from HIP events on the caller's stream around
+the K back-to-back calls of the timed region, against the 8 TB/s HBM peak), the CPU oracle timed
+on a bounded sample of the same workload, and one object per other workload of the path (the
+isotropic forward, the packed variable-length batch, the decode workload's prefill and decode
+steps, the gain scan alone, the backward, the layer forward with its maps fused), timed the same
+way (decode: events around every call, whose host side would otherwise set the pace).
 The larger workloads draw their inputs on the GPU with the same laws (timing only; their parity
 is checked by the tests on host-drawn inputs).
 """
@@ -111,21 +112,37 @@ def gpu_inputs(torch, variant, B, T, H, dk, dv, seed, apc=True, random_state=Fal
 NAMES = ("q", "k", "v", "alpha", "omega", "r")
 
 
-def time_calls(torch, fn, steps, warmup):
-    """HIP events around every call on torch's current stream (the stream the binding passes to
-    the library; every kernel of a call runs on it). Returns per-call milliseconds."""
+def time_calls(torch, fn, steps, warmup, per_call=False, reps=5):
+    """Milliseconds per call on torch's current stream (the stream the binding passes to the
+    library; every kernel of a call runs on it).
+
+    Default: `reps` regions of `steps` back-to-back calls, HIP events around each region; one
+    value (region time / steps) per region. per_call=True: events around every call instead,
+    one value per call (for calls short enough that the host, not the GPU, would set the pace
+    of back-to-back calls; each pair of timing events adds a few microseconds of its own)."""
     stream = torch.cuda.current_stream()
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    for a, b in ev:
+    if per_call:
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        for a, b in ev:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in ev]
+    out = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        fn()
+        for _ in range(steps):
+            fn()
         b.record(stream)
-    torch.cuda.synchronize()
-    return [a.elapsed_time(b) for a, b in ev]
+        torch.cuda.synchronize()
+        out.append(a.elapsed_time(b) / steps)
+    return out
 
 
 def summary(ms, nbytes, tokens, extra=None):
@@ -191,7 +208,7 @@ def bench_decode_workload(torch, kdn, steps):
         args = [st[n][:, 0].contiguous() for n in NAMES]
         S, P = st["S0"], st["P0"]
         ms = time_calls(torch, lambda: kdn.decode_step(variant, *args, S, P, mu=float(d),
-                                                       scale=d ** -0.5), 64, 5)
+                                                       scale=d ** -0.5), 64, 5, per_call=True)
         out[f"decode_{variant}"] = summary(
             ms, decode_bytes(R, H, d, d, 2, variant), R,
             {"workload": f"{variant}-decode-R256-H16-d128 (state pool of 256 slots, 256 MiB)",
@@ -201,7 +218,7 @@ def bench_decode_workload(torch, kdn, steps):
     slots = torch.arange(0, 4 * R, 4, dtype=torch.int32, device="cuda")
     ms = time_calls(torch, lambda: kdn.decode_step("diag", *args, st["S0"], st["P0"],
                                                    slot_idx=slots, mu=float(d),
-                                                   scale=d ** -0.5), 64, 5)
+                                                   scale=d ** -0.5), 64, 5, per_call=True)
     out["decode_diag_pool1024"] = summary(
         ms, decode_bytes(R, H, d, d, 2, "diag"), R,
         {"workload": "diag-decode-R256-H16-d128, rows on every fourth slot of a 1024-slot pool "
@@ -337,7 +354,7 @@ def measured_traffic():
         from paper_2609_07816_amd.rocprof_summary import source_hash
         with open(PROFILE) as f:
             rec = json.load(f)
-        if rec.get("kernel_source_sha256") != source_hash():
+        if rec.get("kernel_source_sha256") != source_hash(rec.get("kernel_sources")):
             return None
         return int(round(rec["traffic_bytes"]))
     except (OSError, ValueError, KeyError):
@@ -407,27 +424,24 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: K steps between two synchronisations; HIP events around every forward
-    # call on torch's current stream, which the binding passes to the library (every kernel of
-    # the call runs on that stream)
+    # timed region: K steps between two synchronisations, back to back on torch's current
+    # stream, which the binding passes to the library (every kernel of the call runs on that
+    # stream); HIP events around the region give the GPU's time per call
     stream = torch.cuda.current_stream()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev0.record(stream)
     for i in range(args.steps):
-        ev[i][0].record(stream)
         step()
-        ev[i][1].record(stream)
+    ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    kmean = ev0.elapsed_time(ev1) / args.steps
 
     ms_per_step = 1e3 * wall / args.steps
     tokens = B * T
     value = tokens / (ms_per_step / 1e3)
-    kmean = float(np.mean(kern_ms))
-    kmed = float(np.median(kern_ms))
     abytes = forward_bytes(B * T, B, H, dk, dv, 2, "diag")
     aflops = forward_flops(B * T, H, dk, dv)
     achieved = abytes / (kmean * 1e-3) / 1e9
@@ -453,7 +467,7 @@ def main():
                      "traffic": measured_traffic(),
                      "kernel": FORWARD_KERNELS + "; bf16, dk=dv=128, chunk 64",
                      "algorithmic_bytes_per_launch": abytes,
-                     "kernel_ms_mean": round(kmean, 4), "kernel_ms_median": round(kmed, 4),
+                     "kernel_ms_mean": round(kmean, 4),
                      "mfma_frac": round(aflops / (kmean * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
                                         4)},
     }

@@ -32,14 +32,16 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_07816_amd", "csrc")
 
 
-def source_hash() -> str:
-    """Hash of every HIP source and header of the library (a summary is stale once any of the
-    kernels it measured has changed)."""
+def source_hash(names=None) -> str:
+    """Hash of the library's HIP sources and headers that define and launch the kernels a
+    summary measured (`names`, file names under csrc/; default: all of them). A summary is stale
+    once any of those files has changed."""
+    if names is None:
+        names = [n for n in os.listdir(CSRC) if n.endswith((".hip", ".h"))]
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(CSRC, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in sorted(names):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
 
 
@@ -157,6 +159,8 @@ def main():
                     "which the first kept unit is still dropped as a warm-up)")
     ap.add_argument("--notes", default="", help="text file appended to the summary")
     ap.add_argument("--commands", required=True, help="text file with the commands that ran")
+    ap.add_argument("--sources", default="", help="comma-separated csrc/ files that define and "
+                    "launch the measured kernels (default: all of csrc/)")
     args = ap.parse_args()
 
     window = tuple(int(v) for v in args.window.split(":")) if args.window else None
@@ -181,7 +185,9 @@ def main():
     read_b = fk * 1024.0 * f_scale
     write_b = wk * 1024.0 * w_scale
     sq = sq_counters(args.sq, units) if args.sq else {}
-    rec = dict(unit=args.title or args.name, kernel_source_sha256=source_hash(),
+    sources = sorted(args.sources.split(",")) if args.sources else None
+    rec = dict(unit=args.title or args.name, kernel_source_sha256=source_hash(sources),
+               kernel_sources=sources,
                units=len(steady), span_ns=span_ns, kernels=stats,
                fetch_kib_per_unit=fk, write_kib_per_unit=wk, counter_units=[nf, nw],
                fetch_kib_per_kernel=fkk, write_kib_per_kernel=wkk,
@@ -211,7 +217,8 @@ def main():
     md = f"""# {args.name}
 
 Unit: {args.title or args.name}.
-Kernel source sha256 (all of csrc/): `{rec['kernel_source_sha256']}`
+Kernel source sha256 ({', '.join(sources) if sources else 'all of csrc/'}):
+`{rec['kernel_source_sha256']}`
 
 ## Span and kernels (rocprofv3 --kernel-trace --stats)
 
