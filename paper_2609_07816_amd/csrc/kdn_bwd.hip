@@ -650,26 +650,43 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
 // ------------------------------------------------------------------------------------------
 // bw_grad: chunk-parallel gradients of the memory scan and the variance-adjoint coefficients
 // ------------------------------------------------------------------------------------------
+// Wave w owns row block rb = w % 4 of the chunk and the channel tiles ct = w / 4 + 2 k: it keeps
+// dq, dk and dkappa of those 16 x 16 tiles in registers through both phases (float32 MFMA).
+//  1. products over the value columns, by slabs of 32 columns: Psi S_in^T, dO S_in^T and
+//     Delta dS_out^T on the owned tiles; dO Delta^T and Psi Delta^T (the adjoints of B and T)
+//     on the ten lower 16 x 16 blocks, wave w taking blocks w and w + 8; the diagonal terms
+//     sum_j S_in,ij dS_out,ij of the chunk-end decay.
+//  2. the terms through T and B, whose entries carry the decay ratios R_ts = gamma_t / gamma_s
+//     per channel, by slabs of 32 channels. For 16-token blocks b > c the ratio splits into the
+//     decay from the start of block b to t, the decay of the blocks between (a per-channel
+//     factor on the block product) and the decay from s to the end of block c, each <= 1;
+//     inside a diagonal block both sides are referenced to its token 8 (a factor saturates at
+//     2^100, beyond the inverse of any 8-token decay above 2^-100). The scaled operands are
+//     staged transposed; each block pair is one 16-deep MFMA step. Wave w forms the rows of
+//     block rb as the later token (dq, dk) and as the earlier token (dkappa).
+// The log-decay adjoint of an entry is then q dq + k dk - kappa dkappa; its chunk-end part
+// enters through column sums.
 template <int DK>
 struct GradLds {
-    static constexpr int SLB = DK < 32 ? DK : 32, LDV = 33, LDC = C + 1, LDZ = DK + 1;
-    static constexpr int LDS_ = SLB + 1;
-    static constexpr size_t OFF_DB = 0;                                      // [C][LDC]
-    static constexpr size_t OFF_DT = OFF_DB + (size_t)C * LDC * 4;
-    static constexpr size_t OFF_W = OFF_DT + (size_t)C * LDC * 4;
-    // value slabs: Delta, Psi, dO [C][LDV]; S_in, dS_out [DK][LDV]
-    static constexpr size_t W_D = 0, W_P = W_D + (size_t)C * LDV * 4, W_O = W_P + (size_t)C * LDV * 4;
-    static constexpr size_t W_S = W_O + (size_t)C * LDV * 4, W_G = W_S + (size_t)DK * LDV * 4;
-    static constexpr size_t W1 = W_G + (size_t)DK * LDV * 4;
-    // channel slabs: q, k, kappa [C][LDS_], lambda [C][LDS_] double
-    static constexpr size_t W_Q = 0, W_K = W_Q + (size_t)C * LDS_ * 4, W_KP = W_K + (size_t)C * LDS_ * 4;
-    static constexpr size_t W_L = al16(W_KP + (size_t)C * LDS_ * 4);
-    static constexpr size_t W2 = W_L + (size_t)C * LDS_ * 8;
-    static constexpr size_t OFF_C = OFF_W + al16(cmax(W1, W2));              // [C][LDZ]
-    static constexpr size_t OFF_DL = OFF_C + (size_t)C * LDZ * 4;            // dlambda [C][LDZ]
-    static constexpr size_t OFF_P6 = OFF_DL + (size_t)C * LDZ * 4;           // [DK]
+    static constexpr int SW = 32, LDW = SW + 4;     // value slab, rows padded to 16 bytes
+    static constexpr int SLB = DK < 32 ? DK : 32;   // channel slab of phase 2
+    static constexpr int LDC = C + 4, LDZ = DK + 1;
+    // phase 1: Delta, Psi, dO [C][LDW]; S_in, dS_out [DK][LDW]
+    static constexpr size_t P_D = 0, P_P = (size_t)C * LDW * 4, P_O = 2 * P_P;
+    static constexpr size_t P_S = 3 * P_P, P_G = P_S + (size_t)DK * LDW * 4;
+    static constexpr size_t P_END = P_G + (size_t)DK * LDW * 4;
+    // phase 2: dB, dT, dB^T, dT^T [C][LDC]; six operand slabs [SLB][LDC] (over phase 1)
+    static constexpr size_t CC = (size_t)C * LDC * 4, OPS = (size_t)SLB * LDC;
+    static constexpr size_t Q_DB = 0, Q_DT = CC, Q_DBT = 2 * CC, Q_DTT = 3 * CC, Q_OP = 4 * CC;
+    static constexpr size_t Q_END = Q_OP + 6 * OPS * 4;
+    // then the log-decay adjoint [C][LDZ] (over phase 2)
+    static constexpr size_t MAIN = cmax(cmax(P_END, Q_END), (size_t)C * LDZ * 4);
+    static constexpr size_t OFF_CP = al16(MAIN);                   // column sums [4][DK]
+    static constexpr size_t OFF_P6 = OFF_CP + (size_t)4 * DK * 4;  // [DK]
     static constexpr size_t TOTAL = al16(OFF_P6 + (size_t)DK * 4);
 };
+
+constexpr float RSAT = 1.2676506e30f;  // 2^100
 
 template <class TI, int DK, int VARIANT, bool APC>
 __global__ __launch_bounds__(NTB) void bw_grad(Args a)
@@ -677,24 +694,23 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     using R = BwRec<DK>;
     using LY = GradLds<DK>;
     constexpr bool DIAG = VARIANT == 0;
-    constexpr int SLB = LY::SLB, LDV = LY::LDV, LDC = LY::LDC, LDZ = LY::LDZ, LDS_ = LY::LDS_;
-    constexpr int Q = DK / 8;  // channels per thread in the dk-wide products
+    constexpr int SW = LY::SW, LDW = LY::LDW, SLB = LY::SLB, LDC = LY::LDC, LDZ = LY::LDZ;
+    constexpr int NKT = DK / 16, NCW = (NKT + 1) / 2;  // channel tiles; owned per wave
+    constexpr size_t OPS = LY::OPS;
     constexpr int NCHAN = DIAG ? DK : 1;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    float* s_dB = (float*)(smem + LY::OFF_DB);
-    float* s_dT = (float*)(smem + LY::OFF_DT);
-    char* wr = smem + LY::OFF_W;
-    float* s_D = (float*)(wr + LY::W_D);
-    float* s_P = (float*)(wr + LY::W_P);
-    float* s_O = (float*)(wr + LY::W_O);
-    float* s_S = (float*)(wr + LY::W_S);
-    float* s_G = (float*)(wr + LY::W_G);
-    float* s_q = (float*)(wr + LY::W_Q);
-    float* s_k = (float*)(wr + LY::W_K);
-    float* s_kp = (float*)(wr + LY::W_KP);
-    double* s_l = (double*)(wr + LY::W_L);
-    float* s_c = (float*)(smem + LY::OFF_C);
-    float* s_dl = (float*)(smem + LY::OFF_DL);
+    float* s_D = (float*)(smem + LY::P_D);
+    float* s_P = (float*)(smem + LY::P_P);
+    float* s_O = (float*)(smem + LY::P_O);
+    float* s_S = (float*)(smem + LY::P_S);
+    float* s_G = (float*)(smem + LY::P_G);
+    float* s_dB = (float*)(smem + LY::Q_DB);
+    float* s_dT = (float*)(smem + LY::Q_DT);
+    float* s_dBT = (float*)(smem + LY::Q_DBT);
+    float* s_dTT = (float*)(smem + LY::Q_DTT);
+    float* s_op = (float*)(smem + LY::Q_OP);  // [6][SLB][LDC]
+    float* s_dl = (float*)smem;               // [C][LDZ]
+    float* s_cp = (float*)(smem + LY::OFF_CP);
     float* s_p6 = (float*)(smem + LY::OFF_P6);
 
     const int H = a.H, DV = a.DV;
@@ -703,7 +719,9 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     bool last;
     if (!locate_chunk<C>(a.cm, g, n, c0, c1, last)) return;
     const int L = c1 - c0;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int rb = w & 3, cw = w >> 2;
     const size_t gh = (size_t)g * H + h;
     const char* rec = a.rec + gh * R::BYTES;
     const float* __restrict__ kap = (const float*)(rec + R::OFF_KAP);
@@ -717,142 +735,265 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     float* __restrict__ gk = a.dk;
     auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
 
-    // ---- products over the value columns, by slabs of 32 columns ---------------------------
-    //   P1 = dO Delta^T, P2 = Psi Delta^T (thread: row t, 16 columns s)
-    //   P3 = Psi S_in^T, P4 = dO S_in^T, P5 = Delta dS_out^T (thread: row t, Q channels)
-    //   P6_i = sum_j S_in,ij dS_out,ij
-    // lanes 8 r + c: row r; columns s = c + 8 e and channels i = c + 8 e (interleaved, so that
-    // the eight lanes of a row read eight consecutive LDS rows: no bank conflicts)
-    const int tr = tid >> 3, cl = tid & 7;
-    float p1[8], p2[8], p3[Q], p4[Q], p5[Q], p6 = 0.f;
+    // ---- 1. products over the value columns -------------------------------------------------
+    floatx4 p3[NCW], p4[NCW], p5[NCW], p1[2], p2[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) p1[e] = p2[e] = 0.f;
+    for (int k = 0; k < NCW; ++k) p3[k] = p4[k] = p5[k] = zero4();
+    // lower blocks numbered row by row: 0 (0,0), 1 (1,0), 2 (1,1), 3 (2,0), ..., 9 (3,3)
+    int pbt[2], pbs[2];
+    bool pbo[2];
 #pragma unroll
-    for (int e = 0; e < Q; ++e) p3[e] = p4[e] = p5[e] = 0.f;
-    for (int j0 = 0; j0 < DV; j0 += 32) {
-        const int SW = min(32, DV - j0);
+    for (int u = 0; u < 2; ++u) {
+        const int q = w + 8 * u;
+        pbo[u] = q < 10;
+        pbt[u] = q < 1 ? 0 : (q < 3 ? 1 : (q < 6 ? 2 : 3));
+        pbs[u] = q - pbt[u] * (pbt[u] + 1) / 2;
+        p1[u] = p2[u] = zero4();
+    }
+    float p6 = 0.f;  // thread: channel tid / 4, columns 8 (tid % 4) .. + 7 of each slab
+    for (int j0 = 0; j0 < DV; j0 += SW) {
+        const int SWc = min(SW, DV - j0);  // 16 or 32
         __syncthreads();
-        for (int e = tid; e < C * SW; e += NTB) {
-            const int t = e / SW, j = e % SW;
+        for (int e = tid; e < C * SW / 4; e += NTB) {
+            const int t = e / (SW / 4), j4 = 4 * (e % (SW / 4));
+            if (j4 >= SWc) continue;
+            const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 pv = z, ov = z;
+            const float4 dv4 = *reinterpret_cast<const float4*>(a.dlt + (gh * C + t) * DV + j0 + j4);
+            if (t < L) {
+                const size_t o = row(t) * DV + j0 + j4;
+                pv = *reinterpret_cast<const float4*>(a.dv + o);
+                if (a.dO)
+                    ov = make_float4(ld<TI>(a.dO, o), ld<TI>(a.dO, o + 1), ld<TI>(a.dO, o + 2),
+                                     ld<TI>(a.dO, o + 3));
+            }
+            *reinterpret_cast<float4*>(s_D + t * LDW + j4) = dv4;
+            *reinterpret_cast<float4*>(s_P + t * LDW + j4) = pv;
+            *reinterpret_cast<float4*>(s_O + t * LDW + j4) = ov;
+        }
+        for (int e = tid; e < DK * SW / 4; e += NTB) {
+            const int i = e / (SW / 4), j4 = 4 * (e % (SW / 4));
+            if (j4 >= SWc) continue;
+            const size_t o = (gh * DK + i) * DV + j0 + j4;
+            *reinterpret_cast<float4*>(s_S + i * LDW + j4) =
+                *reinterpret_cast<const float4*>(a.ckpt + o);
+            *reinterpret_cast<float4*>(s_G + i * LDW + j4) =
+                *reinterpret_cast<const float4*>(a.dso + o);
+        }
+        __syncthreads();
+        for (int ks = 0; ks < SWc / 16; ++ks) {
+            const int kc = 16 * ks + 4 * lg;
+            const FF::V aP = FF::ld(s_P + (16 * rb + li) * LDW + kc);
+            const FF::V aO = FF::ld(s_O + (16 * rb + li) * LDW + kc);
+            const FF::V aD = FF::ld(s_D + (16 * rb + li) * LDW + kc);
+#pragma unroll
+            for (int k = 0; k < NCW; ++k) {
+                const int ct = cw + 2 * k;
+                if (ct < NKT) {
+                    const FF::V bS = FF::ld(s_S + (16 * ct + li) * LDW + kc);
+                    const FF::V bG = FF::ld(s_G + (16 * ct + li) * LDW + kc);
+                    p3[k] = FF::mma(p3[k], aP, bS);
+                    p4[k] = FF::mma(p4[k], aO, bS);
+                    p5[k] = FF::mma(p5[k], aD, bG);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                if (pbo[u]) {
+                    const FF::V bD = FF::ld(s_D + (16 * pbs[u] + li) * LDW + kc);
+                    p1[u] = FF::mma(p1[u], FF::ld(s_O + (16 * pbt[u] + li) * LDW + kc), bD);
+                    p2[u] = FF::mma(p2[u], FF::ld(s_P + (16 * pbt[u] + li) * LDW + kc), bD);
+                }
+        }
+        if (tid < 4 * DK) {
+            const int i = tid >> 2, jq = 8 * (tid & 3);
+            if (jq < SWc)
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj)
+                    p6 = fmaf(s_S[i * LDW + jq + jj], s_G[i * LDW + jq + jj], p6);
+        }
+    }
+    p6 += __shfl_xor(p6, 1, 64);
+    p6 += __shfl_xor(p6, 2, 64);
+    if (tid < 4 * DK && (tid & 3) == 0) s_p6[tid >> 2] = p6;
+    __syncthreads();  // the slabs are dead: the adjoints of B and T over them
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+        if (pbo[u])
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * pbt[u] + 4 * lg + r, s2 = 16 * pbs[u] + li;
+                const float b = s2 <= t ? a.scale * p1[u][r] : 0.f;  // dB = scale dO Delta^T
+                const float tt = s2 < t ? -p2[u][r] : 0.f;            // dT = -Psi Delta^T
+                s_dB[t * LDC + s2] = b;
+                s_dBT[s2 * LDC + t] = b;
+                s_dT[t * LDC + s2] = tt;
+                s_dTT[s2 * LDC + t] = tt;
+            }
+    // terms through S_in (O = scale Qbar S_in, X = V - Kbar S_in) and the tail operand
+    // (S_out = ... + Ktail^T Delta); the chunk-end decay's column sums of kappa dkappa_tail
+    floatx4 gqa[NCW], gka[NCW], gpa[NCW];
+#pragma unroll
+    for (int k = 0; k < NCW; ++k) {
+        gqa[k] = gka[k] = gpa[k] = zero4();
+        const int ct = cw + 2 * k;
+        if (ct >= NKT) continue;
+        const int i = 16 * ct + li;
+        const double lmC = lam[(C - 1) * DK + i];
+        float cs = 0.f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * rb + 4 * lg + r;
+            const double lm = lam[t * DK + i];
+            const float gm = expf((float)lm), et = expf((float)(lmC - lm));
+            gqa[k][r] = a.scale * gm * p4[k][r];
+            gka[k][r] = -gm * p3[k][r];
+            gpa[k][r] = et * p5[k][r];
+            cs = fmaf(kap[t * DK + i], gpa[k][r], cs);
+        }
+        cs += __shfl_xor(cs, 16, 64);
+        cs += __shfl_xor(cs, 32, 64);
+        if (lg == 0) s_cp[rb * DK + i] = cs;
+    }
+
+    // ---- 2. terms through T and B, by channel slabs ------------------------------------------
+    for (int s0 = 0, kk = 0; s0 < DK; s0 += SLB, ++kk) {
+        __syncthreads();  // dB and dT written; the previous slab's operands read
+        // operands, transposed [ii][t]: kappa scaled to the end of its block and to the block's
+        // token 8 (the column side of dq, dk); q and k scaled from the start of their block and
+        // from its token 8 (the column side of dkappa). Thread: channel s0 + ii, tokens
+        // 4 tg .. 4 tg + 3 (one block)
+        if (tid < SLB * 16) {
+            const int ii = tid % SLB, tg = tid / SLB, i = s0 + ii, b = tg >> 2, tb0 = 4 * tg;
+            const double lst = b > 0 ? lam[(16 * b - 1) * DK + i] : 0.0;
+            const double len = lam[(16 * b + 15) * DK + i], lrf = lam[(16 * b + 7) * DK + i];
+            float o[6][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int t = tb0 + u;
+                const bool ok = t < L;
+                const double lm = lam[t * DK + i];
+                const float kp = kap[t * DK + i];
+                const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+                const float kv = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+                const float ast = __expf((float)(lm - lst));
+                const float amd = fminf(__expf((float)(lm - lrf)), RSAT);
+                const float ben = __expf((float)(len - lm));
+                const float bmd = fminf(__expf((float)(lrf - lm)), RSAT);
+                o[0][u] = ben * kp;
+                o[1][u] = bmd * kp;
+                o[2][u] = ast * qq;
+                o[3][u] = amd * qq;
+                o[4][u] = ast * kv;
+                o[5][u] = amd * kv;
+            }
+#pragma unroll
+            for (int m = 0; m < 6; ++m)
+                *reinterpret_cast<float4*>(s_op + m * OPS + ii * LDC + tb0) =
+                    make_float4(o[m][0], o[m][1], o[m][2], o[m][3]);
+        }
+        __syncthreads();
+        if (16 * cw >= SLB) continue;
+        const int i = s0 + 16 * cw + li;
+        const float* oKen = s_op + 0 * OPS + 16 * cw * LDC;
+        const float* oKmd = s_op + 1 * OPS + 16 * cw * LDC;
+        const float* oQst = s_op + 2 * OPS + 16 * cw * LDC;
+        const float* oQmd = s_op + 3 * OPS + 16 * cw * LDC;
+        const float* oKst = s_op + 4 * OPS + 16 * cw * LDC;
+        const float* oKm2 = s_op + 5 * OPS + 16 * cw * LDC;
+        // log-decays of channel i: before, at the end of and at token 8 of every block; rows
+        double lst[4], len[4], lrf[4], lrow[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            lst[b] = b > 0 ? lam[(16 * b - 1) * DK + i] : 0.0;
+            len[b] = lam[(16 * b + 15) * DK + i];
+            lrf[b] = lam[(16 * b + 7) * DK + i];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) lrow[r] = lam[(16 * rb + 4 * lg + r) * DK + i];
+        const int ar = (16 * rb + li) * LDC, kc = 4 * lg;
+        // rows of block rb as the later token: dq += sum_s dB_ts kappa_s R_ts,
+        // dk += sum_s dT_ts kappa_s R_ts
+        {
+            floatx4 oB = zero4(), oT = zero4();
+            for (int jb = 0; jb < rb; ++jb) {
+                const FF::V bk = FF::ld(oKen + li * LDC + 16 * jb + kc);
+                const floatx4 tB = FF::mma(zero4(), FF::ld(s_dB + ar + 16 * jb + kc), bk);
+                const floatx4 tT = FF::mma(zero4(), FF::ld(s_dT + ar + 16 * jb + kc), bk);
+                const float m = __expf((float)(lst[rb] - len[jb]));
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    oB[r] = fmaf(m, tB[r], oB[r]);
+                    oT[r] = fmaf(m, tT[r], oT[r]);
+                }
+            }
+            const FF::V bk = FF::ld(oKmd + li * LDC + 16 * rb + kc);
+            const floatx4 dB = FF::mma(zero4(), FF::ld(s_dB + ar + 16 * rb + kc), bk);
+            const floatx4 dT = FF::mma(zero4(), FF::ld(s_dT + ar + 16 * rb + kc), bk);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float ast = __expf((float)(lrow[r] - lst[rb]));
+                const float amd = fminf(__expf((float)(lrow[r] - lrf[rb])), RSAT);
+                gqa[kk][r] += ast * oB[r] + amd * dB[r];
+                gka[kk][r] += ast * oT[r] + amd * dT[r];
+            }
+        }
+        // rows of block rb as the earlier token: dkappa += sum_t (dB_ts q_t + dT_ts k_t) R_ts
+        {
+            floatx4 oB = zero4(), oT = zero4();
+            for (int ib = rb + 1; ib < 4; ++ib) {
+                const floatx4 tB = FF::mma(zero4(), FF::ld(s_dBT + ar + 16 * ib + kc),
+                                           FF::ld(oQst + li * LDC + 16 * ib + kc));
+                const floatx4 tT = FF::mma(zero4(), FF::ld(s_dTT + ar + 16 * ib + kc),
+                                           FF::ld(oKst + li * LDC + 16 * ib + kc));
+                const float m = __expf((float)(lst[ib] - len[rb]));
+#pragma unroll
+                for (int r = 0; r < 4; ++r) oB[r] = fmaf(m, tB[r] + tT[r], oB[r]);
+            }
+            const floatx4 dB = FF::mma(zero4(), FF::ld(s_dBT + ar + 16 * rb + kc),
+                                       FF::ld(oQmd + li * LDC + 16 * rb + kc));
+            const floatx4 dT = FF::mma(zero4(), FF::ld(s_dTT + ar + 16 * rb + kc),
+                                       FF::ld(oKm2 + li * LDC + 16 * rb + kc));
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float ben = __expf((float)(len[rb] - lrow[r]));
+                const float bmd = fminf(__expf((float)(lrf[rb] - lrow[r])), RSAT);
+                gpa[kk][r] += ben * oB[r] + bmd * (dB[r] + dT[r]);
+            }
+            (void)oT;
+        }
+    }
+
+    // ---- the gradients out; the log-decay adjoint q dq + k dk - kappa dkappa -----------------
+    __syncthreads();  // phase 2 is over: the log-decay adjoint over its buffers
+#pragma unroll
+    for (int k = 0; k < NCW; ++k) {
+        const int ct = cw + 2 * k;
+        if (ct >= NKT) continue;
+        const int i = 16 * ct + li;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * rb + 4 * lg + r;
             const bool ok = t < L;
-            s_D[t * LDV + j] = a.dlt[(gh * C + t) * DV + j0 + j];
-            s_P[t * LDV + j] = ok ? a.dv[row(t) * DV + j0 + j] : 0.f;
-            s_O[t * LDV + j] = (ok && a.dO) ? ld<TI>(a.dO, row(t) * DV + j0 + j) : 0.f;
-        }
-        for (int e = tid; e < DK * SW; e += NTB) {
-            const int i = e / SW, j = e % SW;
-            s_S[i * LDV + j] = a.ckpt[(gh * DK + i) * DV + j0 + j];
-            s_G[i * LDV + j] = a.dso[(gh * DK + i) * DV + j0 + j];
-        }
-        __syncthreads();
-        for (int j = 0; j < SW; ++j) {
-            const float ot = s_O[tr * LDV + j], pt = s_P[tr * LDV + j], dt = s_D[tr * LDV + j];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float ds = s_D[(cl + 8 * e) * LDV + j];
-                p1[e] = fmaf(ot, ds, p1[e]);
-                p2[e] = fmaf(pt, ds, p2[e]);
+            const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+            const float kv = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+            if (ok) {
+                gq[row(t) * DK + i] = gqa[k][r];
+                gk[row(t) * DK + i] = gka[k][r];
             }
-#pragma unroll
-            for (int e = 0; e < Q; ++e) {
-                const float si = s_S[(cl + 8 * e) * LDV + j];
-                p3[e] = fmaf(pt, si, p3[e]);
-                p4[e] = fmaf(ot, si, p4[e]);
-                p5[e] = fmaf(dt, s_G[(cl + 8 * e) * LDV + j], p5[e]);
-            }
+            dkap[t * DK + i] = gpa[k][r];
+            s_dl[t * LDZ + i] = qq * gqa[k][r] + kv * gka[k][r] - kap[t * DK + i] * gpa[k][r];
         }
-        if (tid < DK)
-            for (int j = 0; j < SW; ++j) p6 = fmaf(s_S[tid * LDV + j], s_G[tid * LDV + j], p6);
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int s = cl + 8 * e;
-        s_dB[tr * LDC + s] = s <= tr ? a.scale * p1[e] : 0.f;  // dB = scale dO Delta^T
-        s_dT[tr * LDC + s] = s < tr ? -p2[e] : 0.f;             // dT = -Psi Delta^T
-    }
-    if (tid < DK) s_p6[tid] = p6;
-    // terms through S_in and the tail operand (each entry owned by this thread)
-#pragma unroll
-    for (int e = 0; e < Q; ++e) {
-        const int i = cl + 8 * e, t = tr;
-        const double lm = lam[t * DK + i], lmC = lam[(C - 1) * DK + i];
-        const float gm = expf((float)lm), et = expf((float)(lmC - lm));
-        const bool ok = t < L;
-        const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
-        const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-        const float kp = kap[t * DK + i];
-        const float dq = a.scale * gm * p4[e];  // O = scale Qbar S_in
-        const float dk = -gm * p3[e];           // X = V - Kbar S_in
-        const float dkp = et * p5[e];           // S_out = ... + Ktail^T Delta
-        if (ok) {
-            gq[row(t) * DK + i] = dq;
-            gk[row(t) * DK + i] = dk;
-        }
-        dkap[t * DK + i] = dkp;
-        s_dl[t * LDZ + i] = qq * dq + kk * dk - kp * dkp;
-        s_c[t * LDZ + i] = kp * dkp;
     }
     __syncthreads();
-
-    // ---- terms through T and B (decay ratios from the log-decays), by channel slabs ---------
-    constexpr int EPT = SLB / 8;  // channels per thread in a slab: ii = cl + 8 e
-    for (int s0 = 0; s0 < DK; s0 += SLB) {
-        for (int e = tid; e < C * SLB; e += NTB) {
-            const int t = e / SLB, ii = e % SLB, i = s0 + ii;
-            const bool ok = t < L;
-            s_q[t * LDS_ + ii] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
-            s_k[t * LDS_ + ii] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-            s_kp[t * LDS_ + ii] = kap[t * DK + i];
-            s_l[t * LDS_ + ii] = lam[t * DK + i];
-        }
-        __syncthreads();
-        float dqB[EPT], dkT[EPT], dkpB[EPT], dkpT[EPT];
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) dqB[e] = dkT[e] = dkpB[e] = dkpT[e] = 0.f;
-        // row tr as the later token t: sum over s <= t
-        for (int s = 0; s <= tr; ++s) {
-            const float b = s_dB[tr * LDC + s], tt = s_dT[tr * LDC + s];
-#pragma unroll
-            for (int e = 0; e < EPT; ++e) {
-                const int ii = cl + 8 * e;
-                const float rt = __expf((float)(s_l[tr * LDS_ + ii] - s_l[s * LDS_ + ii]));
-                const float x = s_kp[s * LDS_ + ii] * rt;
-                dqB[e] = fmaf(b, x, dqB[e]);
-                dkT[e] = fmaf(tt, x, dkT[e]);
-            }
-        }
-        // row tr as the earlier token s: sum over t >= s
-        for (int t = tr; t < C; ++t) {
-            const float b = s_dB[t * LDC + tr], tt = s_dT[t * LDC + tr];
-#pragma unroll
-            for (int e = 0; e < EPT; ++e) {
-                const int ii = cl + 8 * e;
-                const float rt = __expf((float)(s_l[t * LDS_ + ii] - s_l[tr * LDS_ + ii]));
-                dkpB[e] = fmaf(b, s_q[t * LDS_ + ii] * rt, dkpB[e]);
-                dkpT[e] = fmaf(tt, s_k[t * LDS_ + ii] * rt, dkpT[e]);
-            }
-        }
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-            const int ii = cl + 8 * e, i = s0 + ii, t = tr;
-            const float dkp = dkpB[e] + dkpT[e];
-            if (t < L) {
-                gq[row(t) * DK + i] += dqB[e];
-                gk[row(t) * DK + i] += dkT[e];
-            }
-            dkap[t * DK + i] += dkp;
-            s_dl[t * LDZ + i] += s_q[t * LDS_ + ii] * dqB[e] + s_k[t * LDS_ + ii] * dkT[e] -
-                                 s_kp[t * LDS_ + ii] * dkp;
-        }
-        __syncthreads();
-    }
 
     // ---- d(log-decay) -> dalpha (memory part): alpha_s dalpha_s = sum_{t >= s} dlambda_t, the
     // chunk-end terms (gamma_C) entering at the last token ---------------------------------------
     if (tid < DK) {  // suffix sums over the chunk, in LDS
         const int i = tid;
         float acc = gC[i] * s_p6[i];
-        for (int t = 0; t < C; ++t) acc += s_c[t * LDZ + i];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) acc += s_cp[b * DK + i];
         for (int t = C - 1; t >= 0; --t) {
             acc += s_dl[t * LDZ + i];
             s_dl[t * LDZ + i] = acc;
