@@ -42,6 +42,11 @@ constexpr int NTH = 256;  // bw_final and the forward's summary kernel
 // bw_prep, the walks and bw_grad hold a whole chunk in LDS (one workgroup per CU): 512 threads
 // put two waves on every SIMD to hide the LDS and memory latency
 constexpr int NTB = 512, NWB = NTB / 64;
+// saturation of the decay factors referenced to a block's token 8 (2^100: beyond the inverse of
+// any 8-token decay above 2^-100)
+constexpr float RSAT = 1.2676506e30f;
+
+using FF = Frag<float, 16>;  // one 16-deep step of a float32 product: four 16 x 16 x 4 MFMAs
 
 // Per (chunk, head) record written by bw_prep.
 template <int DK>
@@ -121,7 +126,7 @@ __device__ __forceinline__ float ld(const void* p, size_t i)
 template <int DK>
 struct PrepLds {
     static constexpr int SLB = DK < 32 ? DK : 32;  // channel slab of the T / B products
-    static constexpr int LDK = DK + 1, LDC = C + 1, LDL = SLB + 1;
+    static constexpr int LDK = DK + 1, LDC = C + 1, LDO = SLB + 4;
     static constexpr size_t SZ_CK = (size_t)C * LDK * 4;
     static constexpr size_t OFF_K = 0;                    // k [C][LDK]
     static constexpr size_t OFF_AQ = OFF_K + SZ_CK;       // alpha, then q [C][LDK]
@@ -132,12 +137,17 @@ struct PrepLds {
     static constexpr size_t OFF_AA = OFF_BETA + C * 4;    // isotropic mean alpha^2 [C]
     static constexpr size_t OFF_NK = OFF_AA + C * 4;      // isotropic ||k||^2 [C]
     static constexpr size_t OFF_W1 = OFF_NK + C * 4;      // isotropic omega [C]
-    static constexpr size_t OFF_LC = al16(OFF_W1 + C * 4);            // lambda_C [DK] double
-    static constexpr size_t OFF_L = al16(OFF_LC + (size_t)DK * 8);    // lambda slab [C][LDL]
-    static constexpr size_t OFF_T = OFF_L + (size_t)C * LDL * 8;      // T [C][LDC]
-    static constexpr size_t OFF_A = OFF_T + (size_t)C * LDC * 4;      // (I + T)^-1 [C][LDC]
-    static constexpr size_t OFF_X = OFF_A + (size_t)C * LDC * 4;      // block products [3][16][17]
-    static constexpr size_t TOTAL = al16(OFF_X + (size_t)3 * 16 * 17 * 4);
+    static constexpr size_t OFF_LC = al16(OFF_W1 + C * 4);             // lambda_C [DK] double
+    static constexpr size_t OFF_MID = al16(OFF_LC + (size_t)DK * 8);   // [3][SLB]
+    // six operand slabs [C][LDO] of the T / B products; afterwards T, (I + T)^-1 [C][LDC] and
+    // the block products [3][16][17] over them
+    static constexpr size_t OFF_OP = al16(OFF_MID + (size_t)3 * SLB * 4);
+    static constexpr size_t SZ_OP = (size_t)C * LDO * 4;
+    static constexpr size_t OFF_T = OFF_OP;
+    static constexpr size_t OFF_A = OFF_T + (size_t)C * LDC * 4;
+    static constexpr size_t OFF_X = OFF_A + (size_t)C * LDC * 4;
+    static constexpr size_t TOTAL =
+        al16(cmax(OFF_OP + 6 * SZ_OP, OFF_X + (size_t)3 * 16 * 17 * 4));
 };
 
 template <class TI, int DK, int VARIANT, bool APC>
@@ -146,7 +156,7 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
     using R = BwRec<DK>;
     using LY = PrepLds<DK>;
     constexpr bool DIAG = VARIANT == 0;
-    constexpr int SLB = LY::SLB, LDK = LY::LDK, LDC = LY::LDC, LDL = LY::LDL;
+    constexpr int SLB = LY::SLB, LDK = LY::LDK, LDC = LY::LDC, LDO = LY::LDO;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_k = (float*)(smem + LY::OFF_K);
     float* s_aq = (float*)(smem + LY::OFF_AQ);
@@ -158,7 +168,8 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
     float* s_nk = (float*)(smem + LY::OFF_NK);
     float* s_w1 = (float*)(smem + LY::OFF_W1);
     double* s_lc = (double*)(smem + LY::OFF_LC);
-    double* s_l = (double*)(smem + LY::OFF_L);
+    float* s_mid = (float*)(smem + LY::OFF_MID);
+    float* s_op = (float*)(smem + LY::OFF_OP);
     float* s_T = (float*)(smem + LY::OFF_T);
     float* s_A = (float*)(smem + LY::OFF_A);
     float* s_X = (float*)(smem + LY::OFF_X);
@@ -296,37 +307,98 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
     }
     __syncthreads();
 
-    // ---- T (s < t) and B (s <= t), channel slab by channel slab; thread: row t, 16 columns s
-    float accT[8], accB[8];
+    // ---- T (s < t) and B (s <= t) by 16 x 16 blocks on float32 MFMA, contracting over channel
+    // slabs. The decay ratio R_ts,i = gamma_t,i / gamma_s,i splits per block pair: for blocks
+    // b > c, the decay from the start of block b to t (row side), over the blocks between them
+    // (a per-channel factor on the column side) and from s to the end of block c (column side),
+    // each <= 1; inside a diagonal block both sides are referenced to its token 8 (a factor
+    // saturates at 2^100). Wave w computes T and B of the lower blocks w and w + 8 of the ten.
+    const int li = lane & 15, lg = lane >> 4;
+    int pbt[2], pbs[2];
+    bool pbo[2];
+    floatx4 accT[2], accB[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) accT[e] = accB[e] = 0.f;
-    const int tr = tid >> 3, cl = tid & 7;  // row tr; columns s = cl + 8 e
+    for (int u = 0; u < 2; ++u) {
+        const int q = w + 8 * u;
+        pbo[u] = q < 10;
+        pbt[u] = q < 1 ? 0 : (q < 3 ? 1 : (q < 6 ? 2 : 3));
+        pbs[u] = q - pbt[u] * (pbt[u] + 1) / 2;
+        accT[u] = accB[u] = zero4();
+    }
     for (int s0 = 0; s0 < DK; s0 += SLB) {
-        for (int e = tid; e < C * SLB; e += NTB) {
-            const int t = e / SLB, ii = e % SLB;
-            s_l[t * LDL + ii] = lam[t * DK + s0 + ii];
+        // operands of channels s0 .. s0 + SLB - 1, row-major [t][ii]: k, q scaled from the start
+        // of their block and from its token 8; kappa scaled to the end of its block and to its
+        // token 8. Thread: token tid / 8, four channels
+        for (int e = tid; e < C * SLB / 4; e += NTB) {
+            const int t = e / (SLB / 4), i4 = 4 * (e % (SLB / 4)), b = t >> 4;
+            float o[6][4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = s0 + i4 + u;
+                const double lm = lam[t * DK + i];
+                const double lst = b > 0 ? lam[(16 * b - 1) * DK + i] : 0.0;
+                const double len = lam[(16 * b + 15) * DK + i], lrf = lam[(16 * b + 7) * DK + i];
+                const float ast = __expf((float)(lm - lst));
+                const float amd = fminf(__expf((float)(lm - lrf)), RSAT);
+                const float ben = __expf((float)(len - lm));
+                const float bmd = fminf(__expf((float)(lrf - lm)), RSAT);
+                const float kk = s_k[t * LDK + i], qq = s_aq[t * LDK + i], kp = s_wp[t * LDK + i];
+                o[0][u] = ast * kk;
+                o[1][u] = ast * qq;
+                o[2][u] = ben * kp;
+                o[3][u] = amd * kk;
+                o[4][u] = amd * qq;
+                o[5][u] = bmd * kp;
+            }
+#pragma unroll
+            for (int m = 0; m < 6; ++m)
+                *reinterpret_cast<float4*>(s_op + m * (C * LDO) + t * LDO + i4) =
+                    make_float4(o[m][0], o[m][1], o[m][2], o[m][3]);
+        }
+        // decay over the blocks between two blocks two or three apart: (2, 0), (3, 0), (3, 1)
+        if (tid < 3 * SLB) {
+            const int pr = tid / SLB, i = s0 + tid % SLB;
+            const int bt = pr == 0 ? 2 : 3, bs = pr == 2 ? 1 : 0;
+            s_mid[tid] = __expf((float)(lam[(16 * bt - 1) * DK + i] - lam[(16 * bs + 15) * DK + i]));
         }
         __syncthreads();
-#pragma unroll 1
-        for (int ii = 0; ii < SLB; ++ii) {
-            const double lt = s_l[tr * LDL + ii];
-            const float qt = s_aq[tr * LDK + s0 + ii], kt = s_k[tr * LDK + s0 + ii];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int s = cl + 8 * e;
-                const float rt = s <= tr ? __expf((float)(lt - s_l[s * LDL + ii])) : 0.f;
-                const float x = s_wp[s * LDK + s0 + ii] * rt;
-                accB[e] = fmaf(qt, x, accB[e]);
-                accT[e] = fmaf(kt, x, accT[e]);
+        for (int u = 0; u < 2; ++u) {
+            if (!pbo[u]) continue;
+            const int tb = pbt[u], sb = pbs[u], dg = tb == sb;
+            const float* oK = s_op + (dg ? 3 : 0) * (C * LDO) + 16 * tb * LDO;
+            const float* oQ = s_op + (dg ? 4 : 1) * (C * LDO) + 16 * tb * LDO;
+            const float* oP = s_op + (dg ? 5 : 2) * (C * LDO) + 16 * sb * LDO;
+            const int pm = tb - sb < 2 ? -1 : (tb == 2 ? 0 : (sb == 0 ? 1 : 2));
+#pragma unroll
+            for (int ks = 0; ks < SLB / 16; ++ks) {
+                const int kc = 16 * ks + 4 * lg;
+                FF::V bp = FF::ld(oP + li * LDO + kc);
+                if (pm >= 0) bp = FF::scale(bp, s_mid + pm * SLB + kc);
+                accT[u] = FF::mma(accT[u], FF::ld(oK + li * LDO + kc), bp);
+                accB[u] = FF::mma(accB[u], FF::ld(oQ + li * LDO + kc), bp);
             }
         }
         __syncthreads();
     }
+    // T and B out (the operand slabs are dead): lower blocks from the products, masked inside
+    // the diagonal blocks; zeros above
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int s = cl + 8 * e;
-        Bm[tr * C + s] = s <= tr ? accB[e] : 0.f;
-        s_T[tr * LDC + s] = s < tr ? accT[e] : 0.f;
+    for (int u = 0; u < 2; ++u) {
+        if (!pbo[u]) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * pbt[u] + 4 * lg + r, s2 = 16 * pbs[u] + li;
+            Bm[t * C + s2] = s2 <= t ? accB[u][r] : 0.f;
+            s_T[t * LDC + s2] = s2 < t ? accT[u][r] : 0.f;
+        }
+    }
+    for (int e = tid; e < 6 * 256; e += NTB) {  // the six blocks above the diagonal
+        const int q = e >> 8, tb = q < 3 ? 0 : (q < 5 ? 1 : 2);
+        const int sb = tb + 1 + (q - (tb == 0 ? 0 : (tb == 1 ? 3 : 5)));
+        const int t = 16 * tb + ((e >> 4) & 15), s2 = 16 * sb + (e & 15);
+        Bm[t * C + s2] = 0.f;
+        s_T[t * LDC + s2] = 0.f;
     }
     for (int e = tid; e < C * C; e += NTB) s_A[(e / C) * LDC + e % C] = 0.f;
     __syncthreads();
@@ -403,7 +475,6 @@ struct WalkLds {
     static constexpr size_t TOTAL = cmax(F_TOTAL, R_TOTAL);
 };
 
-using FF = Frag<float, 16>;  // one 16-deep step of a float32 product: four 16 x 16 x 4 MFMAs
 
 // acc += A[ar0 + 16 rows][k0 .. k0 + 16 * nk) * B[k][br0 + 16 columns], A row-major (lda), B
 // stored transposed (row = output column, ldb), k-steps ks0 .. ks1 - 1 of 16
@@ -685,8 +756,6 @@ struct GradLds {
     static constexpr size_t OFF_P6 = OFF_CP + (size_t)4 * DK * 4;  // [DK]
     static constexpr size_t TOTAL = al16(OFF_P6 + (size_t)DK * 4);
 };
-
-constexpr float RSAT = 1.2676506e30f;  // 2^100
 
 template <class TI, int DK, int VARIANT, bool APC>
 __global__ __launch_bounds__(NTB) void bw_grad(Args a)
