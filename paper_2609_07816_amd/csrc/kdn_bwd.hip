@@ -459,7 +459,8 @@ struct WalkLds {
     static constexpr size_t F_XT = F_A + (size_t)C * LDC * 4;              // X^T [BVM][LDC]
     static constexpr size_t F_DT = F_XT + (size_t)BVM * LDC * 4;           // Delta^T
     static constexpr size_t F_GC = F_DT + (size_t)BVM * LDC * 4;           // gamma_C [DK]
-    static constexpr size_t F_TOTAL = al16(F_GC + (size_t)DK * 4);
+    static constexpr size_t F_V = al16(F_GC + (size_t)DK * 4);             // V [C][BVM + 1]
+    static constexpr size_t F_TOTAL = al16(F_V + (size_t)C * (BVM + 1) * 4);
     // reverse walk
     static constexpr size_t R_ST = 0;                                      // dS^T [BVM][LDK]
     static constexpr size_t R_BT = R_ST + (size_t)BVM * LDK * 4;           // B^T [C][LDC]
@@ -492,12 +493,37 @@ __device__ __forceinline__ floatx4 mfma_rows(floatx4 acc, const float* A, int ld
     return acc;
 }
 
+// Block -> (sequence-head slot, value tile): the NV tiles of one head get block indices
+// congruent modulo 8, so round-robin dispatch puts them on one XCD, where they share the L2 copy
+// of the head's chunk records. The grid is padded to a multiple of 8 slots.
+__device__ __forceinline__ bool walk_slot(const Args& a, int NV, int& slot, int& vt)
+{
+    const int xcd = (int)(blockIdx.x % 8), rest = (int)(blockIdx.x / 8);
+    vt = rest % NV;
+    slot = (rest / NV) * 8 + xcd;
+    return slot < a.cm.N * a.H;
+}
+
+// Pieces of a chunk's operands each thread moves: float4 pieces of a [C][DK] and a [C][C]
+// matrix, values of a [C][32] value tile.
+template <int DK>
+struct WalkPieces {
+    static constexpr int NK4 = C * DK / 4, PK = (NK4 + NTB - 1) / NTB;
+    static constexpr int NC4 = C * C / 4, PC = NC4 / NTB;
+    static constexpr int PV = C * WalkLds<DK>::BVM / NTB;
+    static_assert(NC4 % NTB == 0 && (C * WalkLds<DK>::BVM) % NTB == 0, "whole pieces");
+};
+
+// The operands of chunk ci + 1 (fwalk) or ci - 1 (rwalk) are loaded into registers while chunk
+// ci is computed, and stored to LDS after the barrier that ends it.
 template <class TI, int DK>
 __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
-    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16;
+    using WP = WalkPieces<DK>;
+    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16, BVM = LY::BVM, LDV = BVM + 1;
+    constexpr int PK = WP::PK, PC = WP::PC, PV = WP::PV, NK4 = WP::NK4;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_St = (float*)(smem + LY::F_ST);
     float* s_kb = (float*)(smem + LY::F_KB);
@@ -506,10 +532,11 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
     float* s_XT = (float*)(smem + LY::F_XT);
     float* s_DT = (float*)(smem + LY::F_DT);
     float* s_gc = (float*)(smem + LY::F_GC);
+    float* s_V = (float*)(smem + LY::F_V);
 
     const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJT = BV / 16;
-    const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
-    if (slot >= a.cm.N * H) return;
+    int slot, vt;
+    if (!walk_slot(a, NV, slot, vt)) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, li = lane & 15, lg = lane >> 4;
     float* __restrict__ ckpt = a.ckpt;
@@ -521,34 +548,67 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
         const int i = e / BV, j = e % BV;
         s_St[j * LDK + i] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
-    for (int ci = 0; ci < nch; ++ci) {
-        const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
-        const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
-        const size_t gh = (size_t)g * H + h;
-        const float* __restrict__ kbar = (const float*)(rec + R::OFF_KBAR);
-        const float* __restrict__ ktl = (const float*)(rec + R::OFF_KTL);
-        const float* __restrict__ Am = (const float*)(rec + R::OFF_A);
-        const float* __restrict__ gC = (const float*)(rec + R::OFF_GC);
-        __syncthreads();
-        for (int e = tid; e < DK * BV; e += NTB) {  // checkpoint: S_in of this chunk
-            const int i = e / BV, j = e % BV;
-            ckpt[(gh * DK + i) * DV + j0 + j] = s_St[j * LDK + i];
+    floatx4 kb4[PK], kt4[PK], am4[PC];
+    float vv[PV], gcv = 0.f;
+    auto load = [&](int ci) __attribute__((always_inline)) {
+        const int c0 = t0 + ci * C, L = min(C, t1 - c0);
+        const char* rec = a.rec + ((size_t)(g0 + ci) * H + h) * R::BYTES;
+        const floatx4* kbar = (const floatx4*)(rec + R::OFF_KBAR);
+        const floatx4* ktl = (const floatx4*)(rec + R::OFF_KTL);
+        const floatx4* Am = (const floatx4*)(rec + R::OFF_A);
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+            const int e = min(tid + NTB * u, NK4 - 1);
+            kb4[u] = kbar[e];
+            kt4[u] = ktl[e];
         }
-        for (int e = tid; e < C * DK / 4; e += NTB) {
-            const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
-            *reinterpret_cast<float4*>(s_kb + t * LDK + i4) =
-                *reinterpret_cast<const float4*>(kbar + (size_t)t * DK + i4);
+#pragma unroll
+        for (int u = 0; u < PC; ++u) am4[u] = Am[tid + NTB * u];
+        if (tid < DK) gcv = ((const float*)(rec + R::OFF_GC))[tid];
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {  // rows past the end of the sequence read as zeros
+            const int e = tid + NTB * u, t = e / BVM, j = e % BVM;
+            vv[u] = (t < L && j < BV) ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
+                                      : 0.f;
         }
-        for (int e = tid; e < C * DK; e += NTB) {  // Ktail^T: coalesced reads, transposed writes
-            const int t = e / DK, i = e % DK;
-            s_ktT[i * LDC + t] = ktl[e];
+    };
+    auto store = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+            const int e = tid + NTB * u;
+            if (e < NK4) {
+                const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
+                *reinterpret_cast<floatx4*>(s_kb + t * LDK + i4) = kb4[u];
+                s_ktT[(i4 + 0) * LDC + t] = kt4[u][0];  // Ktail^T
+                s_ktT[(i4 + 1) * LDC + t] = kt4[u][1];
+                s_ktT[(i4 + 2) * LDC + t] = kt4[u][2];
+                s_ktT[(i4 + 3) * LDC + t] = kt4[u][3];
+            }
         }
-        for (int e = tid; e < C * C / 4; e += NTB) {
-            const int t = e / (C / 4), s4 = 4 * (e % (C / 4));
-            *reinterpret_cast<float4*>(s_A + t * LDC + s4) =
-                *reinterpret_cast<const float4*>(Am + (size_t)t * C + s4);
+#pragma unroll
+        for (int u = 0; u < PC; ++u) {
+            const int e = tid + NTB * u, t = e / (C / 4), s4 = 4 * (e % (C / 4));
+            *reinterpret_cast<floatx4*>(s_A + t * LDC + s4) = am4[u];
         }
-        for (int e = tid; e < DK; e += NTB) s_gc[e] = gC[e];
+        if (tid < DK) s_gc[tid] = gcv;
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {
+            const int e = tid + NTB * u;
+            s_V[(e / BVM) * LDV + e % BVM] = vv[u];
+        }
+    };
+    for (int ci = -1; ci < nch; ++ci) {  // ci = -1: only the first chunk's loads
+        const size_t gh = (size_t)(g0 + ci) * H + h;
+        if (ci >= 0) {
+            __syncthreads();
+            for (int e = tid; e < DK * BV; e += NTB) {  // checkpoint: S_in of this chunk
+                const int i = e / BV, j = e % BV;
+                ckpt[(gh * DK + i) * DV + j0 + j] = s_St[j * LDK + i];
+            }
+            store();
+        }
+        if (ci + 1 < nch) load(ci + 1);
+        if (ci < 0) continue;
         __syncthreads();
         // X = V - Kbar S_in (tile: rows 16 tb, columns 16 jb); stored as X^T
         for (int tile = w; tile < 4 * NJT; tile += NWB) {
@@ -558,12 +618,8 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
                             lane);
             float x[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int t = 16 * tb + 4 * lg + r;
-                const float vv =
-                    t < L ? ld<TI>(a.v, ((size_t)(c0 + t) * H + h) * DV + j0 + 16 * jb + li) : 0.f;
-                x[r] = vv - acc[r];
-            }
+            for (int r = 0; r < 4; ++r)
+                x[r] = s_V[(16 * tb + 4 * lg + r) * LDV + 16 * jb + li] - acc[r];
             *reinterpret_cast<float4*>(s_XT + (16 * jb + li) * LDC + 16 * tb + 4 * lg) =
                 make_float4(x[0], x[1], x[2], x[3]);
         }
@@ -602,7 +658,9 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
 {
     using R = BwRec<DK>;
     using LY = WalkLds<DK>;
-    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16;
+    using WP = WalkPieces<DK>;
+    constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16, BVM = LY::BVM;
+    constexpr int PK = WP::PK, PC = WP::PC, PV = WP::PV, NK4 = WP::NK4;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_dST = (float*)(smem + LY::R_ST);
     float* s_BT = (float*)(smem + LY::R_BT);
@@ -616,8 +674,8 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
     float* s_kT = (float*)(smem + LY::R_R2);   // Kbar^T [DK][LDC]
 
     const int H = a.H, DV = a.DV, BV = a.BV, NV = DV / BV, NJT = BV / 16;
-    const int slot = (int)(blockIdx.x / NV), vt = (int)(blockIdx.x % NV);
-    if (slot >= a.cm.N * H) return;
+    int slot, vt;
+    if (!walk_slot(a, NV, slot, vt)) return;
     const int n = slot / H, h = slot % H, j0 = vt * BV;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, li = lane & 15, lg = lane >> 4;
     float* __restrict__ dso = a.dso;
@@ -629,38 +687,103 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
         const int i = e / BV, j = e % BV;
         s_dST[j * LDK + i] = a.dS_T ? a.dS_T[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
+    // first group: Ktail, B, A, gamma_C, scale dO (stored at the chunk's start); second group:
+    // Qbar, Kbar (stored over Ktail once it is read)
+    floatx4 kt4[PK], bm4[PC], am4[PC], qb4[PK], kb4[PK];
+    float ov[PV], gcv = 0.f;
+    auto rec_of = [&](int ci) { return a.rec + ((size_t)(g0 + ci) * H + h) * R::BYTES; };
+    auto load1 = [&](int ci) __attribute__((always_inline)) {
+        const int c0 = t0 + ci * C, L = min(C, t1 - c0);
+        const char* rec = rec_of(ci);
+        const floatx4* ktl = (const floatx4*)(rec + R::OFF_KTL);
+        const floatx4* Am = (const floatx4*)(rec + R::OFF_A);
+        const floatx4* Bm = (const floatx4*)(rec + R::OFF_B);
+#pragma unroll
+        for (int u = 0; u < PK; ++u) kt4[u] = ktl[min(tid + NTB * u, NK4 - 1)];
+#pragma unroll
+        for (int u = 0; u < PC; ++u) {
+            am4[u] = Am[tid + NTB * u];
+            bm4[u] = Bm[tid + NTB * u];
+        }
+        if (tid < DK) gcv = ((const float*)(rec + R::OFF_GC))[tid];
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {
+            const int e = tid + NTB * u, t = e / BVM, j = e % BVM;
+            ov[u] = (t < L && j < BV && a.dO)
+                        ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
+                        : 0.f;
+        }
+    };
+    auto store1 = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+            const int e = tid + NTB * u;
+            if (e < NK4) {
+                const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
+                *reinterpret_cast<floatx4*>(s_kt + t * LDK + i4) = kt4[u];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < PC; ++u) {  // B^T and A^T
+            const int e = tid + NTB * u, t = e / (C / 4), s4 = 4 * (e % (C / 4));
+            s_BT[(s4 + 0) * LDC + t] = bm4[u][0];
+            s_BT[(s4 + 1) * LDC + t] = bm4[u][1];
+            s_BT[(s4 + 2) * LDC + t] = bm4[u][2];
+            s_BT[(s4 + 3) * LDC + t] = bm4[u][3];
+            s_AT[(s4 + 0) * LDC + t] = am4[u][0];
+            s_AT[(s4 + 1) * LDC + t] = am4[u][1];
+            s_AT[(s4 + 2) * LDC + t] = am4[u][2];
+            s_AT[(s4 + 3) * LDC + t] = am4[u][3];
+        }
+        if (tid < DK) s_gc[tid] = gcv;
+#pragma unroll
+        for (int u = 0; u < PV; ++u) {  // scale dO, transposed
+            const int e = tid + NTB * u;
+            s_OT[(e % BVM) * LDC + e / BVM] = ov[u];
+        }
+    };
+    auto load2 = [&](int ci) __attribute__((always_inline)) {
+        const char* rec = rec_of(ci);
+        const floatx4* qbar = (const floatx4*)(rec + R::OFF_QBAR);
+        const floatx4* kbar = (const floatx4*)(rec + R::OFF_KBAR);
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+            const int e = min(tid + NTB * u, NK4 - 1);
+            qb4[u] = qbar[e];
+            kb4[u] = kbar[e];
+        }
+    };
+    auto store2 = [&]() __attribute__((always_inline)) {  // Qbar^T and Kbar^T
+#pragma unroll
+        for (int u = 0; u < PK; ++u) {
+            const int e = tid + NTB * u;
+            if (e < NK4) {
+                const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
+                s_qT[(i4 + 0) * LDC + t] = qb4[u][0];
+                s_qT[(i4 + 1) * LDC + t] = qb4[u][1];
+                s_qT[(i4 + 2) * LDC + t] = qb4[u][2];
+                s_qT[(i4 + 3) * LDC + t] = qb4[u][3];
+                s_kT[(i4 + 0) * LDC + t] = kb4[u][0];
+                s_kT[(i4 + 1) * LDC + t] = kb4[u][1];
+                s_kT[(i4 + 2) * LDC + t] = kb4[u][2];
+                s_kT[(i4 + 3) * LDC + t] = kb4[u][3];
+            }
+        }
+    };
+    if (nch > 0) {
+        load1(nch - 1);
+        load2(nch - 1);
+    }
     for (int ci = nch - 1; ci >= 0; --ci) {
-        const int g = g0 + ci, c0 = t0 + ci * C, L = min(C, t1 - c0);
-        const char* rec = a.rec + ((size_t)g * H + h) * R::BYTES;
-        const size_t gh = (size_t)g * H + h;
-        const float* __restrict__ ktl = (const float*)(rec + R::OFF_KTL);
-        const float* __restrict__ Am = (const float*)(rec + R::OFF_A);
-        const float* __restrict__ Bm = (const float*)(rec + R::OFF_B);
-        const float* __restrict__ gC = (const float*)(rec + R::OFF_GC);
-        const float* __restrict__ qbar = (const float*)(rec + R::OFF_QBAR);
-        const float* __restrict__ kbar = (const float*)(rec + R::OFF_KBAR);
+        const int c0 = t0 + ci * C, L = min(C, t1 - c0);
+        const size_t gh = (size_t)(g0 + ci) * H + h;
         __syncthreads();
         for (int e = tid; e < DK * BV; e += NTB) {  // dS_out of this chunk
             const int i = e / BV, j = e % BV;
             dso[(gh * DK + i) * DV + j0 + j] = s_dST[j * LDK + i];
         }
-        for (int e = tid; e < C * DK / 4; e += NTB) {
-            const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
-            *reinterpret_cast<float4*>(s_kt + t * LDK + i4) =
-                *reinterpret_cast<const float4*>(ktl + (size_t)t * DK + i4);
-        }
-        for (int e = tid; e < C * C; e += NTB) {  // B^T and A^T
-            const int t = e / C, s2 = e % C;
-            s_BT[s2 * LDC + t] = Bm[e];
-            s_AT[s2 * LDC + t] = Am[e];
-        }
-        for (int e = tid; e < DK; e += NTB) s_gc[e] = gC[e];
-        for (int e = tid; e < C * BV; e += NTB) {  // scale dO, transposed
-            const int t = e / BV, j = e % BV;
-            s_OT[j * LDC + t] = (t < L && a.dO)
-                                    ? a.scale * ld<TI>(a.dO, ((size_t)(c0 + t) * H + h) * DV + j0 + j)
-                                    : 0.f;
-        }
+        store1();
+        if (ci > 0) load1(ci - 1);
         __syncthreads();
         // dDelta = B^T (scale dO) + Ktail dS_out (tile: rows 16 sb, columns 16 jb), stored
         // transposed; B^T is upper triangular: k-steps from the row tile on
@@ -690,11 +813,8 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
             }
         }
         __syncthreads();
-        for (int e = tid; e < C * DK; e += NTB) {  // Qbar^T and Kbar^T over the Ktail area
-            const int t = e / DK, i = e % DK;
-            s_qT[i * LDC + t] = qbar[e];
-            s_kT[i * LDC + t] = kbar[e];
-        }
+        store2();
+        if (ci > 0) load2(ci - 1);
         __syncthreads();
         // dS_in^T = dS_out^T diag(gamma_C) + (scale dO)^T Qbar - Psi^T Kbar
         for (int tile = w; tile < NJT * NKT; tile += NWB) {
@@ -1336,7 +1456,7 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     const int NV = bc.dv / a.BV;
-    const dim3 wgrid((unsigned)((size_t)sa.N * sa.H * NV));
+    const dim3 wgrid((unsigned)(((size_t)sa.N * sa.H + 7) / 8 * 8 * NV));
     hipLaunchKernelGGL((bw_fwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::F_TOTAL, st, a);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL((bw_rwalk<TI, DK>), wgrid, dim3(NTB), WalkLds<DK>::R_TOTAL, st, a);
