@@ -861,7 +861,7 @@ template <int DK>
 struct GradLds {
     static constexpr int SW = 32, LDW = SW + 4;     // value slab, rows padded to 16 bytes
     static constexpr int SLB = DK < 32 ? DK : 32;   // channel slab of phase 2
-    static constexpr int LDC = C + 4, LDZ = DK + 1;
+    static constexpr int LDC = C + 4;
     // phase 1: Delta, Psi, dO [C][LDW]; S_in, dS_out [DK][LDW]
     static constexpr size_t P_D = 0, P_P = (size_t)C * LDW * 4, P_O = 2 * P_P;
     static constexpr size_t P_S = 3 * P_P, P_G = P_S + (size_t)DK * LDW * 4;
@@ -870,11 +870,12 @@ struct GradLds {
     static constexpr size_t CC = (size_t)C * LDC * 4, OPS = (size_t)SLB * LDC;
     static constexpr size_t Q_DB = 0, Q_DT = CC, Q_DBT = 2 * CC, Q_DTT = 3 * CC, Q_OP = 4 * CC;
     static constexpr size_t Q_END = Q_OP + 6 * OPS * 4;
-    // then the log-decay adjoint [C][LDZ] (over phase 2)
-    static constexpr size_t MAIN = cmax(cmax(P_END, Q_END), (size_t)C * LDZ * 4);
+    static constexpr size_t MAIN = cmax(P_END, Q_END);
     static constexpr size_t OFF_CP = al16(MAIN);                   // column sums [4][DK]
     static constexpr size_t OFF_P6 = OFF_CP + (size_t)4 * DK * 4;  // [DK]
-    static constexpr size_t TOTAL = al16(OFF_P6 + (size_t)DK * 4);
+    static constexpr size_t OFF_BT = OFF_P6 + (size_t)DK * 4;      // block totals [4][DK]
+    static constexpr size_t OFF_RP = OFF_BT + (size_t)4 * DK * 4;  // row sums [2][3][C]
+    static constexpr size_t TOTAL = al16(OFF_RP + (size_t)6 * C * 4);
 };
 
 template <class TI, int DK, int VARIANT, bool APC>
@@ -883,7 +884,7 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     using R = BwRec<DK>;
     using LY = GradLds<DK>;
     constexpr bool DIAG = VARIANT == 0;
-    constexpr int SW = LY::SW, LDW = LY::LDW, SLB = LY::SLB, LDC = LY::LDC, LDZ = LY::LDZ;
+    constexpr int SW = LY::SW, LDW = LY::LDW, SLB = LY::SLB, LDC = LY::LDC;
     constexpr int NKT = DK / 16, NCW = (NKT + 1) / 2;  // channel tiles; owned per wave
     constexpr size_t OPS = LY::OPS;
     constexpr int NCHAN = DIAG ? DK : 1;
@@ -898,9 +899,10 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     float* s_dBT = (float*)(smem + LY::Q_DBT);
     float* s_dTT = (float*)(smem + LY::Q_DTT);
     float* s_op = (float*)(smem + LY::Q_OP);  // [6][SLB][LDC]
-    float* s_dl = (float*)smem;               // [C][LDZ]
     float* s_cp = (float*)(smem + LY::OFF_CP);
     float* s_p6 = (float*)(smem + LY::OFF_P6);
+    float* s_bt = (float*)(smem + LY::OFF_BT);
+    float* s_rp = (float*)(smem + LY::OFF_RP);
 
     const int H = a.H, DV = a.DV;
     const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
@@ -940,35 +942,59 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
         p1[u] = p2[u] = zero4();
     }
     float p6 = 0.f;  // thread: channel tid / 4, columns 8 (tid % 4) .. + 7 of each slab
+    // slab pieces of 4 columns, loaded into registers one slab ahead: Delta, Psi, dO (one piece
+    // of each per thread), S_in and dS_out (NP2 pieces)
+    constexpr int NP2 = DK * SW / 4, PP2 = (NP2 + NTB - 1) / NTB;
+    static_assert(C * SW / 4 == NTB, "one row piece per thread");
+    floatx4 vd, vp, vo, vs[PP2], vg[PP2];
+    auto load1 = [&](int j0) {
+        const int SWc = min(SW, DV - j0);
+        const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+        {
+            const int t = tid / (SW / 4), j4 = 4 * (tid % (SW / 4));
+            const bool in = j4 < SWc, ok = in && t < L;
+            const size_t o = row(t) * DV + j0 + j4;
+            vd = in ? *reinterpret_cast<const floatx4*>(a.dlt + (gh * C + t) * DV + j0 + j4) : z;
+            vp = ok ? *reinterpret_cast<const floatx4*>(a.dv + o) : z;
+            floatx4 ov = z;
+            if (ok && a.dO) {
+                ov[0] = ld<TI>(a.dO, o);
+                ov[1] = ld<TI>(a.dO, o + 1);
+                ov[2] = ld<TI>(a.dO, o + 2);
+                ov[3] = ld<TI>(a.dO, o + 3);
+            }
+            vo = ov;
+        }
+#pragma unroll
+        for (int u = 0; u < PP2; ++u) {
+            const int e = min(tid + NTB * u, NP2 - 1), i = e / (SW / 4), j4 = 4 * (e % (SW / 4));
+            const size_t o = (gh * DK + i) * DV + j0 + j4;
+            vs[u] = j4 < SWc ? *reinterpret_cast<const floatx4*>(a.ckpt + o) : z;
+            vg[u] = j4 < SWc ? *reinterpret_cast<const floatx4*>(a.dso + o) : z;
+        }
+    };
+    auto store1 = [&]() {
+        {
+            const int t = tid / (SW / 4), j4 = 4 * (tid % (SW / 4));
+            *reinterpret_cast<floatx4*>(s_D + t * LDW + j4) = vd;
+            *reinterpret_cast<floatx4*>(s_P + t * LDW + j4) = vp;
+            *reinterpret_cast<floatx4*>(s_O + t * LDW + j4) = vo;
+        }
+#pragma unroll
+        for (int u = 0; u < PP2; ++u) {
+            const int e = tid + NTB * u, i = e / (SW / 4), j4 = 4 * (e % (SW / 4));
+            if (e < NP2) {
+                *reinterpret_cast<floatx4*>(s_S + i * LDW + j4) = vs[u];
+                *reinterpret_cast<floatx4*>(s_G + i * LDW + j4) = vg[u];
+            }
+        }
+    };
+    load1(0);
     for (int j0 = 0; j0 < DV; j0 += SW) {
         const int SWc = min(SW, DV - j0);  // 16 or 32
         __syncthreads();
-        for (int e = tid; e < C * SW / 4; e += NTB) {
-            const int t = e / (SW / 4), j4 = 4 * (e % (SW / 4));
-            if (j4 >= SWc) continue;
-            const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-            float4 pv = z, ov = z;
-            const float4 dv4 = *reinterpret_cast<const float4*>(a.dlt + (gh * C + t) * DV + j0 + j4);
-            if (t < L) {
-                const size_t o = row(t) * DV + j0 + j4;
-                pv = *reinterpret_cast<const float4*>(a.dv + o);
-                if (a.dO)
-                    ov = make_float4(ld<TI>(a.dO, o), ld<TI>(a.dO, o + 1), ld<TI>(a.dO, o + 2),
-                                     ld<TI>(a.dO, o + 3));
-            }
-            *reinterpret_cast<float4*>(s_D + t * LDW + j4) = dv4;
-            *reinterpret_cast<float4*>(s_P + t * LDW + j4) = pv;
-            *reinterpret_cast<float4*>(s_O + t * LDW + j4) = ov;
-        }
-        for (int e = tid; e < DK * SW / 4; e += NTB) {
-            const int i = e / (SW / 4), j4 = 4 * (e % (SW / 4));
-            if (j4 >= SWc) continue;
-            const size_t o = (gh * DK + i) * DV + j0 + j4;
-            *reinterpret_cast<float4*>(s_S + i * LDW + j4) =
-                *reinterpret_cast<const float4*>(a.ckpt + o);
-            *reinterpret_cast<float4*>(s_G + i * LDW + j4) =
-                *reinterpret_cast<const float4*>(a.dso + o);
-        }
+        store1();
+        if (j0 + SW < DV) load1(j0 + SW);
         __syncthreads();
         for (int ks = 0; ks < SWc / 16; ++ks) {
             const int kc = 16 * ks + 4 * lg;
@@ -1046,40 +1072,53 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     }
 
     // ---- 2. terms through T and B, by channel slabs ------------------------------------------
+    // formation inputs of a slab, loaded into registers one slab ahead. Thread: channel
+    // s0 + tid % SLB, tokens 4 (tid / SLB) .. + 3 (one block)
+    const bool fth = tid < SLB * 16;
+    const int fii = tid % SLB, ftg = min(tid / SLB, 15), fb = ftg >> 2, ft0 = 4 * ftg;
+    double flm[4], fst = 0.0, fen = 0.0, frf = 0.0;
+    float fkp[4], fq[4], fk[4];
+    auto load2 = [&](int s0) {
+        const int i = s0 + fii;
+        fst = fb > 0 ? lam[(16 * fb - 1) * DK + i] : 0.0;
+        fen = lam[(16 * fb + 15) * DK + i];
+        frf = lam[(16 * fb + 7) * DK + i];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int t = ft0 + u;
+            const bool ok = t < L;
+            flm[u] = lam[t * DK + i];
+            fkp[u] = kap[t * DK + i];
+            fq[u] = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
+            fk[u] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+        }
+    };
+    if (fth) load2(0);
     for (int s0 = 0, kk = 0; s0 < DK; s0 += SLB, ++kk) {
         __syncthreads();  // dB and dT written; the previous slab's operands read
         // operands, transposed [ii][t]: kappa scaled to the end of its block and to the block's
         // token 8 (the column side of dq, dk); q and k scaled from the start of their block and
-        // from its token 8 (the column side of dkappa). Thread: channel s0 + ii, tokens
-        // 4 tg .. 4 tg + 3 (one block)
-        if (tid < SLB * 16) {
-            const int ii = tid % SLB, tg = tid / SLB, i = s0 + ii, b = tg >> 2, tb0 = 4 * tg;
-            const double lst = b > 0 ? lam[(16 * b - 1) * DK + i] : 0.0;
-            const double len = lam[(16 * b + 15) * DK + i], lrf = lam[(16 * b + 7) * DK + i];
+        // from its token 8 (the column side of dkappa)
+        if (fth) {
             float o[6][4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const int t = tb0 + u;
-                const bool ok = t < L;
-                const double lm = lam[t * DK + i];
-                const float kp = kap[t * DK + i];
-                const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
-                const float kv = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-                const float ast = __expf((float)(lm - lst));
-                const float amd = fminf(__expf((float)(lm - lrf)), RSAT);
-                const float ben = __expf((float)(len - lm));
-                const float bmd = fminf(__expf((float)(lrf - lm)), RSAT);
-                o[0][u] = ben * kp;
-                o[1][u] = bmd * kp;
-                o[2][u] = ast * qq;
-                o[3][u] = amd * qq;
-                o[4][u] = ast * kv;
-                o[5][u] = amd * kv;
+                const float ast = __expf((float)(flm[u] - fst));
+                const float amd = fminf(__expf((float)(flm[u] - frf)), RSAT);
+                const float ben = __expf((float)(fen - flm[u]));
+                const float bmd = fminf(__expf((float)(frf - flm[u])), RSAT);
+                o[0][u] = ben * fkp[u];
+                o[1][u] = bmd * fkp[u];
+                o[2][u] = ast * fq[u];
+                o[3][u] = amd * fq[u];
+                o[4][u] = ast * fk[u];
+                o[5][u] = amd * fk[u];
             }
 #pragma unroll
             for (int m = 0; m < 6; ++m)
-                *reinterpret_cast<float4*>(s_op + m * OPS + ii * LDC + tb0) =
-                    make_float4(o[m][0], o[m][1], o[m][2], o[m][3]);
+                *reinterpret_cast<floatx4*>(s_op + m * OPS + fii * LDC + ft0) =
+                    floatx4{o[m][0], o[m][1], o[m][2], o[m][3]};
+            if (s0 + SLB < DK) load2(s0 + SLB);
         }
         __syncthreads();
         if (16 * cw >= SLB) continue;
@@ -1153,95 +1192,132 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
         }
     }
 
-    // ---- the gradients out; the log-decay adjoint q dq + k dk - kappa dkappa -----------------
-    __syncthreads();  // phase 2 is over: the log-decay adjoint over its buffers
+    // ---- the gradients out; the log-decay adjoint q dq + k dk - kappa dkappa, its suffix sums
+    // over the chunk (alpha dalpha = sum over t >= s; the chunk-end terms enter at the last
+    // token) and the coefficients of the variance adjoint lambda_{t-1} = A_t lambda_t + B_t, all
+    // on the owned tiles. Row sums over the channels (the gain denominator's adjoint; isotropic:
+    // dbeta, ||k||^2, sum alpha^2) reduce within a tile row, then over the two waves of a row
+    // block; the suffix sums run within a tile, then over the row blocks --------------------------
+    float kvv[NCW][4], alv[NCW][4], suf[NCW][4];
+    float rp0[4] = {0.f, 0.f, 0.f, 0.f}, rp1[4] = {0.f, 0.f, 0.f, 0.f};
+    float rp2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < NCW; ++k) {
         const int ct = cw + 2 * k;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) kvv[k][r] = alv[k][r] = suf[k][r] = 0.f;
         if (ct >= NKT) continue;
         const int i = 16 * ct + li;
+        float x0[4], x1[4], x2[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int t = 16 * rb + 4 * lg + r;
             const bool ok = t < L;
             const float qq = ok ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
             const float kv = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
+            const float al =
+                ok ? (APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t))) : 1.f;
+            const float kp = kap[t * DK + i];
             if (ok) {
                 gq[row(t) * DK + i] = gqa[k][r];
                 gk[row(t) * DK + i] = gka[k][r];
             }
             dkap[t * DK + i] = gpa[k][r];
-            s_dl[t * LDZ + i] = qq * gqa[k][r] + kv * gka[k][r] - kap[t * DK + i] * gpa[k][r];
+            suf[k][r] = qq * gqa[k][r] + kv * gka[k][r] - kp * gpa[k][r];
+            kvv[k][r] = kv;
+            alv[k][r] = al;
+            x0[r] = DIAG ? gpa[k][r] * kp : gpa[k][r] * kv;
+            x1[r] = kv * kv;
+            x2[r] = al * al;
         }
-    }
-    __syncthreads();
-
-    // ---- d(log-decay) -> dalpha (memory part): alpha_s dalpha_s = sum_{t >= s} dlambda_t, the
-    // chunk-end terms (gamma_C) entering at the last token ---------------------------------------
-    if (tid < DK) {  // suffix sums over the chunk, in LDS
-        const int i = tid;
-        float acc = gC[i] * s_p6[i];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) acc += s_cp[b * DK + i];
-        for (int t = C - 1; t >= 0; --t) {
-            acc += s_dl[t * LDZ + i];
-            s_dl[t * LDZ + i] = acc;
-        }
-    }
-    __syncthreads();
-    for (int e = tid; e < C * DK; e += NTB) {
-        const int t = e / DK, i = e % DK;
-        float al = 1.f;
-        if (t < L) al = APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t));
-        dal[e] = t < L ? s_dl[t * LDZ + i] / al : 0.f;
-    }
-
-    // ---- coefficients of the variance adjoint: lambda_{t-1} = A_t lambda_t + B_t ------------
-    for (int j = 0; j < C / NWB; ++j) {
-        const int t = (C / NWB) * w + j;
-        const bool ok = t < L;
-        const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
-        const float dn = den[t];
-        if constexpr (DIAG) {
-            float s1 = 0.f;
-            for (int i = lane; i < DK; i += 64) s1 += dkap[t * DK + i] * kap[t * DK + i];
-            const float dden = -wave_sum(s1) / dn;
-            for (int i = lane; i < DK; i += 64) {
-                const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-                const float al = ok ? ld<TI>(a.alpha, row(t) * DK + i) : 1.f;
-                const float ph = phat[t * DK + i];
-                const float u = a.mu * kk * kk / rr, gg = 1.f + u * ph;
-                const float c = dkap[t * DK + i] * kk / dn + dden * kk * kk;
-                a.acf[(gh * C + t) * NCHAN + i] = ok ? al * al / (gg * gg) : 1.f;
-                a.bcf[(gh * C + t) * NCHAN + i] = ok ? al * al * c : 0.f;
-            }
-            if (lane == 0) a.aux[gh * C + t] = dden;
-        } else {
-            float sb = 0.f, sk = 0.f, sa = 0.f;
-            for (int i = lane; i < DK; i += 64) {
-                const float kk = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-                sb += dkap[t * DK + i] * kk;
-                sk += kk * kk;
-                if (APC) {
-                    const float al = ok ? ld<TI>(a.alpha, row(t) * DK + i) : 1.f;
-                    sa += al * al;
+        for (int o = 1; o < 16; o <<= 1)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                x0[r] += __shfl_xor(x0[r], o, 64);
+                if (!DIAG) {
+                    x1[r] += __shfl_xor(x1[r], o, 64);
+                    if (APC) x2[r] += __shfl_xor(x2[r], o, 64);
                 }
             }
-            const float dbeta = wave_sum(sb), nk = wave_sum(sk);
-            float aa;
-            if (APC) aa = wave_sum(sa) / (float)DK;
-            else {
-                const float al = ok ? ld<TI>(a.alpha, row(t)) : 1.f;
-                aa = al * al;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            rp0[r] += x0[r];
+            rp1[r] += x1[r];
+            rp2[r] += x2[r];
+        }
+        // suffix within the tile: the lane's rows, then the lanes of the later rows
+#pragma unroll
+        for (int r = 2; r >= 0; --r) suf[k][r] += suf[k][r + 1];
+        const float tot = suf[k][0];
+        const float g1 = __shfl(tot, li + 16, 64), g2 = __shfl(tot, li + 32, 64);
+        const float g3 = __shfl(tot, li + 48, 64);
+        const float later = (lg < 1 ? g1 : 0.f) + (lg < 2 ? g2 : 0.f) + (lg < 3 ? g3 : 0.f);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) suf[k][r] += later;
+        if (lg == 0) s_bt[rb * DK + i] = suf[k][0];
+    }
+    if (li == 0)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * rb + 4 * lg + r;
+            s_rp[(cw * 3 + 0) * C + t] = rp0[r];
+            s_rp[(cw * 3 + 1) * C + t] = rp1[r];
+            s_rp[(cw * 3 + 2) * C + t] = rp2[r];
+        }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NCW; ++k) {
+        const int ct = cw + 2 * k;
+        if (ct >= NKT) continue;
+        const int i = 16 * ct + li;
+        float off = gC[i] * s_p6[i];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) off += s_cp[b * DK + i] + (b > rb ? s_bt[b * DK + i] : 0.f);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int t = 16 * rb + 4 * lg + r;
+            dal[t * DK + i] = t < L ? (suf[k][r] + off) / alv[k][r] : 0.f;
+        }
+        if constexpr (DIAG) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * rb + 4 * lg + r;
+                const bool ok = t < L;
+                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                const float dn = den[t];
+                const float dden = -(s_rp[0 * C + t] + s_rp[3 * C + t]) / dn;
+                const float kv = kvv[k][r], al = alv[k][r];
+                const float u = a.mu * kv * kv / rr, gg = 1.f + u * phat[t * DK + i];
+                const float c = gpa[k][r] * kv / dn + dden * kv * kv;
+                a.acf[(gh * C + t) * NCHAN + i] = ok ? al * al / (gg * gg) : 1.f;
+                a.bcf[(gh * C + t) * NCHAN + i] = ok ? al * al * c : 0.f;
+                if (k == 0 && cw == 0 && li == 0) a.aux[gh * C + t] = dden;
             }
-            if (lane == 0) {
+        }
+    }
+    if constexpr (!DIAG) {  // one value per token: the row sums of both waves of the row block
+        if (cw == 0 && li == 0)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * rb + 4 * lg + r;
+                const bool ok = t < L;
+                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
+                const float dn = den[t];
+                const float dbeta = s_rp[0 * C + t] + s_rp[3 * C + t];
+                const float nk = s_rp[1 * C + t] + s_rp[4 * C + t];
+                float aa;
+                if (APC) aa = (s_rp[2 * C + t] + s_rp[5 * C + t]) / (float)DK;
+                else {
+                    const float al = ok ? ld<TI>(a.alpha, row(t)) : 1.f;
+                    aa = al * al;
+                }
                 const float bh = phat[t * DK];
                 const float u = a.mu * nk / ((float)DK * rr), gg = 1.f + u * bh;
                 a.acf[gh * C + t] = ok ? aa / (gg * gg) : 1.f;
                 a.bcf[gh * C + t] = ok ? aa * dbeta * rr / (dn * dn) : 0.f;
                 a.aux[gh * C + t] = dbeta;
             }
-        }
     }
 }
 
