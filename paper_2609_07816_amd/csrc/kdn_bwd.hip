@@ -120,6 +120,27 @@ __device__ __forceinline__ float ld(const void* p, size_t i)
     return to_f32(((const TI*)p)[i]);
 }
 
+// Eight consecutive inputs from element i (a multiple of 8) in float32: one 16-byte load
+// (bf16) or two (float32).
+template <class TI>
+__device__ __forceinline__ void ld8(const void* p, size_t i, float* x)
+{
+    if constexpr (sizeof(TI) == 2) {
+        const uint4 v = *reinterpret_cast<const uint4*>((const TI*)p + i);
+        const float2 a = unpack2(v.x), b = unpack2(v.y), c = unpack2(v.z), d = unpack2(v.w);
+        x[0] = a.x; x[1] = a.y; x[2] = b.x; x[3] = b.y;
+        x[4] = c.x; x[5] = c.y; x[6] = d.x; x[7] = d.y;
+    } else {
+        const floatx4 a = *reinterpret_cast<const floatx4*>((const float*)p + i);
+        const floatx4 b = *reinterpret_cast<const floatx4*>((const float*)p + i + 4);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            x[u] = a[u];
+            x[4 + u] = b[u];
+        }
+    }
+}
+
 // ------------------------------------------------------------------------------------------
 // bw_prep
 // ------------------------------------------------------------------------------------------
@@ -195,14 +216,35 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
     float* __restrict__ den = (float*)(rec + R::OFF_DEN);
     auto row = [&](int t) { return (size_t)(c0 + t) * H + h; };
 
-    // ---- the chunk's inputs in LDS (padding tokens: alpha 1, k 0, omega 0, r 1) -----------
-    for (int e = tid; e < C * DK; e += NTB) {
-        const int t = e / DK, i = e % DK;
+    // ---- the chunk's inputs in LDS (padding tokens: alpha 1, k 0, omega 0, r 1), eight
+    // channels per piece -------------------------------------------------------------------
+    for (int e = tid; e < C * DK / 8; e += NTB) {
+        const int t = e / (DK / 8), i8 = 8 * (e % (DK / 8));
         const bool ok = t < L;
-        s_k[t * LDK + i] = ok ? ld<TI>(a.k, row(t) * DK + i) : 0.f;
-        s_aq[t * LDK + i] =
-            ok ? (APC ? ld<TI>(a.alpha, row(t) * DK + i) : ld<TI>(a.alpha, row(t))) : 1.f;
-        if (DIAG) s_wp[t * LDK + i] = ok ? ld<TI>(a.omega, row(t) * DK + i) : 0.f;
+        float kx[8], ax[8], wx[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            kx[u] = 0.f;
+            ax[u] = 1.f;
+            wx[u] = 0.f;
+        }
+        if (ok) {
+            ld8<TI>(a.k, row(t) * DK + i8, kx);
+            if (APC) {
+                ld8<TI>(a.alpha, row(t) * DK + i8, ax);
+            } else {
+                const float a1 = ld<TI>(a.alpha, row(t));
+#pragma unroll
+                for (int u = 0; u < 8; ++u) ax[u] = a1;
+            }
+            if (DIAG) ld8<TI>(a.omega, row(t) * DK + i8, wx);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            s_k[t * LDK + i8 + u] = kx[u];
+            s_aq[t * LDK + i8 + u] = ax[u];
+            if (DIAG) s_wp[t * LDK + i8 + u] = wx[u];
+        }
     }
     if (tid < C) {
         const bool ok = tid < L;
@@ -291,19 +333,37 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
     }
 
     // ---- kappa, gamma-scaled operands and the tail operand; q into LDS (alpha is dead) ------
-    for (int e = tid; e < C * DK; e += NTB) {
-        const int t = e / DK, i = e % DK;
-        const float kk = s_k[t * LDK + i];
-        const float qq = t < L ? ld<TI>(a.q, row(t) * DK + i) : 0.f;
-        const float kp = DIAG ? s_wp[t * LDK + i] * kk / s_den[t] : s_beta[t] * kk;
-        const double lm = lam[e];
-        const float gm = expf((float)lm);
-        kap[e] = kp;
-        kbar[e] = gm * kk;
-        qbar[e] = gm * qq;
-        ktl[e] = expf((float)(s_lc[i] - lm)) * kp;
-        s_wp[t * LDK + i] = kp;
-        s_aq[t * LDK + i] = qq;
+    for (int e8 = tid; e8 < C * DK / 8; e8 += NTB) {  // eight channels per piece
+        const int t = e8 / (DK / 8), i8 = 8 * (e8 % (DK / 8)), e = t * DK + i8;
+        float qx[8], kpx[8], kbx[8], qbx[8], ktx[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) qx[u] = 0.f;
+        if (t < L) ld8<TI>(a.q, row(t) * DK + i8, qx);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int i = i8 + u;
+            const float kk = s_k[t * LDK + i];
+            const float kp = DIAG ? s_wp[t * LDK + i] * kk / s_den[t] : s_beta[t] * kk;
+            const double lm = lam[e + u];
+            const float gm = expf((float)lm);
+            kpx[u] = kp;
+            kbx[u] = gm * kk;
+            qbx[u] = gm * qx[u];
+            ktx[u] = expf((float)(s_lc[i] - lm)) * kp;
+            s_wp[t * LDK + i] = kp;
+            s_aq[t * LDK + i] = qx[u];
+        }
+#pragma unroll
+        for (int h4 = 0; h4 < 8; h4 += 4) {
+            *reinterpret_cast<floatx4*>(kap + e + h4) =
+                floatx4{kpx[h4], kpx[h4 + 1], kpx[h4 + 2], kpx[h4 + 3]};
+            *reinterpret_cast<floatx4*>(kbar + e + h4) =
+                floatx4{kbx[h4], kbx[h4 + 1], kbx[h4 + 2], kbx[h4 + 3]};
+            *reinterpret_cast<floatx4*>(qbar + e + h4) =
+                floatx4{qbx[h4], qbx[h4 + 1], qbx[h4 + 2], qbx[h4 + 3]};
+            *reinterpret_cast<floatx4*>(ktl + e + h4) =
+                floatx4{ktx[h4], ktx[h4 + 1], ktx[h4 + 2], ktx[h4 + 3]};
+        }
     }
     __syncthreads();
 
