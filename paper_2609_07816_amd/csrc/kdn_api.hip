@@ -8,6 +8,10 @@
 
 #include "kdn_internal.h"
 
+#include <cstdint>
+#include <initializer_list>
+#include <utility>
+
 namespace {
 
 // Scratch of kdn_forward_diag_noalloc: one copy per GPU, held until the process ends. Host code
@@ -77,6 +81,16 @@ kdn_status_t scratch_on_current_device(void** out)
     return KDN_OK;
 }
 
+// Tensors whose innermost dimension is d_k or d_v are read and written in 16-byte pieces: each
+// must start at a 16-byte boundary (null pointers are skipped).
+kdn_status_t check_aligned(std::initializer_list<std::pair<const void*, const char*>> ptrs)
+{
+    for (const auto& p : ptrs)
+        if (p.first && ((uintptr_t)p.first & 15))
+            return fail(KDN_ERR_INVALID_ARG, "%s must be 16-byte aligned", p.second);
+    return KDN_OK;
+}
+
 // Shared validation of the forward / gain argument sets.
 kdn_status_t check_seq(const int32_t* cu, int32_t N, int32_t B, int32_t T, int32_t H)
 {
@@ -111,6 +125,11 @@ kdn_status_t check_forward(int variant, const void* q, const void* k, const void
     if (!(mu > 0.f) || !(scale > 0.f))
         return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
                     scale);
+    st = check_aligned({{q, "q"}, {k, "k"}, {v, "v"}, {(variant == 0 || apc) ? alpha : nullptr,
+                        "alpha"}, {variant == 0 ? omega : nullptr, "omega"}, {o, "o"},
+                        {S0, "S0"}, {S_T, "S_T"}, {variant == 0 ? P0 : nullptr, "P0"},
+                        {variant == 0 ? P_T : nullptr, "P_T"}});
+    if (st != KDN_OK) return st;
     if (!kdn::chunked_supported(chunk))
         return fail(KDN_ERR_UNSUPPORTED, "chunk=%d: the forward runs chunks of 64 tokens (pass 0 "
                     "or 64)", chunk);
@@ -345,6 +364,11 @@ static kdn_status_t decode_common(int32_t variant, const void* q, const void* k,
                     dv);
     if (!(mu > 0.f) || !(scale > 0.f))
         return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive");
+    kdn_status_t sa = check_aligned(
+        {{q, "q"}, {k, "k"}, {v, "v"}, {(variant == 0 || alpha_per_channel) ? alpha : nullptr,
+          "alpha"}, {variant == 0 ? omega : nullptr, "omega"}, {o, "o"}, {S, "S"},
+         {variant == 0 ? P : nullptr, "P"}});
+    if (sa != KDN_OK) return sa;
     const size_t es = esize(dtype), rows = (size_t)R * H;
     const size_t ns = (size_t)num_slots * H * dk * dv * 4;
     const size_t np = (size_t)num_slots * H * (variant == 0 ? dk : 1) * 4;
@@ -409,6 +433,9 @@ kdn_status_t kdn_forward_kam(const void* q, const void* k, const void* v, const 
         return fail(KDN_ERR_UNSUPPORTED, "dk=%d dv=%d: head sizes must be 16, 32, 64 or 128", dk,
                     dv);
     if (!(scale > 0.f)) return fail(KDN_ERR_INVALID_ARG, "scale must be positive (%g)", scale);
+    st = check_aligned({{q, "q"}, {k, "k"}, {v, "v"}, {alpha, "alpha"}, {omega, "omega"},
+                        {o, "o"}, {S0, "S0"}, {P0, "P0"}, {S_T, "S_T"}, {P_T, "P_T"}});
+    if (st != KDN_OK) return st;
     const size_t rows = (size_t)B * T * H, es = esize(dtype);
     const size_t nk = rows * dk * es, nv = rows * dv * es;
     const void* ins[6] = {q, k, v, alpha, omega, r};
@@ -463,6 +490,14 @@ kdn_status_t kdn_backward(int32_t variant, const void* q, const void* k, const v
         return fail(KDN_ERR_INVALID_ARG, "mu and scale must be positive (mu=%g scale=%g)", mu,
                     scale);
     const int apc = (variant == 0 || alpha_per_channel) ? 1 : 0;
+    st = check_aligned({{q, "q"}, {k, "k"}, {v, "v"}, {apc ? alpha : nullptr, "alpha"},
+                        {variant == 0 ? omega : nullptr, "omega"}, {dO, "dO"}, {S0, "S0"},
+                        {variant == 0 ? P0 : nullptr, "P0"}, {dS_T, "dS_T"},
+                        {variant == 0 ? dP_T : nullptr, "dP_T"}, {dq, "dq"}, {dk_out, "dk"},
+                        {dv_out, "dv"}, {apc ? dalpha : nullptr, "dalpha"},
+                        {variant == 0 ? domega : nullptr, "domega"}, {dS0, "dS0"},
+                        {variant == 0 ? dP0 : nullptr, "dP0"}});
+    if (st != KDN_OK) return st;
     const size_t rows = (size_t)B * T * H, es = esize(dtype);
     const size_t pc = variant == 0 ? (size_t)dk : 1;
     // every buffer the call reads or writes, with its extent; the gradients may overlap none
@@ -519,6 +554,13 @@ static kdn_status_t gain_common(int variant, const void* k, const void* alpha, c
     if (st != KDN_OK) return st;
     if (!head_ok(dk)) return fail(KDN_ERR_UNSUPPORTED, "dk=%d: must be 16, 32, 64 or 128", dk);
     if (!(mu > 0.f)) return fail(KDN_ERR_INVALID_ARG, "mu must be positive (mu=%g)", mu);
+    st = check_aligned({{k, "k"}, {(variant == 0 || apc) ? alpha : nullptr, "alpha"},
+                        {variant == 0 ? omega : nullptr, "omega"},
+                        {variant == 0 ? gain_out : nullptr, "gain"},
+                        {variant == 0 ? phat_out : nullptr, "phat"},
+                        {variant == 0 ? P0 : nullptr, "P0"},
+                        {variant == 0 ? P_T : nullptr, "P_T"}});
+    if (st != KDN_OK) return st;
     const size_t need = kdn::gain_workspace_bytes(variant, N, B, T, H, dk);
     if (!ws || ws_bytes < need)
         return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,

@@ -169,3 +169,28 @@ def test_layer_argument_errors(L):
     assert L.kdn_decode_step_layer(*dec, ctypes.byref(opts), None) == kdn.KDN_ERR_INVALID_ARG
     opts = kdn.LayerOpts(0, 0.0, 0, None, 0x1000000 * 11)  # beta_eff inside o
     assert L.kdn_decode_step_layer(*dec, ctypes.byref(opts), None) == kdn.KDN_ERR_INVALID_ARG
+
+
+def test_misaligned_tensors_rejected(L):
+    """Tensors of d_k or d_v columns are moved in 16-byte pieces: a pointer off a 16-byte
+    boundary is refused before any launch (per-head scalars such as r have no such rule)."""
+    off = ctypes.c_void_p(0x1000000 + 8)
+    p = [P(i) for i in range(7)]
+    assert fwd(L, ptrs=[off] + p[1:]) == kdn.KDN_ERR_INVALID_ARG
+    assert "q must be 16-byte aligned" in L.kdn_last_error().decode()
+    assert fwd(L, ptrs=p[:6] + [off]) == kdn.KDN_ERR_INVALID_ARG
+    assert "o must be" in L.kdn_last_error().decode()
+    # r (one value per token and head) may sit anywhere: the call reaches the workspace check
+    assert fwd(L, ptrs=p[:5] + [ctypes.c_void_p(0x6000002)] + p[6:]) == kdn.KDN_ERR_WORKSPACE
+    g = [P(i) for i in range(10, 18)]
+    bwd = [0] + p[:6] + [None, None, None, 1, 1, 8, 2, 64, 64, 1, 1, F(64.0), F(0.125), None,
+                         None, None]
+    ws = [P(40), 1 << 40, None]
+    g_bad = list(g)
+    g_bad[2] = ctypes.c_void_p(0x1b000004)
+    assert L.kdn_backward(*bwd, *g_bad, *ws) == kdn.KDN_ERR_INVALID_ARG
+    assert "dv must be 16-byte aligned" in L.kdn_last_error().decode()
+    dec = [0] + p[:6] + [ctypes.c_void_p(0x8000004), P(8), None, P(10), 4, 4, 2, 64, 64, 1, 1,
+                         F(64.0), F(0.125), None]
+    assert L.kdn_decode_step(*dec) == kdn.KDN_ERR_INVALID_ARG
+    assert "S must be 16-byte aligned" in L.kdn_last_error().decode()
