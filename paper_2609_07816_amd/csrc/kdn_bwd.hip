@@ -571,8 +571,31 @@ struct WalkPieces {
     static constexpr int NK4 = C * DK / 4, PK = (NK4 + NTB - 1) / NTB;
     static constexpr int NC4 = C * C / 4, PC = NC4 / NTB;
     static constexpr int PV = C * WalkLds<DK>::BVM / NTB;
+    // operands stored transposed move in 4 x 4 blocks (four row pieces in, four column pieces
+    // out): one block of a [C][DK] matrix per thread at most, a [C][C] matrix in half the threads
+    static constexpr int NKB = (C / 4) * (DK / 4), NCB = (C / 4) * (C / 4);
+    static_assert(NKB <= NTB && 2 * NCB == NTB, "one block per thread");
     static_assert(NC4 % NTB == 0 && (C * WalkLds<DK>::BVM) % NTB == 0, "whole pieces");
 };
+
+// Block b of an R x K row-major matrix (K / 4 blocks per row band): rows 4 (b / (K / 4)) .. + 3,
+// columns 4 (b % (K / 4)) .. + 3. Load: four row pieces; store transposed: four column pieces.
+template <int K>
+__device__ __forceinline__ void blk_load(const float* src, int b, floatx4* x)
+{
+    const int r4 = 4 * (b / (K / 4)), c4 = 4 * (b % (K / 4));
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = *reinterpret_cast<const floatx4*>(src + (r4 + r) * K + c4);
+}
+template <int K>
+__device__ __forceinline__ void blk_store_t(float* dst, int ld, int b, const floatx4* x)
+{
+    const int r4 = 4 * (b / (K / 4)), c4 = 4 * (b % (K / 4));
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        *reinterpret_cast<floatx4*>(dst + (c4 + u) * ld + r4) =
+            floatx4{x[0][u], x[1][u], x[2][u], x[3][u]};
+}
 
 // The operands of chunk ci + 1 (fwalk) or ci - 1 (rwalk) are loaded into registers while chunk
 // ci is computed, and stored to LDS after the barrier that ends it.
@@ -583,7 +606,7 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
     using LY = WalkLds<DK>;
     using WP = WalkPieces<DK>;
     constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16, BVM = LY::BVM, LDV = BVM + 1;
-    constexpr int PK = WP::PK, PC = WP::PC, PV = WP::PV, NK4 = WP::NK4;
+    constexpr int PK = WP::PK, PC = WP::PC, PV = WP::PV, NK4 = WP::NK4, NKB = WP::NKB;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_St = (float*)(smem + LY::F_ST);
     float* s_kb = (float*)(smem + LY::F_KB);
@@ -608,20 +631,16 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
         const int i = e / BV, j = e % BV;
         s_St[j * LDK + i] = a.S0 ? a.S0[((size_t)slot * DK + i) * DV + j0 + j] : 0.f;
     }
-    floatx4 kb4[PK], kt4[PK], am4[PC];
+    floatx4 kb4[PK], ktb[4], am4[PC];
     float vv[PV], gcv = 0.f;
     auto load = [&](int ci) __attribute__((always_inline)) {
         const int c0 = t0 + ci * C, L = min(C, t1 - c0);
         const char* rec = a.rec + ((size_t)(g0 + ci) * H + h) * R::BYTES;
         const floatx4* kbar = (const floatx4*)(rec + R::OFF_KBAR);
-        const floatx4* ktl = (const floatx4*)(rec + R::OFF_KTL);
         const floatx4* Am = (const floatx4*)(rec + R::OFF_A);
 #pragma unroll
-        for (int u = 0; u < PK; ++u) {
-            const int e = min(tid + NTB * u, NK4 - 1);
-            kb4[u] = kbar[e];
-            kt4[u] = ktl[e];
-        }
+        for (int u = 0; u < PK; ++u) kb4[u] = kbar[min(tid + NTB * u, NK4 - 1)];
+        blk_load<DK>((const float*)(rec + R::OFF_KTL), min(tid, NKB - 1), ktb);
 #pragma unroll
         for (int u = 0; u < PC; ++u) am4[u] = Am[tid + NTB * u];
         if (tid < DK) gcv = ((const float*)(rec + R::OFF_GC))[tid];
@@ -639,12 +658,9 @@ __global__ __launch_bounds__(NTB) void bw_fwalk(Args a)
             if (e < NK4) {
                 const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
                 *reinterpret_cast<floatx4*>(s_kb + t * LDK + i4) = kb4[u];
-                s_ktT[(i4 + 0) * LDC + t] = kt4[u][0];  // Ktail^T
-                s_ktT[(i4 + 1) * LDC + t] = kt4[u][1];
-                s_ktT[(i4 + 2) * LDC + t] = kt4[u][2];
-                s_ktT[(i4 + 3) * LDC + t] = kt4[u][3];
             }
         }
+        if (tid < NKB) blk_store_t<DK>(s_ktT, LDC, tid, ktb);  // Ktail^T
 #pragma unroll
         for (int u = 0; u < PC; ++u) {
             const int e = tid + NTB * u, t = e / (C / 4), s4 = 4 * (e % (C / 4));
@@ -720,7 +736,7 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
     using LY = WalkLds<DK>;
     using WP = WalkPieces<DK>;
     constexpr int LDK = LY::LDK, LDC = LY::LDC, NKT = DK / 16, BVM = LY::BVM;
-    constexpr int PK = WP::PK, PC = WP::PC, PV = WP::PV, NK4 = WP::NK4;
+    constexpr int PK = WP::PK, PV = WP::PV, NK4 = WP::NK4, NKB = WP::NKB, NCB = WP::NCB;
     extern __shared__ __attribute__((aligned(16))) char smem[];
     float* s_dST = (float*)(smem + LY::R_ST);
     float* s_BT = (float*)(smem + LY::R_BT);
@@ -749,22 +765,18 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
     }
     // first group: Ktail, B, A, gamma_C, scale dO (stored at the chunk's start); second group:
     // Qbar, Kbar (stored over Ktail once it is read)
-    floatx4 kt4[PK], bm4[PC], am4[PC], qb4[PK], kb4[PK];
+    // B or A (half the threads each) and Qbar, Kbar move in 4 x 4 blocks (stored transposed)
+    floatx4 kt4[PK], cb[4], qbb[4], kbb[4];
+    const bool isb = tid < NCB;
     float ov[PV], gcv = 0.f;
     auto rec_of = [&](int ci) { return a.rec + ((size_t)(g0 + ci) * H + h) * R::BYTES; };
     auto load1 = [&](int ci) __attribute__((always_inline)) {
         const int c0 = t0 + ci * C, L = min(C, t1 - c0);
         const char* rec = rec_of(ci);
         const floatx4* ktl = (const floatx4*)(rec + R::OFF_KTL);
-        const floatx4* Am = (const floatx4*)(rec + R::OFF_A);
-        const floatx4* Bm = (const floatx4*)(rec + R::OFF_B);
 #pragma unroll
         for (int u = 0; u < PK; ++u) kt4[u] = ktl[min(tid + NTB * u, NK4 - 1)];
-#pragma unroll
-        for (int u = 0; u < PC; ++u) {
-            am4[u] = Am[tid + NTB * u];
-            bm4[u] = Bm[tid + NTB * u];
-        }
+        blk_load<C>((const float*)(rec + (isb ? R::OFF_B : R::OFF_A)), isb ? tid : tid - NCB, cb);
         if (tid < DK) gcv = ((const float*)(rec + R::OFF_GC))[tid];
 #pragma unroll
         for (int u = 0; u < PV; ++u) {
@@ -783,18 +795,7 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
                 *reinterpret_cast<floatx4*>(s_kt + t * LDK + i4) = kt4[u];
             }
         }
-#pragma unroll
-        for (int u = 0; u < PC; ++u) {  // B^T and A^T
-            const int e = tid + NTB * u, t = e / (C / 4), s4 = 4 * (e % (C / 4));
-            s_BT[(s4 + 0) * LDC + t] = bm4[u][0];
-            s_BT[(s4 + 1) * LDC + t] = bm4[u][1];
-            s_BT[(s4 + 2) * LDC + t] = bm4[u][2];
-            s_BT[(s4 + 3) * LDC + t] = bm4[u][3];
-            s_AT[(s4 + 0) * LDC + t] = am4[u][0];
-            s_AT[(s4 + 1) * LDC + t] = am4[u][1];
-            s_AT[(s4 + 2) * LDC + t] = am4[u][2];
-            s_AT[(s4 + 3) * LDC + t] = am4[u][3];
-        }
+        blk_store_t<C>(isb ? s_BT : s_AT, LDC, isb ? tid : tid - NCB, cb);  // B^T or A^T
         if (tid < DK) s_gc[tid] = gcv;
 #pragma unroll
         for (int u = 0; u < PV; ++u) {  // scale dO, transposed
@@ -804,30 +805,13 @@ __global__ __launch_bounds__(NTB) void bw_rwalk(Args a)
     };
     auto load2 = [&](int ci) __attribute__((always_inline)) {
         const char* rec = rec_of(ci);
-        const floatx4* qbar = (const floatx4*)(rec + R::OFF_QBAR);
-        const floatx4* kbar = (const floatx4*)(rec + R::OFF_KBAR);
-#pragma unroll
-        for (int u = 0; u < PK; ++u) {
-            const int e = min(tid + NTB * u, NK4 - 1);
-            qb4[u] = qbar[e];
-            kb4[u] = kbar[e];
-        }
+        blk_load<DK>((const float*)(rec + R::OFF_QBAR), min(tid, NKB - 1), qbb);
+        blk_load<DK>((const float*)(rec + R::OFF_KBAR), min(tid, NKB - 1), kbb);
     };
     auto store2 = [&]() __attribute__((always_inline)) {  // Qbar^T and Kbar^T
-#pragma unroll
-        for (int u = 0; u < PK; ++u) {
-            const int e = tid + NTB * u;
-            if (e < NK4) {
-                const int t = e / (DK / 4), i4 = 4 * (e % (DK / 4));
-                s_qT[(i4 + 0) * LDC + t] = qb4[u][0];
-                s_qT[(i4 + 1) * LDC + t] = qb4[u][1];
-                s_qT[(i4 + 2) * LDC + t] = qb4[u][2];
-                s_qT[(i4 + 3) * LDC + t] = qb4[u][3];
-                s_kT[(i4 + 0) * LDC + t] = kb4[u][0];
-                s_kT[(i4 + 1) * LDC + t] = kb4[u][1];
-                s_kT[(i4 + 2) * LDC + t] = kb4[u][2];
-                s_kT[(i4 + 3) * LDC + t] = kb4[u][3];
-            }
+        if (tid < NKB) {
+            blk_store_t<DK>(s_qT, LDC, tid, qbb);
+            blk_store_t<DK>(s_kT, LDC, tid, kbb);
         }
     };
     if (nch > 0) {
