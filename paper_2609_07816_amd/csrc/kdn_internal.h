@@ -30,11 +30,26 @@ __device__ __forceinline__ float ldf(const T* p, size_t i) { return to_f32(p[i])
 // ------------------------------------------------------------------------------------------
 // wavefront reductions (64 lanes)
 // ------------------------------------------------------------------------------------------
+// Sum over the 64 lanes of a wave, returned to every lane (wave-uniform). All lanes must be
+// active. DPP: inclusive scans inside each row of 16 lanes (row_shr 1, 2, 4, 8), then each row
+// takes the running total of the rows before it (row_bcast 15 into rows 1 and 3, row_bcast 31
+// into rows 2 and 3), so lane 63 holds the total; lanes whose DPP source falls outside their row
+// read 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_add(float x)
+{
+    return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
+                                             0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xf, false));
+}
 __device__ __forceinline__ float wave_sum(float x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
-    return x;
+    x = dpp_add<0x111, 0xf>(x);  // row_shr:1
+    x = dpp_add<0x112, 0xf>(x);  // row_shr:2
+    x = dpp_add<0x114, 0xf>(x);  // row_shr:4
+    x = dpp_add<0x118, 0xf>(x);  // row_shr:8
+    x = dpp_add<0x142, 0xa>(x);  // row_bcast:15
+    x = dpp_add<0x143, 0xc>(x);  // row_bcast:31
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
 }
 
 // Power-of-two rescale of a homogeneous pair (n, d): exact, keeps n/d, keeps max(|n|,|d|) in
