@@ -1121,9 +1121,17 @@ __global__ __launch_bounds__(NTH) void walk_kernel(WalkArgs a)
                     Sacc[j][2] *= gc[p].z;
                     Sacc[j][3] *= gc[p].w;
                     static_assert(NNT <= 2, "value tiles of at most 32 columns");
+                    // with SHARE the value tile is a compile-time index into rf; otherwise the
+                    // fragment is read again from LDS (a runtime index would put rf in scratch)
 #pragma unroll
-                    for (int s = 0; s < NSC; ++s)
-                        Sacc[j] = FC::mma(Sacc[j], pf[p][s], nt == 0 ? rf[0][s] : rf[NNT - 1][s]);
+                    for (int s = 0; s < NSC; ++s) {
+                        typename FC::V rv;
+                        if constexpr (CF::SHARE)
+                            rv = rf[j % NNT][s];
+                        else
+                            rv = FC::ld(RT + (16 * nt + li) * LDC + FC::KF * s + (FC::KF / 4) * lg);
+                        Sacc[j] = FC::mma(Sacc[j], pf[p][s], rv);
+                    }
                     store4<MT>(SmT + (16 * nt + li) * LDK + 16 * ik + 4 * lg, Sacc[j][0],
                                Sacc[j][1], Sacc[j][2], Sacc[j][3]);
                 }
