@@ -114,3 +114,35 @@ def test_backward_small_gates_and_zero_noise():
                       alpha_law=("uniform", 0.01, 0.3), omega_law=("const", 0.0),
                       r_law=("uniform", 1e-3, 2e-3))
     compare_backward(x, seed=96)
+
+
+# ---------------------------------------------------------------------------------------------
+# full-size workloads (the isotropic B4 T2048 and the diagonal B4 T4096 at H16 d128, bf16), the
+# backward run once over the whole batch, checked on sampled (batch row, head) chains: each
+# chain's gradients depend on that chain's inputs and adjoints only, so the oracle runs on the
+# sampled slices alone
+# ---------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("wid", [1, 2])
+def test_backward_full_workload_sampled(wid):
+    from paper_2609_07816_amd import kdn
+    x = W.draw_workload(wid)
+    dO, dS, dP = adjoints(x, seed=100 + wid)
+    d = to_device(x)
+    got = kdn.backward(x.variant, d["q"], d["k"], d["v"], d["alpha"], d["omega"], d["r"],
+                       S0=d["S0"], P0=d["P0"], mu=x.mu, scale=x.scale,
+                       dO=dev_tensor(dO, x.dtype), dS_T=torch.from_numpy(dS).cuda(),
+                       dP_T=torch.from_numpy(dP).cuda())
+    torch.cuda.synchronize()
+    chains = [(0, 0), (x.B - 1, x.H - 1), (1, 7)]
+    for b, h in chains:
+        tok = (slice(b, b + 1), slice(None), slice(h, h + 1))
+        st = (slice(b, b + 1), slice(h, h + 1))
+        ins = [x.f64(n)[tok] for n in NAMES]
+        ref = oracle.backward(x.variant, *ins, S0=None if x.S0 is None else x.S0[st],
+                              P0=None if x.P0 is None else x.P0[st], mu=x.mu, scale=x.scale,
+                              dO=W.to_f64(dO, x.dtype)[tok], dS_T=dS[st], dP_T=dP[st])
+        print(f" chain (b={b}, h={h})", flush=True)
+        for name in GRADS:
+            sl = st if name in ("dS0", "dP0") else tok
+            check(name, host_f64(got[name][sl]), ref[name])
