@@ -1242,16 +1242,26 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     // on the owned tiles. Row sums over the channels (the gain denominator's adjoint; isotropic:
     // dbeta, ||k||^2, sum alpha^2) reduce within a tile row, then over the two waves of a row
     // block; the suffix sums run within a tile, then over the row blocks --------------------------
-    float kvv[NCW][4], alv[NCW][4], suf[NCW][4];
+    float kvv[NCW][4], alv[NCW][4], suf[NCW][4], phv[NCW][4];
+    float rrv[4], dnv[4];  // r and the gain denominator of the lane's rows
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int t = 16 * rb + 4 * lg + r;
+        rrv[r] = t < L ? ld<TI>(a.r, row(t)) : 1.f;
+        dnv[r] = den[t];
+    }
     float rp0[4] = {0.f, 0.f, 0.f, 0.f}, rp1[4] = {0.f, 0.f, 0.f, 0.f};
     float rp2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k = 0; k < NCW; ++k) {
         const int ct = cw + 2 * k;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) kvv[k][r] = alv[k][r] = suf[k][r] = 0.f;
+        for (int r = 0; r < 4; ++r) kvv[k][r] = alv[k][r] = suf[k][r] = phv[k][r] = 0.f;
         if (ct >= NKT) continue;
         const int i = 16 * ct + li;
+        if (DIAG)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) phv[k][r] = phat[(16 * rb + 4 * lg + r) * DK + i];
         float x0[4], x1[4], x2[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1275,15 +1285,13 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
             x2[r] = al * al;
         }
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                x0[r] += __shfl_xor(x0[r], o, 64);
-                if (!DIAG) {
-                    x1[r] += __shfl_xor(x1[r], o, 64);
-                    if (APC) x2[r] += __shfl_xor(x2[r], o, 64);
-                }
+        for (int r = 0; r < 4; ++r) {  // over the tile's 16 channels (the lanes of a row)
+            x0[r] = row16_sum(x0[r]);
+            if (!DIAG) {
+                x1[r] = row16_sum(x1[r]);
+                if (APC) x2[r] = row16_sum(x2[r]);
             }
+        }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             rp0[r] += x0[r];
@@ -1328,11 +1336,10 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * rb + 4 * lg + r;
                 const bool ok = t < L;
-                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
-                const float dn = den[t];
+                const float rr = rrv[r], dn = dnv[r];
                 const float dden = -(s_rp[0 * C + t] + s_rp[3 * C + t]) / dn;
                 const float kv = kvv[k][r], al = alv[k][r];
-                const float u = a.mu * kv * kv / rr, gg = 1.f + u * phat[t * DK + i];
+                const float u = a.mu * kv * kv / rr, gg = 1.f + u * phv[k][r];
                 const float c = gpa[k][r] * kv / dn + dden * kv * kv;
                 a.acf[(gh * C + t) * NCHAN + i] = ok ? al * al / (gg * gg) : 1.f;
                 a.bcf[(gh * C + t) * NCHAN + i] = ok ? al * al * c : 0.f;
@@ -1346,8 +1353,7 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * rb + 4 * lg + r;
                 const bool ok = t < L;
-                const float rr = ok ? ld<TI>(a.r, row(t)) : 1.f;
-                const float dn = den[t];
+                const float rr = rrv[r], dn = dnv[r];
                 const float dbeta = s_rp[0 * C + t] + s_rp[3 * C + t];
                 const float nk = s_rp[1 * C + t] + s_rp[4 * C + t];
                 float aa;

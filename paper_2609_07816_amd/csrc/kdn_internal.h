@@ -41,6 +41,17 @@ __device__ __forceinline__ float dpp_add(float x)
     return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(
                                              0, __builtin_bit_cast(int, x), CTRL, ROWS, 0xf, false));
 }
+// Sum over each row of 16 lanes, returned to every lane of the row: DPP quad permutations
+// [1,0,3,2] and [2,3,0,1] (quads), then the half-row mirror (lane i with 7 - i: quad pairs) and
+// the row mirror (lane i with 15 - i: the two halves). Every source lane is inside the row.
+__device__ __forceinline__ float row16_sum(float x)
+{
+    x = dpp_add<0xb1, 0xf>(x);   // quad_perm [1,0,3,2]
+    x = dpp_add<0x4e, 0xf>(x);   // quad_perm [2,3,0,1]
+    x = dpp_add<0x141, 0xf>(x);  // row_half_mirror
+    x = dpp_add<0x140, 0xf>(x);  // row_mirror
+    return x;
+}
 __device__ __forceinline__ float wave_sum(float x)
 {
     x = dpp_add<0x111, 0xf>(x);  // row_shr:1
