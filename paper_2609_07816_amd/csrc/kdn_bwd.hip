@@ -68,7 +68,7 @@ struct BwRec {
 
 // Workspace of one backward call.
 struct BwMap {
-    size_t choff, summ, carry, rec, ckpt, dlt, dso, dkap, dal, acf, bcf, aux, lamp, total;
+    size_t choff, summ, carry, rec, ckpt, dlt, dso, dkap, dal, acf, bcf, aux, cmap, lpe, total;
     int maxch;
 };
 
@@ -97,7 +97,8 @@ inline BwMap bw_map(int variant, bool packed, int N, int B, int T, int H, int dk
     m.acf = take(ch * C * nchan * 4);
     m.bcf = take(ch * C * nchan * 4);
     m.aux = take(ch * C * 4);
-    m.lamp = take(ch * C * nchan * 4);
+    m.cmap = take(ch * nchan * 8);
+    m.lpe = take(ch * nchan * 4);
     m.total = off;
     return m;
 }
@@ -111,7 +112,9 @@ struct Args {
     float mu, scale;
     const float2* carry;
     char* rec;
-    float *ckpt, *dlt, *dso, *dkap, *dal, *acf, *bcf, *aux, *lamp;
+    float *ckpt, *dlt, *dso, *dkap, *dal, *acf, *bcf, *aux;
+    float2* cmap;  // per (chunk, head, variance channel): the chunk's reverse map of the adjoint
+    float* lpe;    // per (chunk, head, variance channel): the adjoint at the chunk's end
 };
 
 template <class TI>
@@ -1369,10 +1372,33 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
                 a.aux[gh * C + t] = dbeta;
             }
     }
+    // the chunk's map of the variance adjoint from its end to its start, per channel:
+    // lambda_start = m.x lambda_end + m.y, the steps lambda_{t-1} = A_t lambda_t + B_t composed
+    // from the last token down (the coefficients above are this workgroup's own writes)
+    __syncthreads();
+    if (tid < NCHAN) {
+        float mx = 1.f, my = 0.f;
+        for (int tb = C - 16; tb >= 0; tb -= 16) {
+            float av[16], bv[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                av[e] = a.acf[(gh * C + tb + e) * NCHAN + tid];
+                bv[e] = a.bcf[(gh * C + tb + e) * NCHAN + tid];
+            }
+#pragma unroll
+            for (int e = 15; e >= 0; --e) {
+                mx *= av[e];
+                my = fmaf(av[e], my, bv[e]);
+            }
+        }
+        a.cmap[gh * NCHAN + tid] = make_float2(mx, my);
+    }
 }
 
 // ------------------------------------------------------------------------------------------
-// bw_scan: the variance adjoint backwards in time, one thread per (sequence, head, channel)
+// bw_scan: the variance adjoint backwards over the chunks, one thread per (sequence, head,
+// channel): each chunk's composed map (from bw_grad) applied in reverse; the adjoint at every
+// chunk's end is kept for bw_final, which replays the chunk's tokens from it
 // ------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void bw_scan(Args a, int nchan)
 {
@@ -1384,19 +1410,19 @@ __global__ __launch_bounds__(64) void bw_scan(Args a, int nchan)
     seq_span(a.cm, n, t0, t1);
     seq_chunks<C>(a.cm, n, t0, t1, g0, nch);
     float lp = a.dP_T ? a.dP_T[(size_t)slot * nchan + c] : 0.f;
-    for (int ci = nch - 1; ci >= 0; --ci) {
-        const size_t base = ((size_t)(g0 + ci) * H + h) * C;
-        for (int tb = C - 16; tb >= 0; tb -= 16) {
-            float av[16], bv[16];
+    for (int cb = nch; cb > 0; cb -= 16) {  // chunks cb - 1 down to max(cb - 16, 0)
+        float2 mv[16];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                av[e] = a.acf[(base + tb + e) * nchan + c];
-                bv[e] = a.bcf[(base + tb + e) * nchan + c];
-            }
+        for (int e = 0; e < 16; ++e) {
+            const int ci = max(cb - 1 - e, 0);
+            mv[e] = a.cmap[((size_t)(g0 + ci) * H + h) * nchan + c];
+        }
 #pragma unroll
-            for (int e = 15; e >= 0; --e) {
-                a.lamp[(base + tb + e) * nchan + c] = lp;
-                lp = fmaf(av[e], lp, bv[e]);
+        for (int e = 0; e < 16; ++e) {
+            const int ci = cb - 1 - e;
+            if (ci >= 0) {
+                a.lpe[((size_t)(g0 + ci) * H + h) * nchan + c] = lp;
+                lp = fmaf(mv[e].x, lp, mv[e].y);
             }
         }
     }
@@ -1427,6 +1453,26 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
     const float* dkap = a.dkap + gh * C * DK;
     const float* dal = a.dal + gh * C * DK;
     const float mu = a.mu;
+    // the variance adjoint at every token of the chunk, replayed from its value at the chunk's
+    // end: lambda_{t-1} = A_t lambda_t + B_t
+    __shared__ float s_lp[C * NCHAN];
+    if (tid < NCHAN) {
+        float lp = a.lpe[gh * NCHAN + tid];
+        for (int tb = C - 16; tb >= 0; tb -= 16) {
+            float av[16], bv[16];
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                av[e] = a.acf[(gh * C + tb + e) * NCHAN + tid];
+                bv[e] = a.bcf[(gh * C + tb + e) * NCHAN + tid];
+            }
+#pragma unroll
+            for (int e = 15; e >= 0; --e) {
+                s_lp[(tb + e) * NCHAN + tid] = lp;
+                lp = fmaf(av[e], lp, bv[e]);
+            }
+        }
+    }
+    __syncthreads();
     for (int j = 0; j < C / 4; ++j) {
         const int t = (C / 4) * w + j;
         if (t >= L) break;  // uniform per wave
@@ -1439,7 +1485,7 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
                 const float kk = ld<TI>(a.k, row * DK + i), al = ld<TI>(a.alpha, row * DK + i);
                 const float ph = phat[t * DK + i], pp = pprv[t * DK + i];
                 const float dkp = dkap[t * DK + i];
-                const float lp = a.lamp[(gh * C + t) * NCHAN + i];
+                const float lp = s_lp[t * NCHAN + i];
                 const float u = mu * kk * kk / rr, gg = 1.f + u * ph, ig2 = 1.f / (gg * gg);
                 const float dph = dkp * kk / dn + dden * kk * kk + lp * ig2;
                 const float du = -lp * ph * ph * ig2;
@@ -1452,7 +1498,7 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
             if (lane == 0) a.dr[row] = dden - s2 / (rr * rr);
         } else {
             const float dbeta = aux, bh = phat[t * DK], pp = pprv[t * DK];
-            const float lp = a.lamp[gh * C + t];
+            const float lp = s_lp[t];
             float sk = 0.f, sa = 0.f, sd = 0.f;
             for (int i = lane; i < DK; i += 64) {
                 const float kk = ld<TI>(a.k, row * DK + i);
@@ -1566,7 +1612,8 @@ hipError_t run(const BwdCall& bc, hipStream_t st)
     a.acf = (float*)(ws + m.acf);
     a.bcf = (float*)(ws + m.bcf);
     a.aux = (float*)(ws + m.aux);
-    a.lamp = (float*)(ws + m.lamp);
+    a.cmap = (float2*)(ws + m.cmap);
+    a.lpe = (float*)(ws + m.lpe);
     static bool attr = false;
     if (!attr) {
         if ((e = lds_attr(bw_prep<TI, DK, VARIANT, APC>, PrepLds<DK>::TOTAL)) != hipSuccess ||
