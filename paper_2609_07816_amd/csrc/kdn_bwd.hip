@@ -922,7 +922,8 @@ struct GradLds {
     static constexpr size_t OFF_P6 = OFF_CP + (size_t)4 * DK * 4;  // [DK]
     static constexpr size_t OFF_BT = OFF_P6 + (size_t)DK * 4;      // block totals [4][DK]
     static constexpr size_t OFF_RP = OFF_BT + (size_t)4 * DK * 4;  // row sums [2][3][C]
-    static constexpr size_t TOTAL = al16(OFF_RP + (size_t)6 * C * 4);
+    static constexpr size_t OFF_BM = al16(OFF_RP + (size_t)6 * C * 4);  // block maps [4][DK]
+    static constexpr size_t TOTAL = al16(OFF_BM + (size_t)4 * DK * 8);
 };
 
 template <class TI, int DK, int VARIANT, bool APC>
@@ -950,6 +951,7 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     float* s_p6 = (float*)(smem + LY::OFF_P6);
     float* s_bt = (float*)(smem + LY::OFF_BT);
     float* s_rp = (float*)(smem + LY::OFF_RP);
+    float2* s_bm = (float2*)(smem + LY::OFF_BM);
 
     const int H = a.H, DV = a.DV;
     const int g = (int)(blockIdx.x / H), h = (int)(blockIdx.x % H);
@@ -1335,6 +1337,7 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
             dal[t * DK + i] = t < L ? (suf[k][r] + off) / alv[k][r] : 0.f;
         }
         if constexpr (DIAG) {
+            float av[4], bv[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * rb + 4 * lg + r;
@@ -1344,10 +1347,29 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
                 const float kv = kvv[k][r], al = alv[k][r];
                 const float u = a.mu * kv * kv / rr, gg = 1.f + u * phv[k][r];
                 const float c = gpa[k][r] * kv / dn + dden * kv * kv;
-                a.acf[(gh * C + t) * NCHAN + i] = ok ? al * al / (gg * gg) : 1.f;
-                a.bcf[(gh * C + t) * NCHAN + i] = ok ? al * al * c : 0.f;
+                av[r] = ok ? al * al / (gg * gg) : 1.f;
+                bv[r] = ok ? al * al * c : 0.f;
+                a.acf[(gh * C + t) * NCHAN + i] = av[r];
+                a.bcf[(gh * C + t) * NCHAN + i] = bv[r];
                 if (k == 0 && cw == 0 && li == 0) a.aux[gh * C + t] = dden;
             }
+            // the block's map of the variance adjoint (lambda_start = mx lambda_end + my): the
+            // lane's rows composed from the last down, then the lane groups in time order
+            // (f o g: x -> f.x (g.x x + g.y) + f.y)
+            float mx = 1.f, my = 0.f;
+#pragma unroll
+            for (int r = 3; r >= 0; --r) {
+                mx *= av[r];
+                my = fmaf(av[r], my, bv[r]);
+            }
+            float px = __shfl(mx, lane + 16, 64), py = __shfl(my, lane + 16, 64);
+            my = fmaf(mx, py, my);  // groups 0, 2: own rows after the next group's
+            mx *= px;
+            px = __shfl(mx, lane + 32, 64);
+            py = __shfl(my, lane + 32, 64);
+            my = fmaf(mx, py, my);  // group 0: rows 0-7 after rows 8-15
+            mx *= px;
+            if (lg == 0) s_bm[rb * DK + i] = make_float2(mx, my);
         }
     }
     if constexpr (!DIAG) {  // one value per token: the row sums of both waves of the row block
@@ -1374,9 +1396,20 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
     }
     // the chunk's map of the variance adjoint from its end to its start, per channel:
     // lambda_start = m.x lambda_end + m.y, the steps lambda_{t-1} = A_t lambda_t + B_t composed
-    // from the last token down (the coefficients above are this workgroup's own writes)
+    // from the last token down: diagonal, the four row blocks' maps in time order; isotropic,
+    // the one chain's coefficients (this workgroup's own writes above)
     __syncthreads();
-    if (tid < NCHAN) {
+    if constexpr (DIAG) {
+        if (tid < DK) {
+            float2 m = s_bm[3 * DK + tid];
+#pragma unroll
+            for (int b = 2; b >= 0; --b) {
+                const float2 f = s_bm[b * DK + tid];
+                m = make_float2(f.x * m.x, fmaf(f.x, m.y, f.y));
+            }
+            a.cmap[gh * NCHAN + tid] = m;
+        }
+    } else if (tid < NCHAN) {
         float mx = 1.f, my = 0.f;
         for (int tb = C - 16; tb >= 0; tb -= 16) {
             float av[16], bv[16];
