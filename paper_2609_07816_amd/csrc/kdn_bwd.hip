@@ -1506,15 +1506,20 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
         }
     }
     __syncthreads();
+    constexpr int NI = (DK + 63) / 64;  // channels per lane: i = lane + 64 ii
+#pragma unroll 4
     for (int j = 0; j < C / 4; ++j) {
         const int t = (C / 4) * w + j;
-        if (t >= L) break;  // uniform per wave
+        if (t >= L) continue;  // uniform per wave
         const size_t row = (size_t)(c0 + t) * H + h;
         const float rr = ld<TI>(a.r, row), dn = den[t], aux = a.aux[gh * C + t];
         if constexpr (DIAG) {
             const float dden = aux;
             float s2 = 0.f;
-            for (int i = lane; i < DK; i += 64) {
+#pragma unroll
+            for (int ii = 0; ii < NI; ++ii) {
+                const int i = lane + 64 * ii;
+                if (i >= DK) break;
                 const float kk = ld<TI>(a.k, row * DK + i), al = ld<TI>(a.alpha, row * DK + i);
                 const float ph = phat[t * DK + i], pp = pprv[t * DK + i];
                 const float dkp = dkap[t * DK + i];
