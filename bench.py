@@ -37,6 +37,7 @@ sys.path.insert(0, ROOT)
 METRIC = "KDN forward tokens/s (H=16,d=128,T=4096) + % of MFMA/HBM roofline"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense float32 (the backward's products)
 FORWARD_KERNELS = "forward call: 4 kernels (chunk summaries, log-depth carry scan, per-chunk " \
                   "prep, walk over the chunks)"
 
@@ -243,6 +244,18 @@ def backward_bytes(tokens, H, dk, dv, es):
     return tokens * H * ((5 * dk + 2 * dv) * es + es + (4 * dk + dv + 1) * 4)
 
 
+def backward_flops(tokens, H, dk, dv, C=64):
+    """Dense flop count (a multiply-add is two) of the chunked backward per token-head, products
+    with a triangular factor counted at half:
+      replay: T and B (2 C dk), (I + T)^-1 (2 C^2 / 3);
+      forward walk: X = V - Kbar S, S update (2 x 2 dk dv), Delta = A X (C dv);
+      reverse walk: Ktail dS_out, dS_in's two products (3 x 2 dk dv), B^T dO and A^T dDelta
+        (2 x C dv);
+      gradients: Psi S_in^T, dO S_in^T, Delta dS_out^T (3 x 2 dk dv), dO Delta^T and
+        Psi Delta^T (2 x C dv), the four T/B terms (4 C dk)."""
+    return tokens * H * (16 * dk * dv + 5 * C * dv + 6 * C * dk + 2 * C * C / 3.0)
+
+
 def bench_backward(torch, kdn, x, steps):
     """kdn_backward at the headline shape, with random incoming adjoints of o, S_T and P_T."""
     B, T, H, d = x["k"].shape
@@ -253,8 +266,12 @@ def bench_backward(torch, kdn, x, steps):
     dP = torch.randn((B, H, d), generator=g, device="cuda")
     ms = time_calls(torch, lambda: kdn.backward("diag", *[x[n] for n in NAMES], mu=float(d),
                                                 dO=dO, dS_T=dS, dP_T=dP), steps, 3)
+    flops = backward_flops(B * T, H, d, d)
+    mean = float(np.mean(ms))
     return summary(ms, backward_bytes(B * T, H, d, d, 2), B * T,
                    {"workload": "diag-bwd-B4-H16-T4096-d128 (float32 gradients)",
+                    "flops": flops, "mfma_peak_tflops": FP32_MFMA_PEAK_TFLOPS,
+                    "mfma_frac": round(flops / (mean * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
                     "kernels": "backward: chunk summaries, carry scan, per-chunk replay, forward "
                                "walk, reverse walk, per-chunk gradients, variance-adjoint scan, "
                                "per-token gain gradients"})
