@@ -13,7 +13,8 @@
 //   3. replay of every chunk from its carry, emitting p_hat and the gain before each token's
 //      matrix is applied (eqs. chunk-gain-local-prefix, chunk-gain-emission).
 // Every product is rescaled by an exact power of two, which leaves n / d unchanged.
-// The diagonal chain gives every channel its own thread (channels are independent); the
+// The diagonal chain gives every (chunk, head) one wavefront whose lanes hold the channels
+// (channels are independent; the gain's normalisation sums them across the wavefront); the
 // isotropic chain gives every token a lane and scans inside the wavefront.
 #include "kdn_device.h"
 
@@ -57,73 +58,208 @@ __device__ __forceinline__ Mat2 shfl_up_mat(const Mat2& x, int off)
 // Diagonal chain
 // ------------------------------------------------------------------------------------------
 
-// Pass 1: one thread per channel composes the chunk's token matrices (later on the left).
+// One wavefront per (chunk, head): lane l holds the CPL adjacent channels from l * CPL
+// (CPL = 2 for dk = 128, else 1; lanes past dk idle for dk < 64) and reads them with one load
+// per array and token. The chunk's tokens are fetched G at a time into registers, the next
+// group while the current one is computed; rows past the chunk's end are clamped to its last
+// token, so every load is in bounds and unconditional.
+template <class E, int N> struct Lanes;
+template <> struct Lanes<float, 1> { typedef float T; };
+template <> struct Lanes<float, 2> { typedef float T __attribute__((ext_vector_type(2))); };
+template <> struct Lanes<bf16, 1> { typedef bf16 T; };
+template <> struct Lanes<bf16, 2> { typedef bf16 T __attribute__((ext_vector_type(2))); };
+
+__device__ __forceinline__ float lane_el(float v, int) { return v; }
+__device__ __forceinline__ float lane_el(bf16 v, int) { return (float)v; }
+template <class V> __device__ __forceinline__ float lane_el(const V& v, int i)
+{
+    return (float)v[i];
+}
+
+// Row access through a buffer descriptor of one wavefront-uniform row (built on the scalar
+// unit per row): the lane's byte offset stays in one vector register and no per-row address
+// arithmetic runs on the vector unit; rows are addressed with 64-bit pointers, so tensors of any
+// size are reachable.
+__device__ __forceinline__ rsrc_t row_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+template <int B> struct RowIO;
+template <> struct RowIO<2> {
+    template <class V> static __device__ __forceinline__ V load(rsrc_t r, uint32_t off)
+    {
+        const short x = (short)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+        return __builtin_bit_cast(V, x);
+    }
+};
+template <> struct RowIO<4> {
+    template <class V> static __device__ __forceinline__ V load(rsrc_t r, uint32_t off)
+    {
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+    }
+    static __device__ __forceinline__ void store(float x, float, rsrc_t r, uint32_t off)
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, (int)off, 0, 0);
+    }
+};
+template <> struct RowIO<8> {
+    template <class V> static __device__ __forceinline__ V load(rsrc_t r, uint32_t off)
+    {
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+    }
+    static __device__ __forceinline__ void store(float x, float y, rsrc_t r, uint32_t off)
+    {
+        typedef unsigned u2 __attribute__((ext_vector_type(2)));
+        const u2 v = {__float_as_uint(x), __float_as_uint(y)};
+        __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)off, 0, 0);
+    }
+};
+
+template <class E, int DK, int CPL_>
+struct DiagLanes {
+    static constexpr int CPL = CPL_;
+    static constexpr int G = 8;  // tokens per prefetch group
+    typedef typename Lanes<E, CPL>::T VT;
+    struct Group {
+        VT k[G], al[G], w[G];
+        float r[G];
+    };
+    // loads tokens j0 .. j0 + G - 1 of the chunk starting at c0 (length L); every row pointer
+    // is wavefront-uniform and the lane adds its byte offset lo
+    static __device__ __forceinline__ void load(Group& b, const E* k, const E* alpha,
+                                                const E* omega, const E* r, int c0, int L,
+                                                int j0, int H, int h, uint32_t lo)
+    {
+#pragma unroll
+        for (int jj = 0; jj < G; ++jj) {
+            const size_t row = (size_t)(c0 + min(j0 + jj, L - 1)) * H + h;
+            typedef RowIO<sizeof(VT)> IO;
+            b.k[jj] = IO::template load<VT>(row_rsrc(k + row * DK, DK * sizeof(E)), lo);
+            b.al[jj] = IO::template load<VT>(row_rsrc(alpha + row * DK, DK * sizeof(E)), lo);
+            b.w[jj] = IO::template load<VT>(row_rsrc(omega + row * DK, DK * sizeof(E)), lo);
+            b.r[jj] = ldf(r, row);
+        }
+    }
+};
+
+// Pass 1: each lane composes its channels' token matrices over the chunk (later on the left).
 template <class E, int DK>
-__global__ __launch_bounds__(DK) void diag_summary_kernel(
+__global__ __launch_bounds__(64) void diag_summary_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
     const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
 {
-    const int g = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+    typedef DiagLanes<E, DK, (DK >= 64 ? DK / 64 : 1)> DL;
+    constexpr int CPL = DL::CPL, G = DL::G;
+    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
-    Mat2 acc = {1.f, 0.f, 0.f, 1.f};
-    for (int t = c0; t < c1; ++t) {
-        const size_t row = (size_t)t * H + h;
-        const float al = ldf(alpha, row * DK + c), kk = ldf(k, row * DK + c);
-        const float a = al * al, u = mu * kk * kk / ldf(r, row);
-        acc = mul(token_mat(a, ldf(omega, row * DK + c), u), acc);
+    const bool act = lane * CPL < DK;
+    const int c = act ? lane * CPL : 0, L = c1 - c0;
+    const uint32_t lo = c * sizeof(E);
+    float m[CPL][4];
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) {
+        m[i][0] = m[i][3] = 1.f;
+        m[i][1] = m[i][2] = 0.f;
     }
-    summ[((size_t)g * H + h) * DK + c] = make_float4(acc.a, acc.b, acc.c, acc.d);
+    typename DL::Group ga, gb;
+    auto step = [&](const typename DL::Group& b, int j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int jj = 0; jj < G; ++jj) {
+            if (j0 + jj >= L) break;
+            const float mur = mu * __builtin_amdgcn_rcpf(b.r[jj]);
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) {
+                const float al = lane_el(b.al[jj], i), kk = lane_el(b.k[jj], i);
+                mob_left(m[i], al * al, lane_el(b.w[jj], i), mur * kk * kk);
+                rescale4(m[i]);
+            }
+        }
+    };
+    DL::load(ga, k, alpha, omega, r, c0, L, 0, H, h, lo);
+    for (int j0 = 0; j0 < L; j0 += 2 * G) {
+        if (j0 + G < L) DL::load(gb, k, alpha, omega, r, c0, L, j0 + G, H, h, lo);
+        step(ga, j0);
+        if (j0 + G >= L) break;
+        if (j0 + 2 * G < L) DL::load(ga, k, alpha, omega, r, c0, L, j0 + 2 * G, H, h, lo);
+        step(gb, j0 + G);
+    }
+    if (act) {
+#pragma unroll
+        for (int i = 0; i < CPL; ++i)
+            summ[((size_t)g * H + h) * DK + c + i] =
+                make_float4(m[i][0], m[i][1], m[i][2], m[i][3]);
+    }
 }
 
 // Pass 3: replay each chunk from its carry; p_hat_t = a_t n/d + w_t before M_t is applied;
-// kappa_t = p_hat_t k_t / (r_t + sum_i p_hat_ti k_ti^2) (eq. chunk-gain-emission).
+// kappa_t = p_hat_t k_t / (r_t + sum_i p_hat_ti k_ti^2) (eq. chunk-gain-emission), the sum over
+// the head's channels taken across the wavefront with DPP.
 template <class E, int DK>
-__global__ __launch_bounds__(DK) void diag_emit_kernel(
+__global__ __launch_bounds__(64) void diag_emit_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
     const E* __restrict__ r, const float2* __restrict__ carry, ChunkMap cm, int H, float mu,
     float* __restrict__ kappa_out, float* __restrict__ phat_out, float* __restrict__ P_T)
 {
-    __shared__ float s_part[CG][DK + 1];
-    __shared__ float s_rden[CG];
-    const int g = blockIdx.x, h = blockIdx.y, c = threadIdx.x;
+    typedef DiagLanes<E, DK, (DK >= 64 ? DK / 64 : 1)> DL;
+    constexpr int CPL = DL::CPL, G = DL::G;
+    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
-    const float2 z = carry[((size_t)g * H + h) * DK + c];
-    float zn = z.x, zd = z.y;
-    float pk[CG];
-    const int L = c1 - c0;
+    const bool act = lane * CPL < DK;
+    const int c = act ? lane * CPL : 0, L = c1 - c0;
+    const uint32_t lo = c * sizeof(E), lo4 = c * 4;
+    float zn[CPL], zd[CPL];
 #pragma unroll
-    for (int j = 0; j < CG; ++j) {
-        if (j < L) {
-            const size_t row = (size_t)(c0 + j) * H + h;
-            const float al = ldf(alpha, row * DK + c), kk = ldf(k, row * DK + c);
-            const float a = al * al, w = ldf(omega, row * DK + c);
-            const float u = mu * kk * kk / ldf(r, row);
-            const float n2 = fmaf(a, zn, w * zd);     // n_t
-            const float ph = n2 / zd;                  // p_hat_t = a n_{t-1}/d_{t-1} + w
-            zd = fmaf(u, n2, zd);                      // d_t = u a n + (1 + u w) d = u n_t + d
-            zn = n2;
-            renorm2(zn, zd);
-            pk[j] = ph * kk;
-            s_part[j][c] = ph * kk * kk;
-            if (phat_out) phat_out[row * DK + c] = ph;
+    for (int i = 0; i < CPL; ++i) {
+        const float2 z = carry[((size_t)g * H + h) * DK + c + i];
+        zn[i] = z.x;
+        zd[i] = z.y;
+    }
+    typename DL::Group ga, gb;
+    auto step = [&](const typename DL::Group& b, int j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int jj = 0; jj < G; ++jj) {
+            if (j0 + jj >= L) break;
+            const size_t row = (size_t)(c0 + j0 + jj) * H + h;
+            const float rr = b.r[jj], mur = mu * __builtin_amdgcn_rcpf(rr);
+            float ph[CPL], pk[CPL], part = 0.f;
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) {
+                const float al = lane_el(b.al[jj], i), kk = lane_el(b.k[jj], i);
+                const float n2 = fmaf(al * al, zn[i], lane_el(b.w[jj], i) * zd[i]);  // n_t
+                ph[i] = n2 * __builtin_amdgcn_rcpf(zd[i]);          // a n_{t-1}/d_{t-1} + w
+                zd[i] = fmaf(mur * kk * kk, n2, zd[i]);             // d_t = u n_t + d_{t-1}
+                zn[i] = n2;
+                rescale2(zn[i], zd[i]);
+                pk[i] = ph[i] * kk;
+                part = fmaf(pk[i], kk, part);
+            }
+            const float rden = __builtin_amdgcn_rcpf(rr + wave_sum(act ? part : 0.f));
+            if (act) {
+                typedef RowIO<4 * CPL> IO;
+                IO::store(pk[0] * rden, pk[CPL - 1] * rden,
+                          row_rsrc(kappa_out + row * DK, DK * 4), lo4);
+                if (phat_out)
+                    IO::store(ph[0], ph[CPL - 1], row_rsrc(phat_out + row * DK, DK * 4), lo4);
+            }
         }
+    };
+    DL::load(ga, k, alpha, omega, r, c0, L, 0, H, h, lo);
+    for (int j0 = 0; j0 < L; j0 += 2 * G) {
+        if (j0 + G < L) DL::load(gb, k, alpha, omega, r, c0, L, j0 + G, H, h, lo);
+        step(ga, j0);
+        if (j0 + G >= L) break;
+        if (j0 + 2 * G < L) DL::load(ga, k, alpha, omega, r, c0, L, j0 + 2 * G, H, h, lo);
+        step(gb, j0 + G);
     }
-    if (last && P_T) P_T[((size_t)n * H + h) * DK + c] = zn / zd;
-    __syncthreads();
-    // den_t = r_t + sum_c p_hat k^2 : DK threads reduce CG rows
-    for (int j = c; j < L; j += DK) {
-        float s = 0.f;
-        for (int i = 0; i < DK; ++i) s += s_part[j][i];
-        s_rden[j] = 1.f / (ldf(r, (size_t)(c0 + j) * H + h) + s);
-    }
-    __syncthreads();
+    if (last && P_T && act) {
 #pragma unroll
-    for (int j = 0; j < CG; ++j)
-        if (j < L) kappa_out[((size_t)(c0 + j) * H + h) * DK + c] = pk[j] * s_rden[j];
+        for (int i = 0; i < CPL; ++i) P_T[((size_t)n * H + h) * DK + c + i] = zn[i] / zd[i];
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -246,7 +382,7 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
         return e;
     const dim3 grid(maxch, sa.H);
     if (variant == 0) {
-        hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
+        hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(64), 0, st, k_, a_, w_, r_,
                            cm, sa.H, mu, summ);
     } else if (apc) {
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,
@@ -259,7 +395,7 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
     if ((e = launch_carry_scan(summ, P0, cm, CG, sa.H, nchan, carry, P_T, st)) != hipSuccess)
         return e;
     if (variant == 0) {
-        hipLaunchKernelGGL((diag_emit_kernel<E, DK>), grid, dim3(DK), 0, st, k_, a_, w_, r_,
+        hipLaunchKernelGGL((diag_emit_kernel<E, DK>), grid, dim3(64), 0, st, k_, a_, w_, r_,
                            carry, cm, sa.H, mu, gain_out, phat_out, P_T);
     } else if (apc) {
         hipLaunchKernelGGL((iso_emit_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,

@@ -165,6 +165,48 @@ def test_gain_scan(variant, apc, dtype, packed):
     check("P_T", host_f64(P), ref["P_T"], 1e-5)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [32, 128])
+@pytest.mark.parametrize("variant", ["diag", "iso"])
+def test_gain_scan_head_sizes(variant, d, dtype):
+    """Head sizes 32 (half the lanes of the diagonal kernels idle) and 128 (two channels per
+    lane) on a packed batch whose chunks end at every offset class: 1, 3, 64, 130, 191."""
+    from paper_2609_07816_amd import kdn
+    lens = [3, 64, 130, 1, 191]
+    x = W.draw_inputs(variant, dtype, 1, sum(lens), 2, d, d, seed=65, lengths=lens,
+                      random_state=True)
+    dd = to_device(x)
+    f = kdn.gain_diag if variant == "diag" else kdn.gain_iso
+    g, ph, P = f(dd["k"], dd["alpha"], dd["omega"], dd["r"], P0=dd["P0"], cu_seqlens=dd["cu"],
+                 mu=x.mu)
+    torch.cuda.synchronize()
+    ref = run_oracle_forward(x, traces=True)
+    gname, pname = ("kappa", "phat") if variant == "diag" else ("beta", "bhat")
+    check(gname, host_f64(g), ref[gname], 1e-5)
+    check(pname, host_f64(ph), ref[pname], 1e-5)
+    check("P_T", host_f64(P), ref["P_T"], 1e-5)
+
+
+def test_gain_scan_full_workload_sampled():
+    """The Diagonal gain scan at B4 T4096 H16 d128 bf16 (the gain bench's shape) in the launch
+    configuration the bench times; three (row, head) chains against the oracle."""
+    from paper_2609_07816_amd import kdn
+    x = W.draw_workload(2)
+    d = to_device(x)
+    g0, _, _ = kdn.gain_diag(d["k"], d["alpha"], d["omega"], d["r"], P0=d["P0"], mu=x.mu,
+                             want_phat=False)
+    g, ph, P = kdn.gain_diag(d["k"], d["alpha"], d["omega"], d["r"], P0=d["P0"], mu=x.mu)
+    torch.cuda.synchronize()
+    assert torch.equal(g0, g), "kappa must not depend on whether p_hat is written"
+    chains = [(0, 0), (x.B - 1, x.H - 1), (1, 7)]
+    g, ph, P = host_f64(g), host_f64(ph), host_f64(P)
+    for (b, h), ref in zip(chains, run_oracle_forward(x, chains=chains, traces=True)):
+        print(f" chain (b={b}, h={h})", flush=True)
+        check("kappa", g[b:b + 1, :, h:h + 1], ref["kappa"], 1e-5)
+        check("phat", ph[b:b + 1, :, h:h + 1], ref["phat"], 1e-5)
+        check("P_T", P[b:b + 1, h:h + 1], ref["P_T"], 1e-5)
+
+
 # ---------------------------------------------------------------------------------------------
 # decode
 # ---------------------------------------------------------------------------------------------
