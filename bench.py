@@ -227,14 +227,26 @@ def bench_decode_workload(torch, kdn, steps):
     return out
 
 
-def bench_gain(torch, kdn, x, steps):
+def bench_gain(torch, kdn, x, steps, copies=4):
     """The gain scan alone (kdn_gain_diag) at the headline shape: chunk summaries, carry scan
-    and emission of the float32 gains."""
+    and emission of the float32 gains. The calls take `copies` copies of the inputs in turn
+    (4 x 201 MB, more than the 256 MB last-level cache), so that every call reads its inputs
+    from HBM, as the first call on fresh inputs does."""
     B, T, H, d = x["k"].shape
-    ms = time_calls(torch, lambda: kdn.gain_diag(x["k"], x["alpha"], x["omega"], x["r"],
-                                                 mu=float(d), want_phat=False), steps, 3)
+    names = ("k", "alpha", "omega", "r")
+    sets = [x] + [{n: x[n].clone() for n in names} for _ in range(copies - 1)]
+    turn = [0]
+
+    def call():
+        y = sets[turn[0] % copies]
+        turn[0] += 1
+        return kdn.gain_diag(y["k"], y["alpha"], y["omega"], y["r"], mu=float(d),
+                             want_phat=False)
+
+    ms = time_calls(torch, call, steps, 3)
     return summary(ms, gain_bytes(B * T, H, d, 2), B * T,
                    {"workload": "diag-gain-scan-B4-H16-T4096-d128 (kappa out, float32)",
+                    "inputs": f"{copies} copies taken in turn",
                     "kernels": "gain scan: chunk summaries, carry scan, emission"})
 
 

@@ -151,7 +151,8 @@ __global__ __launch_bounds__(64) void diag_summary_kernel(
 {
     typedef DiagLanes<E, DK, (DK >= 64 ? DK / 64 : 1)> DL;
     constexpr int CPL = DL::CPL, G = DL::G;
-    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
+    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
@@ -205,7 +206,8 @@ __global__ __launch_bounds__(64) void diag_emit_kernel(
 {
     typedef DiagLanes<E, DK, (DK >= 64 ? DK / 64 : 1)> DL;
     constexpr int CPL = DL::CPL, G = DL::G;
-    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
+    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
@@ -299,7 +301,8 @@ __global__ __launch_bounds__(64) void iso_summary_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
     const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
 {
-    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
+    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
@@ -327,7 +330,8 @@ __global__ __launch_bounds__(64) void iso_emit_kernel(
     const E* __restrict__ r, const float2* __restrict__ carry, ChunkMap cm, int H, float mu,
     float* __restrict__ beta_out, float* __restrict__ bhat_out, float* __restrict__ P_T)
 {
-    const int g = blockIdx.x, h = blockIdx.y, lane = threadIdx.x;
+    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
+    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
     int n, c0, c1;
     bool last;
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
@@ -380,7 +384,8 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
     if (sa.cu_seqlens &&
         (e = launch_chunk_table(sa.cu_seqlens, sa.N, cm.ntok, CG, maxch, choff, st)) != hipSuccess)
         return e;
-    const dim3 grid(maxch, sa.H);
+    // one workgroup per (chunk, head), h * maxch + g in a 1-D grid (chunks of a head adjacent)
+    const dim3 grid((unsigned)((size_t)maxch * sa.H));
     if (variant == 0) {
         hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(64), 0, st, k_, a_, w_, r_,
                            cm, sa.H, mu, summ);

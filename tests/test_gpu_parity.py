@@ -207,6 +207,26 @@ def test_gain_scan_full_workload_sampled():
         check("P_T", P[b:b + 1, h:h + 1], ref["P_T"], 1e-5)
 
 
+def test_many_heads_gain_and_forward():
+    """H = 66000 heads (more than a grid's y or z extent may hold), T = 3, d = 16: the gain
+    scans and the forward index their workgroups over (chunk, head) in one grid dimension."""
+    from paper_2609_07816_amd import kdn
+    H = 66000
+    for variant in ("diag", "iso"):
+        x = W.draw_inputs(variant, "f32", 1, 3, H, 16, 16, seed=66, random_state=True)
+        d = to_device(x)
+        f = kdn.gain_diag if variant == "diag" else kdn.gain_iso
+        g, ph, P = f(d["k"], d["alpha"], d["omega"], d["r"], P0=d["P0"], mu=x.mu)
+        o, S, P2 = run_gpu_forward(x)
+        torch.cuda.synchronize()
+        ref = run_oracle_forward(x, traces=True)
+        gname = "kappa" if variant == "diag" else "beta"
+        check(f"{variant} {gname}", host_f64(g), ref[gname], 1e-5)
+        check(f"{variant} P_T (gain)", host_f64(P), ref["P_T"], 1e-5)
+        check(f"{variant} o", o, ref["o"], TOL["f32"])
+        check(f"{variant} P_T (forward)", P2, ref["P_T"], TOL["f32"])
+
+
 # ---------------------------------------------------------------------------------------------
 # decode
 # ---------------------------------------------------------------------------------------------
