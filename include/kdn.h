@@ -230,7 +230,8 @@ kdn_status_t kdn_decode_step_layer(int32_t variant, const void* q, const void* k
  *   Diagonal: kappa_out [B,T,H,dk] float32 (kappa_t), phat_out [B,T,H,dk] float32 or NULL
  *   (p_hat_t), P_T [N,H,dk] float32 or NULL.
  *   Isotropic: beta_out [B,T,H] float32 (beta_t), bhat_out [B,T,H] or NULL, P_T [N,H] or NULL.
- *   Inputs as in the forward (v, q are not needed). workspace: kdn_gain_workspace_bytes(...).
+ *   Inputs as in the forward (v, q are not needed), each smaller than 2 GiB
+ *   (KDN_ERR_UNSUPPORTED otherwise). workspace: kdn_gain_workspace_bytes(...).
  */
 kdn_status_t kdn_gain_diag(const void* k, const void* alpha, const void* omega, const void* r,
                            const float* P0, float* kappa_out, float* phat_out, float* P_T,

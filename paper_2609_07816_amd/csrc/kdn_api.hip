@@ -561,6 +561,9 @@ static kdn_status_t gain_common(int variant, const void* k, const void* alpha, c
                         {variant == 0 ? P0 : nullptr, "P0"},
                         {variant == 0 ? P_T : nullptr, "P_T"}});
     if (st != KDN_OK) return st;
+    if ((size_t)B * T * H * dk * esize(dtype) >= ((size_t)1 << 31))
+        return fail(KDN_ERR_UNSUPPORTED, "each input tensor must be smaller than 2 GiB (the "
+                    "chunk summaries address it with 32-bit offsets)");
     const size_t need = kdn::gain_workspace_bytes(variant, N, B, T, H, dk);
     if (!ws || ws_bytes < need)
         return fail(KDN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,

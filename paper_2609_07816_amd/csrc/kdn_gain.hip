@@ -13,10 +13,12 @@
 //   3. replay of every chunk from its carry, emitting p_hat and the gain before each token's
 //      matrix is applied (eqs. chunk-gain-local-prefix, chunk-gain-emission).
 // Every product is rescaled by an exact power of two, which leaves n / d unchanged.
-// The diagonal chain gives every (chunk, head) one wavefront whose lanes hold the channels
-// (channels are independent; the gain's normalisation sums them across the wavefront); the
-// isotropic chain gives every token a lane and scans inside the wavefront.
+// The diagonal chain takes the forward's chunk summaries (pass 1) and gives every (chunk, head)
+// one wavefront for the emission, its lanes holding the channels (channels are independent; the
+// gain's normalisation sums them across the wavefront); the isotropic chain gives every token a
+// lane and scans inside the wavefront.
 #include "kdn_device.h"
+#include "kdn_fwd.h"
 
 namespace kdn {
 namespace {
@@ -143,59 +145,7 @@ struct DiagLanes {
     }
 };
 
-// Pass 1: each lane composes its channels' token matrices over the chunk (later on the left).
-template <class E, int DK>
-__global__ __launch_bounds__(64) void diag_summary_kernel(
-    const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
-{
-    typedef DiagLanes<E, DK, (DK >= 64 ? DK / 64 : 1)> DL;
-    constexpr int CPL = DL::CPL, G = DL::G;
-    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
-    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
-    int n, c0, c1;
-    bool last;
-    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
-    const bool act = lane * CPL < DK;
-    const int c = act ? lane * CPL : 0, L = c1 - c0;
-    const uint32_t lo = c * sizeof(E);
-    float m[CPL][4];
-#pragma unroll
-    for (int i = 0; i < CPL; ++i) {
-        m[i][0] = m[i][3] = 1.f;
-        m[i][1] = m[i][2] = 0.f;
-    }
-    typename DL::Group ga, gb;
-    auto step = [&](const typename DL::Group& b, int j0) __attribute__((always_inline)) {
-#pragma unroll
-        for (int jj = 0; jj < G; ++jj) {
-            if (j0 + jj >= L) break;
-            const float mur = mu * __builtin_amdgcn_rcpf(b.r[jj]);
-#pragma unroll
-            for (int i = 0; i < CPL; ++i) {
-                const float al = lane_el(b.al[jj], i), kk = lane_el(b.k[jj], i);
-                mob_left(m[i], al * al, lane_el(b.w[jj], i), mur * kk * kk);
-                rescale4(m[i]);
-            }
-        }
-    };
-    DL::load(ga, k, alpha, omega, r, c0, L, 0, H, h, lo);
-    for (int j0 = 0; j0 < L; j0 += 2 * G) {
-        if (j0 + G < L) DL::load(gb, k, alpha, omega, r, c0, L, j0 + G, H, h, lo);
-        step(ga, j0);
-        if (j0 + G >= L) break;
-        if (j0 + 2 * G < L) DL::load(ga, k, alpha, omega, r, c0, L, j0 + 2 * G, H, h, lo);
-        step(gb, j0 + G);
-    }
-    if (act) {
-#pragma unroll
-        for (int i = 0; i < CPL; ++i)
-            summ[((size_t)g * H + h) * DK + c + i] =
-                make_float4(m[i][0], m[i][1], m[i][2], m[i][3]);
-    }
-}
-
-// Pass 3: replay each chunk from its carry; p_hat_t = a_t n/d + w_t before M_t is applied;
+// Pass 3 (pass 1 is the forward's summary kernel): replay each chunk from its carry; p_hat_t = a_t n/d + w_t before M_t is applied;
 // kappa_t = p_hat_t k_t / (r_t + sum_i p_hat_ti k_ti^2) (eq. chunk-gain-emission), the sum over
 // the head's channels taken across the wavefront with DPP.
 template <class E, int DK>
@@ -387,8 +337,18 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
     // one workgroup per (chunk, head), h * maxch + g in a 1-D grid (chunks of a head adjacent)
     const dim3 grid((unsigned)((size_t)maxch * sa.H));
     if (variant == 0) {
-        hipLaunchKernelGGL((diag_summary_kernel<E, DK>), grid, dim3(64), 0, st, k_, a_, w_, r_,
-                           cm, sa.H, mu, summ);
+        // the forward's summary kernel: four waves per (chunk, head), each with its 16 tokens'
+        // loads in flight at once, the four block products composed in LDS
+        fwd::InArgs in = {};
+        in.q = k; in.k = k; in.alpha = alpha; in.omega = omega; in.r = r;
+        const size_t ntok = (size_t)sa.B * sa.T * sa.H;
+        in.bytes_k = (uint32_t)(ntok * DK * sizeof(E));
+        in.bytes_h = (uint32_t)(ntok * sizeof(E));
+        in.H = sa.H;
+        in.mu = mu;
+        hipLaunchKernelGGL((fwd::summary_kernel<E, fwd::VarCfg<E, DK, 0, true>>),
+                           dim3((unsigned)((size_t)maxch * sa.H)), dim3(fwd::NTH), 0, st, in, cm,
+                           summ);
     } else if (apc) {
         hipLaunchKernelGGL((iso_summary_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,
                            r_, cm, sa.H, mu, summ);

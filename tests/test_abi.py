@@ -93,6 +93,14 @@ def test_gain_argument_errors(L):
     st = L.kdn_gain_diag(*p[:4], None, p[4], None, None, None, 1, 1, 8, 2, 64, 1, F(-1.0),
                          P(30), need, None)
     assert st == kdn.KDN_ERR_INVALID_ARG
+    # an input tensor of 2 GiB or more (T = 2^20, H = 16, d 128 bf16: 4 GiB) is refused before
+    # the workspace is even looked at
+    for f in (L.kdn_gain_diag, L.kdn_gain_iso):
+        args = [*p[:4], None, p[4], None, None, None, 1, 1, 1 << 20, 16, 128, 1]
+        if f is L.kdn_gain_iso:
+            args.append(1)
+        st = f(*args, F(64.0), None, 0, None)
+        assert st == kdn.KDN_ERR_UNSUPPORTED
 
 
 def test_forward_workspace(L):
