@@ -79,6 +79,12 @@ def gain_bytes(tokens, H, dk, es):
     return tokens * H * (3 * dk * es + es + 4 * dk)
 
 
+def gain_iso_bytes(tokens, H, dk, es, apc):
+    """Minimum traffic of the isotropic gain scan alone: k (and alpha per channel) read once,
+    the per-head alpha, omega and r read once, beta written once in float32."""
+    return tokens * H * (dk * es * (2 if apc else 1) + (2 if apc else 3) * es + 4)
+
+
 # ---------------------------------------------------------------------------------------------
 # inputs drawn on the GPU (same laws as paper_2609_07816_amd/workloads.py)
 # ---------------------------------------------------------------------------------------------
@@ -171,6 +177,33 @@ def bench_iso(torch, kdn, steps):
     return summary(ms, forward_bytes(B * T, B, H, d, d, 2, "iso", apc=False), B * T,
                    {"workload": "iso-fwd-B4-H16-T2048-d128 (scalar gates)",
                     "kernels": FORWARD_KERNELS})
+
+
+def bench_gain_iso(torch, kdn, steps, copies=4):
+    """The isotropic gain scan alone (kdn_gain_iso) at workload 1's shape (B4 H16 T2048 d128
+    bf16), with scalar gates (workload 1's) and with gates per channel, on `copies` copies of the
+    inputs taken in turn (as for the diagonal gain scan)."""
+    B, T, H, d = 4, 2048, 16, 128
+    out = {}
+    for apc in (False, True):
+        x = gpu_inputs(torch, "iso", B, T, H, d, d, seed=1001, apc=apc)
+        names = ("k", "alpha", "omega", "r")
+        sets = [x] + [{n: x[n].clone() for n in names} for _ in range(copies - 1)]
+        turn = [0]
+
+        def call():
+            y = sets[turn[0] % copies]
+            turn[0] += 1
+            return kdn.gain_iso(y["k"], y["alpha"], y["omega"], y["r"], mu=float(d),
+                                want_phat=False)
+
+        ms = time_calls(torch, call, steps, 3)
+        gates = "per channel" if apc else "scalar"
+        out["gates_per_channel" if apc else "scalar_gates"] = summary(
+            ms, gain_iso_bytes(B * T, H, d, 2, apc), B * T,
+            {"workload": f"iso-gain-scan-B4-H16-T2048-d128 ({gates} gates, beta out, float32)",
+             "inputs": f"{copies} copies taken in turn"})
+    return out
 
 
 def bench_varlen(torch, kdn, W, steps):
@@ -398,8 +431,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--only", default="all",
-                    choices=["all", "headline", "iso", "varlen", "decode", "gain", "backward",
-                             "layer"],
+                    choices=["all", "headline", "iso", "varlen", "decode", "gain", "gain_iso",
+                             "backward", "layer"],
                     help="run only the headline forward or one other workload (profiling runs)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (used to "
@@ -426,8 +459,9 @@ def main():
                           "launches": 5}))
         return
     kdn.lib()
-    if args.only in ("iso", "varlen", "decode", "layer"):
+    if args.only in ("iso", "varlen", "decode", "layer", "gain_iso"):
         fn = {"iso": lambda: bench_iso(torch, kdn, args.steps),
+              "gain_iso": lambda: bench_gain_iso(torch, kdn, args.steps),
               "varlen": lambda: bench_varlen(torch, kdn, W, args.steps),
               "decode": lambda: bench_decode_workload(torch, kdn, args.steps),
               "layer": lambda: bench_layer(torch, kdn, args.steps)}[args.only]
@@ -504,6 +538,7 @@ def main():
         rec["workloads"] = {"iso_forward": bench_iso(torch, kdn, args.steps),
                             "varlen_forward": bench_varlen(torch, kdn, W, args.steps),
                             "gain_scan": bench_gain(torch, kdn, dev, args.steps),
+                            "gain_scan_iso": bench_gain_iso(torch, kdn, args.steps),
                             "backward": bench_backward(torch, kdn, dev, args.steps),
                             "layer_forward": bench_layer(torch, kdn, args.steps)}
         rec["workloads"].update(bench_decode_workload(torch, kdn, args.steps))

@@ -218,62 +218,71 @@ __global__ __launch_bounds__(64) void diag_emit_kernel(
 // Isotropic chain: one lane per token of the chunk
 // ------------------------------------------------------------------------------------------
 
-// Token coefficients of the isotropic chain: a = mean_i alpha_i^2 (or alpha^2), w = omega,
-// u = mu ||k||^2 / (dk r); also returns ||k||^2.
+// ||k_t||^2 and sum_i alpha_ti^2 (per-channel gates) of the chunk's tokens, token t's sums
+// returned to lane t: the wavefront reads each row once with its lanes over the channels (CPL
+// adjacent channels per lane, as in the diagonal emission), G rows ahead, and sums across the
+// lanes by DPP. All 64 lanes must be active.
 template <class E, int DK, bool APC>
-__device__ __forceinline__ void iso_coeffs(const E* k, const E* alpha, const E* omega,
-                                           const E* r, size_t row, float mu, float& a, float& w,
-                                           float& u, float& nk)
+__device__ __forceinline__ void iso_row_sums(const E* k, const E* alpha, int c0, int L, int H,
+                                             int h, int lane, float& nk, float& sa)
 {
-    float sa = 0.f, sk = 0.f;
-#pragma unroll 8
-    for (int i = 0; i < DK; ++i) {
-        const float kk = ldf(k, row * DK + i);
-        sk += kk * kk;
-        if (APC) {
-            const float al = ldf(alpha, row * DK + i);
-            sa += al * al;
-        }
-    }
-    if (APC) {
-        a = sa / (float)DK;
-    } else {
-        const float al = ldf(alpha, row);
-        a = al * al;
-    }
-    w = ldf(omega, row);
-    nk = sk;
-    u = mu * sk / ((float)DK * ldf(r, row));
-}
-
-template <class E, int DK, bool APC>
-__global__ __launch_bounds__(64) void iso_summary_kernel(
-    const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
-    const E* __restrict__ r, ChunkMap cm, int H, float mu, float4* __restrict__ summ)
-{
-    const int g = (int)(blockIdx.x % (unsigned)cm.maxch);
-    const int h = (int)(blockIdx.x / (unsigned)cm.maxch), lane = threadIdx.x;
-    int n, c0, c1;
-    bool last;
-    if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
-    Mat2 x = {1.f, 0.f, 0.f, 1.f};
-    if (c0 + lane < c1) {
-        float a, w, u, nk;
-        iso_coeffs<E, DK, APC>(k, alpha, omega, r, (size_t)(c0 + lane) * H + h, mu, a, w, u, nk);
-        x = token_mat(a, w, u);
-    }
+    constexpr int CPL = DK >= 64 ? DK / 64 : 1, G = 8;
+    typedef typename Lanes<E, CPL>::T VT;
+    typedef RowIO<sizeof(VT)> IO;
+    const bool act = lane * CPL < DK;
+    const uint32_t lo = (act ? lane * CPL : 0) * sizeof(E);
+    struct Buf {
+        VT k[G], a[APC ? G : 1];
+    };
+    auto load = [&](Buf& b, int j0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {  // tree product over the lanes, later on the left
-        Mat2 y;
-        y.a = __shfl_down(x.a, off, 64);
-        y.b = __shfl_down(x.b, off, 64);
-        y.c = __shfl_down(x.c, off, 64);
-        y.d = __shfl_down(x.d, off, 64);
-        if ((lane & (2 * off - 1)) == 0) x = mul(y, x);
+        for (int jj = 0; jj < G; ++jj) {
+            const size_t row = (size_t)(c0 + min(j0 + jj, L - 1)) * H + h;
+            b.k[jj] = IO::template load<VT>(row_rsrc(k + row * DK, DK * sizeof(E)), lo);
+            if constexpr (APC)
+                b.a[jj] = IO::template load<VT>(row_rsrc(alpha + row * DK, DK * sizeof(E)), lo);
+        }
+    };
+    auto sums = [&](const Buf& b, int j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int jj = 0; jj < G; ++jj) {
+            if (j0 + jj >= L) break;
+            float s = 0.f, t = 0.f;
+#pragma unroll
+            for (int i = 0; i < CPL; ++i) {
+                const float kk = lane_el(b.k[jj], i);
+                s = fmaf(kk, kk, s);
+                if constexpr (APC) {
+                    const float al = lane_el(b.a[jj], i);
+                    t = fmaf(al, al, t);
+                }
+            }
+            s = wave_sum(act ? s : 0.f);
+            if (lane == j0 + jj) nk = s;
+            if constexpr (APC) {
+                t = wave_sum(act ? t : 0.f);
+                if (lane == j0 + jj) sa = t;
+            }
+        }
+    };
+    nk = 0.f;
+    sa = 0.f;
+    Buf ba, bb;
+    load(ba, 0);
+    for (int j0 = 0; j0 < L; j0 += 2 * G) {
+        if (j0 + G < L) load(bb, j0 + G);
+        sums(ba, j0);
+        if (j0 + G >= L) break;
+        if (j0 + 2 * G < L) load(ba, j0 + 2 * G);
+        sums(bb, j0 + G);
     }
-    if (lane == 0) summ[(size_t)g * H + h] = make_float4(x.a, x.b, x.c, x.d);
 }
 
+// Pass 3 of the isotropic chain (pass 1 is the forward's summary kernel): lane t holds token t
+// of the chunk; its coefficients a = mean_i alpha_i^2 (or alpha^2), w = omega,
+// u = mu ||k||^2 / (dk r) (eq. iso-kla-box-mobius), the inclusive prefix of the token matrices
+// across the lanes, the state before the token from the carry, and
+// beta_t = b_hat_t / (r_t + b_hat_t ||k_t||^2) (eq. chunk-gain-emission).
 template <class E, int DK, bool APC>
 __global__ __launch_bounds__(64) void iso_emit_kernel(
     const E* __restrict__ k, const E* __restrict__ alpha, const E* __restrict__ omega,
@@ -287,8 +296,20 @@ __global__ __launch_bounds__(64) void iso_emit_kernel(
     if (!locate_chunk<CG>(cm, g, n, c0, c1, last)) return;
     const bool valid = c0 + lane < c1;
     const size_t row = (size_t)(c0 + lane) * H + h;
+    float nks, sas;
+    iso_row_sums<E, DK, APC>(k, alpha, c0, c1 - c0, H, h, lane, nks, sas);
     float a = 1.f, w = 0.f, u = 0.f, nk = 0.f;
-    if (valid) iso_coeffs<E, DK, APC>(k, alpha, omega, r, row, mu, a, w, u, nk);
+    if (valid) {
+        if (APC) {
+            a = sas / (float)DK;
+        } else {
+            const float al = ldf(alpha, row);
+            a = al * al;
+        }
+        w = ldf(omega, row);
+        nk = nks;
+        u = mu * nks / ((float)DK * ldf(r, row));
+    }
     Mat2 x = token_mat(a, w, u);
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {  // inclusive prefix within the chunk
@@ -336,26 +357,25 @@ hipError_t launch_gain_t(int variant, const void* k, const void* alpha, const vo
         return e;
     // one workgroup per (chunk, head), h * maxch + g in a 1-D grid (chunks of a head adjacent)
     const dim3 grid((unsigned)((size_t)maxch * sa.H));
-    if (variant == 0) {
-        // the forward's summary kernel: four waves per (chunk, head), each with its 16 tokens'
-        // loads in flight at once, the four block products composed in LDS
-        fwd::InArgs in = {};
-        in.q = k; in.k = k; in.alpha = alpha; in.omega = omega; in.r = r;
-        const size_t ntok = (size_t)sa.B * sa.T * sa.H;
-        in.bytes_k = (uint32_t)(ntok * DK * sizeof(E));
-        in.bytes_h = (uint32_t)(ntok * sizeof(E));
-        in.H = sa.H;
-        in.mu = mu;
-        hipLaunchKernelGGL((fwd::summary_kernel<E, fwd::VarCfg<E, DK, 0, true>>),
-                           dim3((unsigned)((size_t)maxch * sa.H)), dim3(fwd::NTH), 0, st, in, cm,
-                           summ);
-    } else if (apc) {
-        hipLaunchKernelGGL((iso_summary_kernel<E, DK, true>), grid, dim3(64), 0, st, k_, a_, w_,
-                           r_, cm, sa.H, mu, summ);
-    } else {
-        hipLaunchKernelGGL((iso_summary_kernel<E, DK, false>), grid, dim3(64), 0, st, k_, a_,
-                           w_, r_, cm, sa.H, mu, summ);
-    }
+    // pass 1: the forward's summary kernel, four waves per (chunk, head), each with its 16
+    // tokens' loads in flight at once, the four block products composed in LDS
+    fwd::InArgs in = {};
+    in.q = k; in.k = k; in.alpha = alpha; in.omega = omega; in.r = r;
+    const size_t ntok = (size_t)sa.B * sa.T * sa.H;
+    in.bytes_k = (uint32_t)(ntok * DK * sizeof(E));
+    in.bytes_h = (uint32_t)(ntok * sizeof(E));
+    in.H = sa.H;
+    in.mu = mu;
+    const dim3 cgrid((unsigned)((size_t)maxch * sa.H));
+    if (variant == 0)
+        hipLaunchKernelGGL((fwd::summary_kernel<E, fwd::VarCfg<E, DK, 0, true>>), cgrid,
+                           dim3(fwd::NTH), 0, st, in, cm, summ);
+    else if (apc)
+        hipLaunchKernelGGL((fwd::summary_kernel<E, fwd::VarCfg<E, DK, 1, true>>), cgrid,
+                           dim3(fwd::NTH), 0, st, in, cm, summ);
+    else
+        hipLaunchKernelGGL((fwd::summary_kernel<E, fwd::VarCfg<E, DK, 1, false>>), cgrid,
+                           dim3(fwd::NTH), 0, st, in, cm, summ);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = launch_carry_scan(summ, P0, cm, CG, sa.H, nchan, carry, P_T, st)) != hipSuccess)
         return e;
