@@ -201,23 +201,34 @@ __device__ __forceinline__ void load_seg(SegIn<TI, CF, WQ>& in, const Src& sr, u
 struct TokIn {
     float2 K, Q, A, W;
 };
+template <class P2> __device__ __forceinline__ P2 pair_of_ones();
+template <> __device__ __forceinline__ unsigned pair_of_ones<unsigned>() { return 0x3F803F80u; }
+template <> __device__ __forceinline__ float2 pair_of_ones<float2>()
+{
+    return make_float2(1.f, 1.f);
+}
+
 template <bool MK, class TI, class CF, bool WQ>
 __device__ __forceinline__ TokIn tok_in(const SegIn<TI, CF, WQ>& in, int j, int Lw)
 {
+    using P2 = typename CF::P2;
     const bool pad = MK && j >= Lw;
     const float2 z = make_float2(0.f, 0.f);
+    // the selects act on the stored pair (one register for two bf16 channels); a pair of zeros
+    // or ones unpacks exactly
+    const P2 zero2 = P2{}, one2 = pair_of_ones<P2>();
     TokIn r;
-    r.K = pad ? z : unpack2(in.kk[j]);
-    if constexpr (WQ) r.Q = pad ? z : unpack2(in.qq[j]);
+    r.K = unpack2(pad ? zero2 : in.kk[j]);
+    if constexpr (WQ) r.Q = unpack2(pad ? zero2 : in.qq[j]);
     else r.Q = z;
     if constexpr (CF::APC) {
-        r.A = pad ? make_float2(1.f, 1.f) : unpack2(in.al[j]);
+        r.A = unpack2(pad ? one2 : in.al[j]);
     } else {
         const float as = pad ? 1.f : Raw1<TI>::f32(in.als[CF::APC ? 0 : j]);
         r.A = make_float2(as, as);
     }
     if constexpr (CF::DIAG) {
-        r.W = pad ? z : unpack2(in.ww[j]);
+        r.W = unpack2(pad ? zero2 : in.ww[j]);
     } else {
         const float w = pad ? 0.f : Raw1<TI>::f32(in.ws[CF::DIAG ? 0 : j]);
         r.W = make_float2(w, w);
