@@ -12,7 +12,9 @@ the per-kernel duration statistics come from the same trace.
 The per-dispatch FETCH_SIZE and WRITE_SIZE counters (KiB) of every kernel of a unit are summed
 per unit, and the same two counters of a plain device copy of N bytes give each counter's scale
 on this device (bytes moved / counter bytes); a unit's HBM traffic is its counters times those
-scales. Optional --sq directories hold further counter runs (SQ_* and the like), reported per
+scales; each kernel's counted bytes over its average duration give its achieved bandwidth
+(FETCH_SIZE counts what leaves the L2 for the memory fabric, last-level cache hits included, so
+this bounds the HBM rate from above). Optional --sq directories hold further counter runs (SQ_* and the like), reported per
 kernel as averages per dispatch. Writes profiles/NAME.md (with the commands that produced the
 data) and profiles/NAME.json (read by bench.py, together with the hash of the kernel sources it
 describes).
@@ -29,6 +31,7 @@ import json
 import os
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 CSRC = os.path.join(ROOT, "paper_2609_07816_amd", "csrc")
 
 
@@ -201,10 +204,14 @@ def main():
     cmds = open(args.commands).read().strip()
     gb = 1e9
     order = sorted(stats.items(), key=lambda kv: -kv[1]["avg_ns"] * kv[1]["calls"])
+    def moved(k, v):  # the kernel's counted bytes over its average duration, and of 8 TB/s
+        gbs = (fkk.get(k, 0) * f_scale + wkk.get(k, 0) * w_scale) * 1024 / v["avg_ns"]
+        return f"{gbs:.0f} GB/s ({gbs / HBM_PEAK_GBS:.2f})"
+
     krows = "\n".join(
         f"| {k} | {v['calls']} | {v['avg_ns'] / 1e3:.1f} us | {v['min_ns'] / 1e3:.1f} us | "
         f"{v['max_ns'] / 1e3:.1f} us | {fkk.get(k, 0) * f_scale * 1024 / gb:.4f} GB | "
-        f"{wkk.get(k, 0) * w_scale * 1024 / gb:.4f} GB |" for k, v in order)
+        f"{wkk.get(k, 0) * w_scale * 1024 / gb:.4f} GB | {moved(k, v)} |" for k, v in order)
     sq_md = ""
     if sq:
         names = sorted({c for d in sq.values() for c in d})
@@ -225,8 +232,8 @@ Kernel source sha256 ({', '.join(sources) if sources else 'all of csrc/'}):
 Average span of {len(steady)} units (first dispatch start to last dispatch end, the first unit of
 the run excluded): **{span_ns / 1e3:.1f} us**.
 
-| kernel | dispatches | average | min | max | HBM read / dispatch | HBM write / dispatch |
-|---|---|---|---|---|---|---|
+| kernel | dispatches | average | min | max | HBM read / dispatch | HBM write / dispatch | read + write / average (of 8 TB/s) |
+|---|---|---|---|---|---|---|---|
 {krows}
 
 ## HBM bytes per unit (rocprofv3 --pmc, one counter per run)
