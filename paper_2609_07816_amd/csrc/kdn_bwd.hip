@@ -268,8 +268,8 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
                 const float ph = al * al * p + s_wp[t * LDK + tid];
                 phat[t * DK + tid] = ph;
                 s_wp[t * LDK + tid] = ph;
-                const float u = a.mu * kk * kk / s_r[t];
-                p = ph / (1.f + u * ph);
+                const float u = a.mu * kk * kk * __builtin_amdgcn_rcpf(s_r[t]);
+                p = ph * __builtin_amdgcn_rcpf(fmaf(u, ph, 1.f));
             }
         }
     } else {
@@ -346,7 +346,8 @@ __global__ __launch_bounds__(NTB) void bw_prep(Args a)
         for (int u = 0; u < 8; ++u) {
             const int i = i8 + u;
             const float kk = s_k[t * LDK + i];
-            const float kp = DIAG ? s_wp[t * LDK + i] * kk / s_den[t] : s_beta[t] * kk;
+            const float kp = DIAG ? s_wp[t * LDK + i] * kk * __builtin_amdgcn_rcpf(s_den[t])
+                                  : s_beta[t] * kk;
             const double lm = lam[e + u];
             const float gm = expf((float)lm);
             kpx[u] = kp;
@@ -1334,7 +1335,7 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int t = 16 * rb + 4 * lg + r;
-            dal[t * DK + i] = t < L ? (suf[k][r] + off) / alv[k][r] : 0.f;
+            dal[t * DK + i] = t < L ? (suf[k][r] + off) * __builtin_amdgcn_rcpf(alv[k][r]) : 0.f;
         }
         if constexpr (DIAG) {
             float av[4], bv[4];
@@ -1342,12 +1343,15 @@ __global__ __launch_bounds__(NTB) void bw_grad(Args a)
             for (int r = 0; r < 4; ++r) {
                 const int t = 16 * rb + 4 * lg + r;
                 const bool ok = t < L;
-                const float rr = rrv[r], dn = dnv[r];
-                const float dden = -(s_rp[0 * C + t] + s_rp[3 * C + t]) / dn;
+                // 1 / r_t, 1 / den_t and 1 / (1 + u p_hat): hardware reciprocals (1 ulp)
+                const float irr = __builtin_amdgcn_rcpf(rrv[r]);
+                const float idn = __builtin_amdgcn_rcpf(dnv[r]);
+                const float dden = -(s_rp[0 * C + t] + s_rp[3 * C + t]) * idn;
                 const float kv = kvv[k][r], al = alv[k][r];
-                const float u = a.mu * kv * kv / rr, gg = 1.f + u * phv[k][r];
-                const float c = gpa[k][r] * kv / dn + dden * kv * kv;
-                av[r] = ok ? al * al / (gg * gg) : 1.f;
+                const float u = a.mu * kv * kv * irr;
+                const float ig = __builtin_amdgcn_rcpf(fmaf(u, phv[k][r], 1.f));
+                const float c = gpa[k][r] * kv * idn + dden * kv * kv;
+                av[r] = ok ? al * al * ig * ig : 1.f;
                 bv[r] = ok ? al * al * c : 0.f;
                 a.acf[(gh * C + t) * NCHAN + i] = av[r];
                 a.bcf[(gh * C + t) * NCHAN + i] = bv[r];
@@ -1514,6 +1518,9 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
         const size_t row = (size_t)(c0 + t) * H + h;
         const float rr = ld<TI>(a.r, row), dn = den[t], aux = a.aux[gh * C + t];
         if constexpr (DIAG) {
+            // 1 / r_t and 1 / den_t once per token, 1 / (1 + u p_hat) per channel: hardware
+            // reciprocals (1 ulp)
+            const float irr = __builtin_amdgcn_rcpf(rr), idn = __builtin_amdgcn_rcpf(dn);
             const float dden = aux;
             float s2 = 0.f;
 #pragma unroll
@@ -1524,16 +1531,18 @@ __global__ __launch_bounds__(NTH) void bw_final(Args a)
                 const float ph = phat[t * DK + i], pp = pprv[t * DK + i];
                 const float dkp = dkap[t * DK + i];
                 const float lp = s_lp[t * NCHAN + i];
-                const float u = mu * kk * kk / rr, gg = 1.f + u * ph, ig2 = 1.f / (gg * gg);
-                const float dph = dkp * kk / dn + dden * kk * kk + lp * ig2;
+                const float u = mu * kk * kk * irr;
+                const float ig = __builtin_amdgcn_rcpf(fmaf(u, ph, 1.f)), ig2 = ig * ig;
+                const float dph = dkp * kk * idn + dden * kk * kk + lp * ig2;
                 const float du = -lp * ph * ph * ig2;
-                a.dk[row * DK + i] += dkp * ph / dn + 2.f * dden * ph * kk + du * 2.f * mu * kk / rr;
+                a.dk[row * DK + i] +=
+                    dkp * ph * idn + 2.f * dden * ph * kk + du * 2.f * mu * kk * irr;
                 s2 += du * mu * kk * kk;
                 a.dalpha[row * DK + i] = dal[t * DK + i] + dph * 2.f * al * pp;
                 a.domega[row * DK + i] = dph;
             }
             s2 = wave_sum(s2);
-            if (lane == 0) a.dr[row] = dden - s2 / (rr * rr);
+            if (lane == 0) a.dr[row] = dden - s2 * irr * irr;
         } else {
             const float dbeta = aux, bh = phat[t * DK], pp = pprv[t * DK];
             const float lp = s_lp[t];
