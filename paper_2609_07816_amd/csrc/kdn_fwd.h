@@ -607,7 +607,7 @@ __device__ __forceinline__ void prep_body(const PrepArgs& a)
             }
         } else {
             const float nn = fmaf(ka[j], n0, Wf[j].x * d0);  // b_hat d
-            const float beta = nn / fmaf(d0, s_r[t], nn * kn[j]);
+            const float beta = nn * __builtin_amdgcn_rcpf(fmaf(d0, s_r[t], nn * kn[j]));
             pk[j] = make_float2(beta * Kf[j].x, beta * Kf[j].y);
             if constexpr (LAYER) {
                 if (a.in.beta_eff && lane == 0 && j < Lw)  // k^T (beta k)
