@@ -13,10 +13,11 @@
 //   3. replay of every chunk from its carry, emitting p_hat and the gain before each token's
 //      matrix is applied (eqs. chunk-gain-local-prefix, chunk-gain-emission).
 // Every product is rescaled by an exact power of two, which leaves n / d unchanged.
-// The diagonal chain takes the forward's chunk summaries (pass 1) and gives every (chunk, head)
-// one wavefront for the emission, its lanes holding the channels (channels are independent; the
-// gain's normalisation sums them across the wavefront); the isotropic chain gives every token a
-// lane and scans inside the wavefront.
+// Pass 1 is the forward's summary kernel and pass 2 the shared carry scan. Pass 3 gives every
+// (chunk, head) one wavefront whose lanes hold the channels and read the chunk's rows eight
+// tokens ahead: the diagonal chain replays each channel on its lane and sums the gain's
+// normalisation across the wavefront; the isotropic chain sums ||k||^2 (and alpha^2) across the
+// wavefront per token, hands token t's sums to lane t and scans the chunk inside the wavefront.
 #include "kdn_device.h"
 #include "kdn_fwd.h"
 
