@@ -18,6 +18,10 @@ steps, the gain scan alone, the backward, the layer forward with its maps fused)
 way (decode: events around every call, whose host side would otherwise set the pace).
 The larger workloads draw their inputs on the GPU with the same laws (timing only; their parity
 is checked by the tests on host-drawn inputs).
+
+The default warmup is 200 untimed forward calls (about 60 ms): the GPU raises its clocks only
+after some tens of milliseconds of load, and five warmup calls leave the timed steps about 9%
+slower than the same calls at steady clocks.
 """
 
 from __future__ import annotations
@@ -119,17 +123,23 @@ def gpu_inputs(torch, variant, B, T, H, dk, dv, seed, apc=True, random_state=Fal
 NAMES = ("q", "k", "v", "alpha", "omega", "r")
 
 
-def time_calls(torch, fn, steps, warmup, per_call=False, reps=5):
+def time_calls(torch, fn, steps, warmup, per_call=False, reps=5, warm_s=0.1):
     """Milliseconds per call on torch's current stream (the stream the binding passes to the
     library; every kernel of a call runs on it).
 
-    Default: `reps` regions of `steps` back-to-back calls, HIP events around each region; one
+    Untimed calls first: `warmup` of them, and more until `warm_s` seconds of GPU work have
+    passed (the GPU's clocks rise only after some tens of milliseconds of load). Then by
+    default `reps` regions of `steps` back-to-back calls, HIP events around each region; one
     value (region time / steps) per region. per_call=True: events around every call instead,
     one value per call (for calls short enough that the host, not the GPU, would set the pace
     of back-to-back calls; each pair of timing events adds a few microseconds of its own)."""
     stream = torch.cuda.current_stream()
-    for _ in range(warmup):
+    t0, n = time.perf_counter(), 0
+    while n < warmup or time.perf_counter() - t0 < warm_s:
         fn()
+        n += 1
+        if n % 16 == 0:
+            torch.cuda.synchronize()  # the host's clock follows the GPU's progress
     torch.cuda.synchronize()
     if per_call:
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -223,6 +233,11 @@ def bench_varlen(torch, kdn, W, steps):
                     "kernels": FORWARD_KERNELS})
 
 
+# decode steps before each decode variant's 64 timed steps: a fixed count (about 0.1 s of
+# steps), so that the timed steps keep fixed positions in a profiler's trace
+DECODE_WARMUP = 1200
+
+
 def bench_decode_workload(torch, kdn, steps):
     """Workload 4: B256 T1024 prefill of every row (diagonal, bf16), then decode steps of both
     variants on 256 rows; also the diagonal step on a pool of 1024 slots (4x the state the
@@ -242,7 +257,8 @@ def bench_decode_workload(torch, kdn, steps):
         args = [st[n][:, 0].contiguous() for n in NAMES]
         S, P = st["S0"], st["P0"]
         ms = time_calls(torch, lambda: kdn.decode_step(variant, *args, S, P, mu=float(d),
-                                                       scale=d ** -0.5), 64, 5, per_call=True)
+                                                       scale=d ** -0.5), 64, DECODE_WARMUP,
+                        per_call=True, warm_s=0.0)
         out[f"decode_{variant}"] = summary(
             ms, decode_bytes(R, H, d, d, 2, variant), R,
             {"workload": f"{variant}-decode-R256-H16-d128 (state pool of 256 slots, 256 MiB)",
@@ -252,7 +268,8 @@ def bench_decode_workload(torch, kdn, steps):
     slots = torch.arange(0, 4 * R, 4, dtype=torch.int32, device="cuda")
     ms = time_calls(torch, lambda: kdn.decode_step("diag", *args, st["S0"], st["P0"],
                                                    slot_idx=slots, mu=float(d),
-                                                   scale=d ** -0.5), 64, 5, per_call=True)
+                                                   scale=d ** -0.5), 64, DECODE_WARMUP,
+                    per_call=True, warm_s=0.0)
     out["decode_diag_pool1024"] = summary(
         ms, decode_bytes(R, H, d, d, 2, "diag"), R,
         {"workload": "diag-decode-R256-H16-d128, rows on every fourth slot of a 1024-slot pool "
@@ -427,7 +444,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--only", default="all",

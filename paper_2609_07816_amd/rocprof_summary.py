@@ -158,15 +158,19 @@ def main():
     ap.add_argument("--copy-bytes", type=int, required=True)
     ap.add_argument("--algorithmic-bytes", type=int, required=True)
     ap.add_argument("--sq", nargs="*", default=[])
-    ap.add_argument("--window", default="", help="a:b, keep units a..b-1 of the run (after "
-                    "which the first kept unit is still dropped as a warm-up)")
+    ap.add_argument("--window", default="", help="a:b as a python slice of the run's units "
+                    "(negative counts from the end; the first kept unit is still dropped as a "
+                    "warm-up)")
     ap.add_argument("--notes", default="", help="text file appended to the summary")
     ap.add_argument("--commands", required=True, help="text file with the commands that ran")
     ap.add_argument("--sources", default="", help="comma-separated csrc/ files that define and "
                     "launch the measured kernels (default: all of csrc/)")
     args = ap.parse_args()
 
-    window = tuple(int(v) for v in args.window.split(":")) if args.window else None
+    window = None
+    if args.window:  # python slice bounds: "a:b", "-n:" (the last n units), "-n:-1"
+        a, b = args.window.split(":")
+        window = (int(a) if a else None, int(b) if b else None)
     units = Units(args.unit_kernels.split(","), args.first_kernel, window)
     groups = trace_units(args.trace, units)
     steady = groups[1:] if len(groups) > 1 else groups  # the first unit pays first-use costs
